@@ -1,0 +1,219 @@
+/*
+ * tgvkv.h -- C ABI of libtgvkv, the MI355X (gfx950) implementation of the
+ * post-prefill KV eviction pass of TGV-KV ("Text-Grounded KV Eviction for
+ * Vision-Language Models") and of single-query decode attention over the
+ * pruned, per-layer ragged cache it produces.
+ *
+ * The pass runs once after prefill (Sec. 3.3):
+ *   tgvkv_score   Text-Weighted Ranking scores and per-layer text->vision mass
+ *                 (Eq. (2), (6)-(9));
+ *   tgvkv_budget  Text-Vision Budgeting: integer per-layer budgets (Eq. (5)-(6));
+ *   tgvkv_select  Text-Prioritised Retention: retained positions (Eq. (10));
+ *   tgvkv_compact gather of the retained K/V rows into a ragged cache;
+ * then every decode step appends one key/value and attends (Eq. (3)-(4)):
+ *   tgvkv_decode_attn.
+ *
+ * Conventions shared by every call
+ *  - Token layout of each sequence: n_sys system-text tokens, then n_vis vision
+ *    tokens, then n_qst question-text tokens; N = n_sys + n_vis + n_qst.  The
+ *    text set T (Eq. (10)) is positions [0, n_sys) U [n_sys + n_vis, N), in
+ *    "text order" (system rows first); the vision set V is [n_sys, n_sys + n_vis).
+ *  - All tensors are row-major, contiguous, device memory owned by the caller,
+ *    16-byte aligned.  bf16 tensors are passed as raw 16-bit patterns.
+ *  - Every call validates its arguments on the host before any HIP call; an
+ *    invalid call returns a negative status and launches nothing.  Kernels are
+ *    enqueued asynchronously on `stream`; the library never allocates, frees or
+ *    synchronises, and keeps no pointer after a call returns.  A launch failure
+ *    returns TGVKV_E_HIP.  Calls are thread-safe (no global mutable state).
+ *  - Query head h reads KV head h / (heads_q / heads_kv).
+ *  - "groups" g: 1 when opts.head_mode == 0 (one retained set per sequence and
+ *    layer, from attention averaged over all query heads), heads_kv when
+ *    head_mode == 1 (one retained set per KV head, from the mean over the query
+ *    heads sharing it).
+ */
+#ifndef TGVKV_H
+#define TGVKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TGVKV_ABI_VERSION 1
+
+typedef enum tgvkv_status {
+    TGVKV_OK = 0,
+    TGVKV_E_INVAL = -1,        /* null pointer, negative size, inconsistent shape or option   */
+    TGVKV_E_UNSUPPORTED = -2,  /* valid, but outside what these kernels implement (head_dim,
+                                  sizes beyond the documented limits)                          */
+    TGVKV_E_WORKSPACE = -3,    /* workspace missing or smaller than tgvkv_workspace_size()    */
+    TGVKV_E_CAPACITY = -4,     /* budget above L*N, or decode step outside the reserve        */
+    TGVKV_E_HIP = -5           /* a kernel launch failed                                      */
+} tgvkv_status;
+
+/* Shape of one batch of prefills.  head_dim must be 64 or 128.  Limits
+ * (TGVKV_E_UNSUPPORTED beyond them): layers <= 512, N <= 2^24,
+ * heads_q / heads_kv <= 16, and the text rows one KV head scores,
+ * (heads_q / heads_kv) * (n_sys + n_qst), at most 16384.  heads_q must be a
+ * multiple of heads_kv; every count is >= 0 and N >= 1 (TGVKV_E_INVAL). */
+typedef struct tgvkv_problem {
+    int32_t batch;
+    int32_t layers;
+    int32_t heads_q;
+    int32_t heads_kv;
+    int32_t head_dim;
+    int32_t n_sys;
+    int32_t n_vis;
+    int32_t n_qst;
+} tgvkv_problem;
+
+/* Options.  Passing NULL selects the defaults {0, 0, 0, 0}. */
+typedef struct tgvkv_opts {
+    float   sm_scale;   /* logit scale; <= 0 selects 1/sqrt(head_dim)                        */
+    int32_t head_mode;  /* 0: per-layer retained set (paper); 1: per-KV-head retained sets   */
+    int32_t n_sink;     /* first n_sink positions are always kept (App. A.2 keeps 4)          */
+    int32_t n_recent;   /* last n_recent positions are always kept (App. A.2 keeps 1)         */
+} tgvkv_opts;
+
+/* Score phases (bit mask for tgvkv_score). */
+enum {
+    TGVKV_SCORE_STATS  = 1,  /* question-row softmax statistics over all visible keys        */
+    TGVKV_SCORE_TEXT   = 2,  /* text scores s^T, weights w~, per-layer text->vision mass      */
+    TGVKV_SCORE_VISION = 4,  /* text-weighted vision scores s^V                               */
+    TGVKV_SCORE_ALL    = 7
+};
+
+/* Which call a workspace is sized for. */
+enum { TGVKV_CALL_SCORE = 0, TGVKV_CALL_DECODE = 1 };
+
+/*
+ * tgvkv_score -- TWR scores and TVB masses of every (sequence, layer).
+ *
+ * Rows of the causal softmax A = softmax(tau Q K^T + M) of Eq. (2) whose queries
+ * are text tokens, tau = sm_scale.  Let Abar be A averaged over the query heads
+ * of a group.  Then, per group:
+ *   s_txt[j] = sum_{i >= j} Abar[i, pi(j)]                       (Eq. (9))
+ *   w_j      = s_txt[j] / (N_t - j),  w_txt = w / sum(w)         (Eq. (7))
+ *   s_vis[j] = sum_i w_txt[i] Abar[i, n_sys + j]                  (Eq. (8))
+ * and per layer (always the mean over all query heads)
+ *   tv_mass  = sum_{i in T, j in V} Abar[i, j]                    (Eq. (5)-(6)).
+ *
+ * q_text  bf16 [B][L][heads_q][N_t][head_dim]   text-row queries, text order
+ * k       bf16 [B][L][heads_kv][N][head_dim]    cached keys (after any positional encoding)
+ * lse     f32  [B][L][heads_q][N_t]  out: natural log-sum-exp of each text row's scaled logits
+ * s_txt   f32  [B][L][g][N_t]        out
+ * w_txt   f32  [B][L][g][N_t]        out (normalised weights; all 0 if sum(w) == 0)
+ * tv_mass f32  [B][L]                out
+ * s_vis   f32  [B][L][g][n_vis]      out
+ * budgets_or_null  int32 [B][L]: if given, the VISION phase skips every layer
+ *                  whose budget leaves no room for vision tokens (budget <=
+ *                  |forced U T|); s_vis of skipped layers is left untouched.
+ * phases  any non-empty OR of TGVKV_SCORE_*.  Phases must run in the order
+ *         STATS, TEXT, VISION, with the same workspace and outputs; a later
+ *         phase reads what the earlier ones left there.  Pointers of phases
+ *         not requested may be NULL (lse is needed by all three, w_txt by VISION).
+ * workspace / workspace_bytes  >= tgvkv_workspace_size(p, o, TGVKV_CALL_SCORE).
+ */
+tgvkv_status tgvkv_score(const tgvkv_problem* problem, const tgvkv_opts* opts, int32_t phases,
+                         const void* q_text, const void* k,
+                         float* lse, float* s_txt, float* w_txt, float* tv_mass, float* s_vis,
+                         const int32_t* budgets_or_null,
+                         void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * tgvkv_budget -- TVB: integer budgets b_l of every layer of every sequence.
+ *
+ * Eq. (5)-(6) give layer l the share m_l / sum_l' m_l' of the sequence budget.
+ * Counts: a floor F = min(|forced|, total/L, N) per layer first; the rest
+ * R = total - L*F water-filled in proportion to the shares with each layer
+ * capped at N - F (uniform shares if all masses are 0; non-finite or negative
+ * masses count as 0); then largest-remainder rounding with ties to the lower
+ * layer.  float64 throughout.  sum_l b_l == total for every sequence.
+ *
+ * tv_mass        f32   [B][L]     per-layer masses (from tgvkv_score)
+ * total_budget   per-sequence budget B_tot (e.g. round(rho * N * L)), 0 <= B_tot <= L*N
+ * decode_reserve token slots reserved after each layer's retained tokens for decode (>= 0)
+ * budgets        int32 [B][L]     out
+ * idx_offsets    int64 [B*L + 1]  out: start of each (b, l) block of tgvkv_select's output,
+ *                                 block size g * b_l; idx_offsets[B*L] = B * B_tot * g
+ * seg_offsets    int64 [B*L + 1]  out: start of each (b, l) cache segment, in units of
+ *                                 heads_kv * head_dim elements; segment size b_l + reserve;
+ *                                 seg_offsets[B*L] = B * (B_tot + L * reserve)
+ */
+tgvkv_status tgvkv_budget(const tgvkv_problem* problem, const tgvkv_opts* opts,
+                          const float* tv_mass, int64_t total_budget, int32_t decode_reserve,
+                          int32_t* budgets, int64_t* idx_offsets, int64_t* seg_offsets,
+                          hipStream_t stream);
+
+/*
+ * tgvkv_select -- TPR: retained positions of every (sequence, layer, group), Eq. (10).
+ *
+ * Forced positions (first n_sink, last n_recent) first; then, if b_l minus the
+ * forced count is at most the remaining text count, the top text tokens by
+ * s_txt, else all text and the top vision tokens by s_vis.  With no forced
+ * tokens this is exactly Eq. (10).  Ties go to the lower position; -0.0 equals
+ * +0.0; scores must not be NaN.  Positions are written in ascending order:
+ * idx[idx_offsets[b*L + l] + gi * b_l + n], n < b_l.
+ *
+ * s_vis  f32 [B][L][g][n_vis]; s_txt f32 [B][L][g][N_t]; budgets, idx_offsets from tgvkv_budget.
+ * idx    int32 out, idx_offsets[B*L] entries.
+ */
+tgvkv_status tgvkv_select(const tgvkv_problem* problem, const tgvkv_opts* opts,
+                          const float* s_vis, const float* s_txt, const int32_t* budgets,
+                          const int64_t* idx_offsets, int32_t* idx, hipStream_t stream);
+
+/*
+ * tgvkv_compact -- gather the retained K/V rows into the ragged per-layer cache.
+ *
+ * The cache of Sec. 3.1 (K, V per layer) keeps only the retained tokens, in
+ * ascending position: for every (b, l), KV head h and n < b_l,
+ *   kc[(seg_offsets[b*L+l] * heads_kv + h * cap + n) * head_dim + :] = k[b][l][h][I[n]][:]
+ * with cap = b_l + decode_reserve and I the (group of h's) retained set.  Same for v.
+ * Bit-exact copy.  Slots b_l .. cap-1 are left for tgvkv_decode_attn.
+ * total_budget / decode_reserve: the values given to tgvkv_budget (they size the
+ * launch on the host: B * total_budget rows per KV head are moved).
+ * kc, vc  bf16, seg_offsets[B*L] * heads_kv * head_dim elements each.
+ */
+tgvkv_status tgvkv_compact(const tgvkv_problem* problem, const tgvkv_opts* opts,
+                           const void* k, const void* v, const int32_t* idx,
+                           const int32_t* budgets, const int64_t* idx_offsets,
+                           const int64_t* seg_offsets, int64_t total_budget, int32_t decode_reserve,
+                           void* kc, void* vc, hipStream_t stream);
+
+/*
+ * tgvkv_decode_attn -- one decode step over the pruned cache, Eq. (3)-(4).
+ *
+ * For every (b, l): writes k_new / v_new at slot b_l + step of each KV head's
+ * segment, then for each query head h computes
+ *   out[b][l][h] = softmax_n(tau q[b][l][h] . Kc[n]) Vc[n],  n < b_l + step + 1.
+ * Steps must run in order 0, 1, ... on the same cache; 0 <= step < decode_reserve.
+ *
+ * q      bf16 [B][L][heads_q][head_dim];  k_new, v_new bf16 [B][L][heads_kv][head_dim]
+ * out    f32  [B][L][heads_q][head_dim]
+ * workspace >= tgvkv_workspace_size(p, o, TGVKV_CALL_DECODE) (may be 0 bytes).
+ */
+tgvkv_status tgvkv_decode_attn(const tgvkv_problem* problem, const tgvkv_opts* opts,
+                               void* kc, void* vc, const int32_t* budgets,
+                               const int64_t* seg_offsets, int32_t decode_reserve, int32_t step,
+                               const void* q, const void* k_new, const void* v_new, float* out,
+                               void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Workspace bytes needed by tgvkv_score (which = TGVKV_CALL_SCORE) or
+ * tgvkv_decode_attn (TGVKV_CALL_DECODE); 0 for an invalid problem. */
+size_t tgvkv_workspace_size(const tgvkv_problem* problem, const tgvkv_opts* opts, int32_t which);
+
+/* Static, NUL-terminated description of a status code. */
+const char* tgvkv_status_string(tgvkv_status status);
+
+/* TGVKV_ABI_VERSION of the library. */
+int32_t tgvkv_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TGVKV_H */

@@ -1,0 +1,263 @@
+"""Python binding of libtgvkv: the C ABI of include/tgvkv.h through ctypes.
+
+Argument marshalling only.  Each function takes torch tensors that already live
+in device memory, checks that they are contiguous, on the GPU and of the
+expected element type, passes their addresses and torch's current HIP stream to
+the C entry point of the same name, and raises TgvkvError on a negative status.
+Every step of the computation runs in the library's HIP kernels; there is no
+fallback path.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtgvkv.so")
+
+TGVKV_OK, TGVKV_E_INVAL, TGVKV_E_UNSUPPORTED, TGVKV_E_WORKSPACE, TGVKV_E_CAPACITY, TGVKV_E_HIP = 0, -1, -2, -3, -4, -5
+SCORE_STATS, SCORE_TEXT, SCORE_VISION, SCORE_ALL = 1, 2, 4, 7
+CALL_SCORE, CALL_DECODE = 0, 1
+
+EXPORTS = ("tgvkv_score", "tgvkv_budget", "tgvkv_select", "tgvkv_compact", "tgvkv_decode_attn",
+           "tgvkv_workspace_size", "tgvkv_status_string", "tgvkv_abi_version")
+
+
+class TgvkvProblem(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("layers", ctypes.c_int32), ("heads_q", ctypes.c_int32),
+                ("heads_kv", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("n_sys", ctypes.c_int32),
+                ("n_vis", ctypes.c_int32), ("n_qst", ctypes.c_int32)]
+
+
+class TgvkvOpts(ctypes.Structure):
+    _fields_ = [("sm_scale", ctypes.c_float), ("head_mode", ctypes.c_int32), ("n_sink", ctypes.c_int32),
+                ("n_recent", ctypes.c_int32)]
+
+
+class TgvkvError(RuntimeError):
+    def __init__(self, fn: str, status: int, text: str):
+        super().__init__(f"{fn} failed: status {status} ({text})")
+        self.status = status
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def load_library(path: Optional[str] = None) -> ctypes.CDLL:
+    """Load libtgvkv.so (built in-tree by __graft_entry__.build()); raises if it is missing."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise RuntimeError(f"{p} is not built; run __graft_entry__.build() (hipcc for gfx950)")
+    lib = ctypes.CDLL(p)
+    P = ctypes.POINTER(TgvkvProblem)
+    O = ctypes.POINTER(TgvkvOpts)
+    vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    lib.tgvkv_score.argtypes = [P, O, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.tgvkv_budget.argtypes = [P, O, vp, i64, i32, vp, vp, vp, vp]
+    lib.tgvkv_select.argtypes = [P, O, vp, vp, vp, vp, vp, vp]
+    lib.tgvkv_compact.argtypes = [P, O, vp, vp, vp, vp, vp, vp, i64, i32, vp, vp, vp]
+    lib.tgvkv_decode_attn.argtypes = [P, O, vp, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, sz, vp]
+    lib.tgvkv_workspace_size.argtypes = [P, O, i32]
+    lib.tgvkv_workspace_size.restype = sz
+    lib.tgvkv_status_string.argtypes = [ctypes.c_int]
+    lib.tgvkv_status_string.restype = ctypes.c_char_p
+    lib.tgvkv_abi_version.argtypes = []
+    for name in ("tgvkv_score", "tgvkv_budget", "tgvkv_select", "tgvkv_compact", "tgvkv_decode_attn",
+                 "tgvkv_abi_version"):
+        getattr(lib, name).restype = ctypes.c_int32
+    if path is None:
+        _lib = lib
+    return lib
+
+
+def make_problem(batch, layers, heads_q, heads_kv, head_dim, n_sys, n_vis, n_qst) -> TgvkvProblem:
+    return TgvkvProblem(batch, layers, heads_q, heads_kv, head_dim, n_sys, n_vis, n_qst)
+
+
+def problem_from(cfg) -> TgvkvProblem:
+    """Problem of a workload config (anything with the eight shape attributes)."""
+    return make_problem(cfg.batch, cfg.layers, cfg.heads_q, cfg.heads_kv, cfg.head_dim, cfg.n_sys, cfg.n_vis,
+                        cfg.n_qst)
+
+
+def make_opts(sm_scale: float = 0.0, head_mode: int = 0, n_sink: int = 0, n_recent: int = 0) -> TgvkvOpts:
+    return TgvkvOpts(sm_scale, head_mode, n_sink, n_recent)
+
+
+def status_string(status: int) -> str:
+    return load_library().tgvkv_status_string(status).decode()
+
+
+def _check(fn: str, status: int):
+    if status != TGVKV_OK:
+        raise TgvkvError(fn, status, status_string(status))
+
+
+def _ptr(t, dtypes=None, name="tensor"):
+    if t is None:
+        return None
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be in GPU memory")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtypes is not None and t.dtype not in dtypes:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected one of {dtypes}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _bf16():
+    import torch
+    return (torch.bfloat16, torch.int16)
+
+
+def _f32():
+    import torch
+    return (torch.float32,)
+
+
+def workspace_size(problem: TgvkvProblem, opts: Optional[TgvkvOpts], which: int) -> int:
+    return int(load_library().tgvkv_workspace_size(ctypes.byref(problem), _opts_ref(opts), which))
+
+
+def _opts_ref(opts):
+    return ctypes.byref(opts) if opts is not None else None
+
+
+def tgvkv_score(problem, opts, phases, q_text, k, lse, s_txt, w_txt, tv_mass, s_vis, budgets=None,
+                workspace=None, stream=None):
+    import torch
+    lib = load_library()
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    st = lib.tgvkv_score(ctypes.byref(problem), _opts_ref(opts), int(phases),
+                         _ptr(q_text, _bf16(), "q_text"), _ptr(k, _bf16(), "k"), _ptr(lse, _f32(), "lse"),
+                         _ptr(s_txt, _f32(), "s_txt"), _ptr(w_txt, _f32(), "w_txt"),
+                         _ptr(tv_mass, _f32(), "tv_mass"), _ptr(s_vis, _f32(), "s_vis"),
+                         _ptr(budgets, (torch.int32,), "budgets"), _ptr(workspace, None, "workspace"),
+                         ws_bytes, _stream(stream))
+    _check("tgvkv_score", st)
+
+
+def tgvkv_budget(problem, opts, tv_mass, total_budget, decode_reserve, budgets, idx_offsets, seg_offsets,
+                 stream=None):
+    import torch
+    st = load_library().tgvkv_budget(ctypes.byref(problem), _opts_ref(opts), _ptr(tv_mass, _f32(), "tv_mass"),
+                                     int(total_budget), int(decode_reserve),
+                                     _ptr(budgets, (torch.int32,), "budgets"),
+                                     _ptr(idx_offsets, (torch.int64,), "idx_offsets"),
+                                     _ptr(seg_offsets, (torch.int64,), "seg_offsets"), _stream(stream))
+    _check("tgvkv_budget", st)
+
+
+def tgvkv_select(problem, opts, s_vis, s_txt, budgets, idx_offsets, idx, stream=None):
+    import torch
+    st = load_library().tgvkv_select(ctypes.byref(problem), _opts_ref(opts), _ptr(s_vis, _f32(), "s_vis"),
+                                     _ptr(s_txt, _f32(), "s_txt"), _ptr(budgets, (torch.int32,), "budgets"),
+                                     _ptr(idx_offsets, (torch.int64,), "idx_offsets"),
+                                     _ptr(idx, (torch.int32,), "idx"), _stream(stream))
+    _check("tgvkv_select", st)
+
+
+def tgvkv_compact(problem, opts, k, v, idx, budgets, idx_offsets, seg_offsets, total_budget, decode_reserve,
+                  kc, vc, stream=None):
+    import torch
+    st = load_library().tgvkv_compact(ctypes.byref(problem), _opts_ref(opts), _ptr(k, _bf16(), "k"),
+                                      _ptr(v, _bf16(), "v"), _ptr(idx, (torch.int32,), "idx"),
+                                      _ptr(budgets, (torch.int32,), "budgets"),
+                                      _ptr(idx_offsets, (torch.int64,), "idx_offsets"),
+                                      _ptr(seg_offsets, (torch.int64,), "seg_offsets"), int(total_budget),
+                                      int(decode_reserve), _ptr(kc, _bf16(), "kc"), _ptr(vc, _bf16(), "vc"),
+                                      _stream(stream))
+    _check("tgvkv_compact", st)
+
+
+def tgvkv_decode_attn(problem, opts, kc, vc, budgets, seg_offsets, decode_reserve, step, q, k_new, v_new, out,
+                      workspace=None, stream=None):
+    import torch
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    st = load_library().tgvkv_decode_attn(ctypes.byref(problem), _opts_ref(opts), _ptr(kc, _bf16(), "kc"),
+                                          _ptr(vc, _bf16(), "vc"), _ptr(budgets, (torch.int32,), "budgets"),
+                                          _ptr(seg_offsets, (torch.int64,), "seg_offsets"), int(decode_reserve),
+                                          int(step), _ptr(q, _bf16(), "q"), _ptr(k_new, _bf16(), "k_new"),
+                                          _ptr(v_new, _bf16(), "v_new"), _ptr(out, _f32(), "out"),
+                                          _ptr(workspace, None, "workspace"), ws_bytes, _stream(stream))
+    _check("tgvkv_decode_attn", st)
+
+
+# --------------------------------------------------------------------------- whole-pass helpers
+class EvictionBuffers:
+    """Device buffers of one eviction pass plus decode, allocated once for a problem.
+
+    torch is used only to own device memory; every computation is a library call.
+    """
+
+    def __init__(self, problem: TgvkvProblem, opts: Optional[TgvkvOpts], total_budget: int,
+                 decode_reserve: int, device="cuda"):
+        import torch
+        p = problem
+        self.problem, self.opts = p, opts
+        self.total_budget, self.decode_reserve = int(total_budget), int(decode_reserve)
+        B, L, H, Hkv, D = p.batch, p.layers, p.heads_q, p.heads_kv, p.head_dim
+        Nt, Nv = p.n_sys + p.n_qst, p.n_vis
+        g = 1 if opts is None or opts.head_mode == 0 else Hkv
+        f32 = dict(dtype=torch.float32, device=device)
+        self.lse = torch.empty((B, L, H, Nt), **f32)
+        self.s_txt = torch.empty((B, L, g, Nt), **f32)
+        self.w_txt = torch.empty((B, L, g, Nt), **f32)
+        self.tv_mass = torch.empty((B, L), **f32)
+        self.s_vis = torch.zeros((B, L, g, Nv), **f32)
+        self.budgets = torch.empty((B, L), dtype=torch.int32, device=device)
+        self.idx_offsets = torch.empty((B * L + 1,), dtype=torch.int64, device=device)
+        self.seg_offsets = torch.empty((B * L + 1,), dtype=torch.int64, device=device)
+        self.idx = torch.empty((max(1, B * self.total_budget * g),), dtype=torch.int32, device=device)
+        slots = B * (self.total_budget + L * self.decode_reserve)
+        self.kc = torch.empty((max(1, slots * Hkv * D),), dtype=torch.bfloat16, device=device)
+        self.vc = torch.empty_like(self.kc)
+        self.out = torch.empty((B, L, H, D), **f32)
+        self.ws_score = torch.empty((max(1, workspace_size(p, opts, CALL_SCORE)),), dtype=torch.uint8,
+                                    device=device)
+        self.ws_decode = torch.empty((max(1, workspace_size(p, opts, CALL_DECODE)),), dtype=torch.uint8,
+                                     device=device)
+
+    def score(self, q_text, k, phases=SCORE_ALL, budgets=None, stream=None):
+        tgvkv_score(self.problem, self.opts, phases, q_text, k, self.lse, self.s_txt, self.w_txt, self.tv_mass,
+                    self.s_vis, budgets, self.ws_score, stream)
+
+    def budget(self, stream=None):
+        tgvkv_budget(self.problem, self.opts, self.tv_mass, self.total_budget, self.decode_reserve, self.budgets,
+                     self.idx_offsets, self.seg_offsets, stream)
+
+    def select(self, stream=None):
+        tgvkv_select(self.problem, self.opts, self.s_vis, self.s_txt, self.budgets, self.idx_offsets, self.idx,
+                     stream)
+
+    def compact(self, k, v, stream=None):
+        tgvkv_compact(self.problem, self.opts, k, v, self.idx, self.budgets, self.idx_offsets, self.seg_offsets,
+                      self.total_budget, self.decode_reserve, self.kc, self.vc, stream)
+
+    def evict(self, q_text, k, v, skip_text_only_layers=True, stream=None):
+        """Score (text stats, then budgets, then vision scores only where needed), select, compact."""
+        self.score(q_text, k, SCORE_STATS | SCORE_TEXT, stream=stream)
+        self.budget(stream)
+        self.score(q_text, k, SCORE_VISION, budgets=self.budgets if skip_text_only_layers else None,
+                   stream=stream)
+        self.select(stream)
+        self.compact(k, v, stream)
+
+    def decode(self, step, q, k_new, v_new, stream=None):
+        tgvkv_decode_attn(self.problem, self.opts, self.kc, self.vc, self.budgets, self.seg_offsets,
+                          self.decode_reserve, step, q, k_new, v_new, self.out, self.ws_decode, stream)
+        return self.out

@@ -1,0 +1,260 @@
+// libtgvkv C ABI: argument validation on the host, workspace layout, launches.
+//
+// Every entry point checks its arguments before touching the HIP runtime, so an
+// invalid call returns a negative status and enqueues nothing.
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+
+#include "tgvkv.h"
+#include "tgvkv_shape.h"
+
+using tgvkv::RowPlan;
+using tgvkv::Shape;
+
+namespace {
+
+constexpr int32_t kMaxLayers = 512;
+constexpr int64_t kMaxTokens = int64_t(1) << 24;
+constexpr int64_t kMaxTextRowsPerKvHead = 16384;  // LDS row-normaliser buffer of the text pass
+constexpr int32_t kMaxGroup = 16;                  // query heads per KV head (decode registers)
+constexpr int64_t kMaxBlocks = (int64_t(1) << 31) - 1;
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+tgvkv_status make_shape(const tgvkv_problem* p, const tgvkv_opts* o, Shape* s) {
+    if (p == nullptr || s == nullptr) return TGVKV_E_INVAL;
+    tgvkv_opts d;
+    std::memset(&d, 0, sizeof(d));
+    if (o != nullptr) d = *o;
+    if (p->batch < 0 || p->layers < 1 || p->heads_q < 1 || p->heads_kv < 1 || p->n_sys < 0 || p->n_vis < 0 ||
+        p->n_qst < 0)
+        return TGVKV_E_INVAL;
+    if (p->heads_q % p->heads_kv != 0) return TGVKV_E_INVAL;
+    const int64_t N = (int64_t)p->n_sys + p->n_vis + p->n_qst;
+    if (N < 1) return TGVKV_E_INVAL;
+    if (d.head_mode != 0 && d.head_mode != 1) return TGVKV_E_INVAL;
+    if (d.n_sink < 0 || d.n_recent < 0) return TGVKV_E_INVAL;
+    if (!std::isfinite(d.sm_scale)) return TGVKV_E_INVAL;
+    if (p->head_dim != 64 && p->head_dim != 128) return TGVKV_E_UNSUPPORTED;
+    if (p->layers > kMaxLayers || N > kMaxTokens) return TGVKV_E_UNSUPPORTED;
+    const int64_t G = p->heads_q / p->heads_kv;
+    if (G * ((int64_t)p->n_sys + p->n_qst) > kMaxTextRowsPerKvHead) return TGVKV_E_UNSUPPORTED;
+    if (G > kMaxGroup) return TGVKV_E_UNSUPPORTED;
+    if ((int64_t)p->batch * p->layers * p->heads_q * 8 > kMaxBlocks) return TGVKV_E_UNSUPPORTED;
+
+    s->B = p->batch;
+    s->L = p->layers;
+    s->H = p->heads_q;
+    s->Hkv = p->heads_kv;
+    s->D = p->head_dim;
+    s->G = (int32_t)G;
+    s->Ns = p->n_sys;
+    s->Nv = p->n_vis;
+    s->Nq = p->n_qst;
+    s->N = (int32_t)N;
+    s->Nt = p->n_sys + p->n_qst;
+    s->head_mode = d.head_mode;
+    s->ngroups = d.head_mode == 0 ? 1 : p->heads_kv;
+    s->n_sink = d.n_sink;
+    s->n_recent = d.n_recent;
+    s->sm_scale = d.sm_scale > 0.f ? d.sm_scale : 1.0f / std::sqrt((float)p->head_dim);
+    s->scale2 = s->sm_scale * 1.4426950408889634f;
+    return TGVKV_OK;
+}
+
+// |forced|: the first n_sink and the last n_recent positions.
+int32_t forced_count(const Shape& s) {
+    const int64_t fs = std::min<int64_t>(s.n_sink, s.N);
+    const int64_t fr = std::max<int64_t>(s.N - (int64_t)s.n_recent, fs);
+    return (int32_t)(fs + (s.N - fr));
+}
+
+// |forced U T|: a layer needs vision scores only when its budget exceeds this.
+int32_t forced_or_text_count(const Shape& s) {
+    const int64_t fs = std::min<int64_t>(s.n_sink, s.N);
+    const int64_t fr = std::max<int64_t>(s.N - (int64_t)s.n_recent, fs);
+    const int64_t v0 = s.Ns, v1 = (int64_t)s.Ns + s.Nv;
+    int64_t fv = 0;
+    fv += std::max<int64_t>(0, std::min(fs, v1) - v0);
+    fv += std::max<int64_t>(0, v1 - std::max(fr, v0));
+    return (int32_t)(s.Nt + fv);
+}
+
+struct ScoreWs {
+    float* vm;
+    float* colsum;
+    float* vmh;
+    float* part;
+    size_t bytes;
+};
+
+ScoreWs score_workspace(const Shape& s, const RowPlan& rp, void* base) {
+    const size_t bl = (size_t)s.B * s.L;
+    size_t off = 0;
+    ScoreWs w;
+    char* b = static_cast<char*>(base);
+    w.vm = reinterpret_cast<float*>(b ? b + off : nullptr);
+    off = align_up(off + sizeof(float) * bl * s.H * s.Nq);
+    w.colsum = reinterpret_cast<float*>(b ? b + off : nullptr);
+    off = align_up(off + sizeof(float) * bl * s.H * s.Nt);
+    w.vmh = reinterpret_cast<float*>(b ? b + off : nullptr);
+    off = align_up(off + sizeof(float) * bl * s.H);
+    w.part = reinterpret_cast<float*>(b ? b + off : nullptr);
+    off = align_up(off + sizeof(float) * bl * s.Hkv * (size_t)rp.rowgroups * s.Nv);
+    w.bytes = off;
+    return w;
+}
+
+size_t decode_workspace_bytes(const Shape& s) {
+    const int ns = tgvkv::decode_splits(s);
+    if (ns <= 1) return 0;
+    return align_up(sizeof(float) * (size_t)s.B * s.L * s.H * ns * (s.D + 2));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+tgvkv_status hip_status(hipError_t e) { return e == hipSuccess ? TGVKV_OK : TGVKV_E_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+int32_t tgvkv_abi_version(void) { return TGVKV_ABI_VERSION; }
+
+const char* tgvkv_status_string(tgvkv_status st) {
+    switch (st) {
+        case TGVKV_OK: return "ok";
+        case TGVKV_E_INVAL: return "invalid argument";
+        case TGVKV_E_UNSUPPORTED: return "unsupported problem (head_dim or size limit)";
+        case TGVKV_E_WORKSPACE: return "workspace missing or too small";
+        case TGVKV_E_CAPACITY: return "budget or decode step exceeds the cache capacity";
+        case TGVKV_E_HIP: return "HIP launch failed";
+    }
+    return "unknown status";
+}
+
+size_t tgvkv_workspace_size(const tgvkv_problem* problem, const tgvkv_opts* opts, int32_t which) {
+    Shape s;
+    if (make_shape(problem, opts, &s) != TGVKV_OK) return 0;
+    if (which == TGVKV_CALL_SCORE) return score_workspace(s, tgvkv::plan_question_rows(s), nullptr).bytes;
+    if (which == TGVKV_CALL_DECODE) return decode_workspace_bytes(s);
+    return 0;
+}
+
+tgvkv_status tgvkv_score(const tgvkv_problem* problem, const tgvkv_opts* opts, int32_t phases, const void* q_text,
+                         const void* k, float* lse, float* s_txt, float* w_txt, float* tv_mass, float* s_vis,
+                         const int32_t* budgets_or_null, void* workspace, size_t workspace_bytes,
+                         hipStream_t stream) {
+    Shape s;
+    tgvkv_status st = make_shape(problem, opts, &s);
+    if (st != TGVKV_OK) return st;
+    if (phases < 1 || phases > TGVKV_SCORE_ALL) return TGVKV_E_INVAL;
+    if (s.B == 0) return TGVKV_OK;
+    const bool text_rows = s.Nt > 0;
+    if (q_text == nullptr && text_rows) return TGVKV_E_INVAL;
+    if (k == nullptr || (lse == nullptr && text_rows)) return TGVKV_E_INVAL;
+    if ((phases & TGVKV_SCORE_TEXT) && (tv_mass == nullptr || (text_rows && (s_txt == nullptr || w_txt == nullptr))))
+        return TGVKV_E_INVAL;
+    if ((phases & TGVKV_SCORE_VISION) && s.Nv > 0 && (s_vis == nullptr || (text_rows && w_txt == nullptr)))
+        return TGVKV_E_INVAL;
+    if (!aligned16(q_text) || !aligned16(k)) return TGVKV_E_INVAL;
+    const RowPlan rp = tgvkv::plan_question_rows(s);
+    if ((int64_t)s.B * s.L * s.Hkv * std::max(rp.rowgroups, 1) > kMaxBlocks) return TGVKV_E_UNSUPPORTED;
+    const ScoreWs need = score_workspace(s, rp, nullptr);
+    if (workspace == nullptr || workspace_bytes < need.bytes) return TGVKV_E_WORKSPACE;
+    const ScoreWs w = score_workspace(s, rp, workspace);
+    const uint16_t* q = static_cast<const uint16_t*>(q_text);
+    const uint16_t* kk = static_cast<const uint16_t*>(k);
+    const int32_t vthr = forced_or_text_count(s);
+
+    hipError_t e = hipSuccess;
+    if ((phases & TGVKV_SCORE_STATS) && e == hipSuccess) e = tgvkv::launch_score_stats(s, rp, q, kk, lse, w.vm, stream);
+    if ((phases & TGVKV_SCORE_TEXT) && e == hipSuccess) {
+        e = tgvkv::launch_score_text(s, q, kk, lse, w.vm, w.colsum, w.vmh, stream);
+        if (e == hipSuccess) e = tgvkv::launch_score_fin(s, w.colsum, w.vmh, s_txt, w_txt, tv_mass, stream);
+    }
+    if ((phases & TGVKV_SCORE_VISION) && e == hipSuccess && s.Nv > 0) {
+        e = tgvkv::launch_score_vision(s, rp, q, kk, lse, w_txt, budgets_or_null, vthr, w.part, stream);
+        if (e == hipSuccess) e = tgvkv::launch_score_vis_reduce(s, rp, w.part, budgets_or_null, vthr, s_vis, stream);
+    }
+    return hip_status(e);
+}
+
+tgvkv_status tgvkv_budget(const tgvkv_problem* problem, const tgvkv_opts* opts, const float* tv_mass,
+                          int64_t total_budget, int32_t decode_reserve, int32_t* budgets, int64_t* idx_offsets,
+                          int64_t* seg_offsets, hipStream_t stream) {
+    Shape s;
+    tgvkv_status st = make_shape(problem, opts, &s);
+    if (st != TGVKV_OK) return st;
+    if (decode_reserve < 0 || total_budget < 0) return TGVKV_E_INVAL;
+    if (total_budget > (int64_t)s.L * s.N) return TGVKV_E_CAPACITY;
+    if (idx_offsets == nullptr || seg_offsets == nullptr) return TGVKV_E_INVAL;
+    if (s.B > 0 && (tv_mass == nullptr || budgets == nullptr)) return TGVKV_E_INVAL;
+    const int64_t seg_total = (int64_t)s.B * (total_budget + (int64_t)s.L * decode_reserve);
+    if (seg_total > (int64_t(1) << 40)) return TGVKV_E_UNSUPPORTED;
+    if (s.B == 0) return TGVKV_OK;
+    return hip_status(tgvkv::launch_budget(s, tv_mass, total_budget, decode_reserve, forced_count(s), budgets,
+                                           idx_offsets, seg_offsets, stream));
+}
+
+tgvkv_status tgvkv_select(const tgvkv_problem* problem, const tgvkv_opts* opts, const float* s_vis,
+                          const float* s_txt, const int32_t* budgets, const int64_t* idx_offsets, int32_t* idx,
+                          hipStream_t stream) {
+    Shape s;
+    tgvkv_status st = make_shape(problem, opts, &s);
+    if (st != TGVKV_OK) return st;
+    if (s.B == 0) return TGVKV_OK;
+    if (budgets == nullptr || idx_offsets == nullptr || idx == nullptr) return TGVKV_E_INVAL;
+    if ((s.Nv > 0 && s_vis == nullptr) || (s.Nt > 0 && s_txt == nullptr)) return TGVKV_E_INVAL;
+    if ((int64_t)s.B * s.L * s.ngroups > kMaxBlocks) return TGVKV_E_UNSUPPORTED;
+    return hip_status(tgvkv::launch_select(s, s_vis, s_txt, budgets, idx_offsets, idx, stream));
+}
+
+tgvkv_status tgvkv_compact(const tgvkv_problem* problem, const tgvkv_opts* opts, const void* k, const void* v,
+                           const int32_t* idx, const int32_t* budgets, const int64_t* idx_offsets,
+                           const int64_t* seg_offsets, int64_t total_budget, int32_t decode_reserve, void* kc,
+                           void* vc, hipStream_t stream) {
+    Shape s;
+    tgvkv_status st = make_shape(problem, opts, &s);
+    if (st != TGVKV_OK) return st;
+    if (decode_reserve < 0 || total_budget < 0) return TGVKV_E_INVAL;
+    if (total_budget > (int64_t)s.L * s.N) return TGVKV_E_CAPACITY;
+    if (s.B == 0 || total_budget == 0) return TGVKV_OK;
+    if (k == nullptr || v == nullptr || idx == nullptr || budgets == nullptr || idx_offsets == nullptr ||
+        seg_offsets == nullptr || kc == nullptr || vc == nullptr)
+        return TGVKV_E_INVAL;
+    if (!aligned16(k) || !aligned16(v) || !aligned16(kc) || !aligned16(vc)) return TGVKV_E_INVAL;
+    const int64_t rows = (int64_t)s.B * total_budget;
+    if ((rows + 63) / 64 > kMaxBlocks || s.Hkv > 65535) return TGVKV_E_UNSUPPORTED;
+    return hip_status(tgvkv::launch_compact(s, static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), idx,
+                                            budgets, idx_offsets, seg_offsets, decode_reserve, rows,
+                                            static_cast<uint16_t*>(kc), static_cast<uint16_t*>(vc), stream));
+}
+
+tgvkv_status tgvkv_decode_attn(const tgvkv_problem* problem, const tgvkv_opts* opts, void* kc, void* vc,
+                               const int32_t* budgets, const int64_t* seg_offsets, int32_t decode_reserve,
+                               int32_t step, const void* q, const void* k_new, const void* v_new, float* out,
+                               void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    Shape s;
+    tgvkv_status st = make_shape(problem, opts, &s);
+    if (st != TGVKV_OK) return st;
+    if (decode_reserve < 0) return TGVKV_E_INVAL;
+    if (step < 0 || step >= decode_reserve) return TGVKV_E_CAPACITY;
+    if (s.B == 0) return TGVKV_OK;
+    if (kc == nullptr || vc == nullptr || budgets == nullptr || seg_offsets == nullptr || q == nullptr ||
+        k_new == nullptr || v_new == nullptr || out == nullptr)
+        return TGVKV_E_INVAL;
+    if (!aligned16(kc) || !aligned16(vc) || !aligned16(q) || !aligned16(k_new) || !aligned16(v_new))
+        return TGVKV_E_INVAL;
+    const size_t need = decode_workspace_bytes(s);
+    if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return TGVKV_E_WORKSPACE;
+    return hip_status(tgvkv::launch_decode(s, static_cast<uint16_t*>(kc), static_cast<uint16_t*>(vc), budgets,
+                                           seg_offsets, decode_reserve, step, static_cast<const uint16_t*>(q),
+                                           static_cast<const uint16_t*>(k_new), static_cast<const uint16_t*>(v_new),
+                                           out, static_cast<float*>(workspace), stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,73 @@
+// Device-side primitives shared by the gfx950 kernels of libtgvkv.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tgvkv {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+constexpr float kNegInf = -__builtin_inff();
+
+// Wave64 lane id.
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
+
+__device__ __forceinline__ float bf16_bits_to_float(uint32_t bits16) {
+    return __uint_as_float(bits16 << 16);
+}
+
+// 16 bytes of bf16 (8 elements) as an MFMA operand fragment.
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+__device__ __forceinline__ u32x4 load16(const void* p) {
+    return *reinterpret_cast<const u32x4*>(p);
+}
+
+__device__ __forceinline__ void store16(void* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
+
+// v_exp_f32: 2^x, exp2(-inf) = 0.
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
+
+// One 16x16x32 bf16 MFMA: C[m][n] += sum_k A[m][k] B[k][n].  Lane l holds A row
+// l%16 and B column l%16, each with 8 consecutive k of the lane's quarter l/16;
+// the accumulator element j of lane l is C[4*(l/16) + j][l%16].
+__device__ __forceinline__ f32x4 mfma16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+template <typename T>
+__device__ __forceinline__ T shfl_xor(T v, int mask) {
+    return __shfl_xor(v, mask, 64);
+}
+
+// Combine two online-softmax partials (max m in log2 units, sum l, extra sum v
+// that shares the normaliser).
+__device__ __forceinline__ void merge_stats(float& m, float& l, float& v, float m2, float l2, float v2) {
+    float mn = fmaxf(m, m2);
+    if (mn == kNegInf) {
+        m = kNegInf;
+        l = 0.f;
+        v = 0.f;
+        return;
+    }
+    float s1 = fast_exp2(m - mn), s2 = fast_exp2(m2 - mn);
+    l = l * s1 + l2 * s2;
+    v = v * s1 + v2 * s2;
+    m = mn;
+}
+
+// Map a float to an unsigned key with the same order (-0.0 treated as +0.0).
+__device__ __forceinline__ uint32_t ordered_key(float f) {
+    uint32_t b = __float_as_uint(f);
+    if (b == 0x80000000u) b = 0u;
+    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+}  // namespace tgvkv

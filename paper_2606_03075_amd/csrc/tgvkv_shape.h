@@ -1,0 +1,56 @@
+// Problem geometry passed by value to every kernel, and the host-side launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tgvkv {
+
+struct Shape {
+    int32_t B, L, H, Hkv, D, G;
+    int32_t Ns, Nv, Nq, N, Nt;
+    int32_t head_mode, ngroups;
+    int32_t n_sink, n_recent;
+    float sm_scale;
+    float scale2;  // sm_scale * log2(e): logits in base-2 units
+};
+
+// Launch plan of the question-row passes: waves split 16-row blocks into row sets
+// (each up to NSLOT blocks) and, for few blocks, split each key tile into KS parts.
+struct RowPlan {
+    int nslot, ks, rowgroups;
+};
+
+RowPlan plan_question_rows(const Shape& s);
+
+// Score phases.
+hipError_t launch_score_stats(const Shape& s, const RowPlan& rp, const uint16_t* q_text,
+                              const uint16_t* k, float* lse, float* ws_vm, hipStream_t st);
+hipError_t launch_score_text(const Shape& s, const uint16_t* q_text, const uint16_t* k, float* lse,
+                             const float* ws_vm, float* ws_colsum, float* ws_vmh, hipStream_t st);
+hipError_t launch_score_fin(const Shape& s, const float* ws_colsum, const float* ws_vmh, float* s_txt,
+                            float* w_txt, float* tv_mass, hipStream_t st);
+hipError_t launch_score_vision(const Shape& s, const RowPlan& rp, const uint16_t* q_text,
+                               const uint16_t* k, const float* lse, const float* w_txt,
+                               const int32_t* budgets, int32_t vis_threshold, float* ws_part,
+                               hipStream_t st);
+hipError_t launch_score_vis_reduce(const Shape& s, const RowPlan& rp, const float* ws_part,
+                                   const int32_t* budgets, int32_t vis_threshold, float* s_vis,
+                                   hipStream_t st);
+
+hipError_t launch_budget(const Shape& s, const float* tv_mass, int64_t total, int32_t reserve,
+                         int32_t n_forced, int32_t* budgets, int64_t* idx_off, int64_t* seg_off,
+                         hipStream_t st);
+hipError_t launch_select(const Shape& s, const float* s_vis, const float* s_txt, const int32_t* budgets,
+                         const int64_t* idx_off, int32_t* idx, hipStream_t st);
+hipError_t launch_compact(const Shape& s, const uint16_t* k, const uint16_t* v, const int32_t* idx,
+                          const int32_t* budgets, const int64_t* idx_off, const int64_t* seg_off,
+                          int32_t reserve, int64_t rows_total, uint16_t* kc, uint16_t* vc, hipStream_t st);
+
+int decode_splits(const Shape& s);
+hipError_t launch_decode(const Shape& s, uint16_t* kc, uint16_t* vc, const int32_t* budgets,
+                         const int64_t* seg_off, int32_t reserve, int32_t step, const uint16_t* q,
+                         const uint16_t* k_new, const uint16_t* v_new, float* out, float* ws_part,
+                         hipStream_t st);
+
+}  // namespace tgvkv

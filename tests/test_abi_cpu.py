@@ -1,0 +1,127 @@
+"""The C-ABI library loads, exports what include/tgvkv.h declares, and rejects bad calls on the host.
+
+No compute call is made here: every call below must fail validation (or have
+nothing to do) before the library touches the HIP runtime.  Fake non-null
+pointers are used only when no GPU is present, so a validation bug can never
+reach a kernel launch on real hardware.
+"""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_03075_amd import binding as bd
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _gpu():
+    try:
+        import torch
+        return torch.cuda.is_available()
+    except Exception:
+        return False
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(bd.LIB_PATH):
+        from paper_2606_03075_amd import build
+        build.build()
+    return bd.load_library()
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "tgvkv.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(tgvkv_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert set(bd.EXPORTS) <= set(names) and len(names) == len(bd.EXPORTS), names
+    for n in names:
+        assert hasattr(lib, n), n
+    assert lib.tgvkv_abi_version() == 1
+    for st in (0, -1, -2, -3, -4, -5):
+        assert lib.tgvkv_status_string(st)
+    assert lib.tgvkv_status_string(7) == b"unknown status"
+
+
+def P(**kw):
+    base = dict(batch=1, layers=2, heads_q=4, heads_kv=2, head_dim=128, n_sys=3, n_vis=40, n_qst=5)
+    base.update(kw)
+    return bd.make_problem(**base)
+
+
+def test_workspace_size(lib):
+    assert bd.workspace_size(P(), None, bd.CALL_SCORE) > 0
+    assert bd.workspace_size(P(head_dim=96), None, bd.CALL_SCORE) == 0
+    assert bd.workspace_size(P(heads_q=3), None, bd.CALL_SCORE) == 0
+    assert bd.workspace_size(P(), None, 9) == 0
+    # decode needs a split workspace only for small (b, l, kv-head) counts
+    assert bd.workspace_size(P(), None, bd.CALL_DECODE) > 0
+    assert bd.workspace_size(P(batch=64, layers=32, heads_q=32, heads_kv=32), None, bd.CALL_DECODE) == 0
+
+
+@pytest.mark.skipif(_gpu(), reason="fake pointers are used only where no GPU exists")
+def test_validation_before_any_launch(lib):
+    fake = ctypes.c_void_p(0x10000)
+    odd = ctypes.c_void_p(0x10008)
+    big = ctypes.c_size_t(1 << 40)
+    s = ctypes.c_void_p(0)
+    ok = ctypes.byref(P())
+    opts = bd.make_opts()
+    # invalid problems
+    for bad, code in [(P(batch=-1), -1), (P(layers=0), -1), (P(heads_q=3), -1), (P(n_sys=0, n_vis=0, n_qst=0), -1),
+                      (P(head_dim=96), -2), (P(layers=600), -2), (P(heads_q=64, heads_kv=2), -2)]:
+        r = lib.tgvkv_score(ctypes.byref(bad), None, 7, fake, fake, fake, fake, fake, fake, fake, None, fake, big, s)
+        assert r == code, (bad.head_dim, r)
+    assert lib.tgvkv_score(None, None, 7, fake, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
+    # bad options
+    for o in (bd.make_opts(head_mode=2), bd.make_opts(n_sink=-1), bd.make_opts(sm_scale=float("nan"))):
+        assert lib.tgvkv_score(ok, ctypes.byref(o), 7, fake, fake, fake, fake, fake, fake, fake, None, fake, big,
+                               s) == -1
+    # phases, null and misaligned pointers, workspace
+    assert lib.tgvkv_score(ok, None, 0, fake, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
+    assert lib.tgvkv_score(ok, None, 8, fake, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
+    assert lib.tgvkv_score(ok, None, 7, None, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
+    assert lib.tgvkv_score(ok, None, 7, odd, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
+    assert lib.tgvkv_score(ok, None, 2, fake, fake, fake, None, fake, fake, fake, None, fake, big, s) == -1
+    assert lib.tgvkv_score(ok, None, 4, fake, fake, fake, fake, fake, fake, None, None, fake, big, s) == -1
+    assert lib.tgvkv_score(ok, None, 7, fake, fake, fake, fake, fake, fake, fake, None, None, big, s) == -3
+    assert lib.tgvkv_score(ok, None, 7, fake, fake, fake, fake, fake, fake, fake, None, fake, 16, s) == -3
+    # budgets: capacity and arguments
+    L, N = 2, 48
+    assert lib.tgvkv_budget(ok, None, fake, L * N + 1, 0, fake, fake, fake, s) == -4
+    assert lib.tgvkv_budget(ok, None, fake, -1, 0, fake, fake, fake, s) == -1
+    assert lib.tgvkv_budget(ok, None, fake, 10, -1, fake, fake, fake, s) == -1
+    assert lib.tgvkv_budget(ok, None, None, 10, 0, fake, fake, fake, s) == -1
+    # select / compact / decode arguments
+    assert lib.tgvkv_select(ok, None, fake, fake, None, fake, fake, s) == -1
+    assert lib.tgvkv_select(ok, None, None, fake, fake, fake, fake, s) == -1
+    assert lib.tgvkv_compact(ok, None, fake, fake, fake, fake, fake, fake, L * N + 1, 0, fake, fake, s) == -4
+    assert lib.tgvkv_compact(ok, None, fake, fake, fake, fake, fake, fake, 10, 0, fake, None, s) == -1
+    assert lib.tgvkv_compact(ok, None, fake, odd, fake, fake, fake, fake, 10, 0, fake, fake, s) == -1
+    assert lib.tgvkv_decode_attn(ok, None, fake, fake, fake, fake, 4, 4, fake, fake, fake, fake, fake, big, s) == -4
+    assert lib.tgvkv_decode_attn(ok, None, fake, fake, fake, fake, 4, -1, fake, fake, fake, fake, fake, big, s) == -4
+    assert lib.tgvkv_decode_attn(ok, None, fake, fake, fake, fake, 4, 0, fake, fake, fake, None, fake, big, s) == -1
+    assert lib.tgvkv_decode_attn(ok, None, fake, fake, fake, fake, 4, 0, fake, fake, fake, fake, None, 0, s) == -3
+
+
+def test_empty_batch_is_a_no_op(lib):
+    z = ctypes.byref(P(batch=0))
+    s = ctypes.c_void_p(0)
+    assert lib.tgvkv_score(z, None, 7, None, ctypes.c_void_p(0x10000), None, None, None, None, None, None, None,
+                           0, s) == 0
+    assert lib.tgvkv_budget(z, None, None, 5, 0, None, ctypes.c_void_p(0x10000), ctypes.c_void_p(0x10000), s) == 0
+    assert lib.tgvkv_select(z, None, None, None, None, None, None, s) == 0
+    assert lib.tgvkv_compact(z, None, None, None, None, None, None, None, 5, 0, None, None, s) == 0
+    assert lib.tgvkv_decode_attn(z, None, None, None, None, None, 2, 0, None, None, None, None, None, 0, s) == 0
+
+
+def test_binding_fails_loudly_without_library(tmp_path):
+    with pytest.raises(RuntimeError):
+        bd.load_library(str(tmp_path / "missing.so"))

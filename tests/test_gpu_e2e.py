@@ -1,0 +1,136 @@
+"""End-to-end GPU parity: eviction pass (score, budget, vision score, select, compact) then decode steps.
+
+Inputs are the seeded workloads; the oracle runs on the same bf16 values.
+"""
+
+import numpy as np
+import pytest
+
+import oracle.tgvkv_oracle as O
+from paper_2606_03075_amd import binding as bd
+from tests.gpu_util import (DECODE_ATOL, assert_close_rel, bf16_host_bits, budget_allowed, dev_bf16, host,
+                            idx_allowed, log)
+from workloads import bf16_bits_to_f32, make_decode_tensors, make_prefill_tensors, total_budget
+from workloads.configs import CONFIGS, custom_config
+
+pytestmark = pytest.mark.gpu
+
+
+def run_and_check(cfg, rho, head_mode=0, forced=(0, 0), steps=2, seed=0, skip_text_only=True):
+    import torch
+    log(f"e2e {cfg.name} rho={rho} mode={head_mode} forced={forced} steps={steps}")
+    t = make_prefill_tensors(cfg, seed=seed)
+    dec = make_decode_tensors(cfg, seed=seed, steps=steps)
+    B, L, N = cfg.batch, cfg.layers, cfg.n_tokens
+    tot = total_budget(rho, N, L)
+    p = bd.problem_from(cfg)
+    o = bd.make_opts(head_mode=head_mode, n_sink=forced[0], n_recent=forced[1])
+    buf = bd.EvictionBuffers(p, o, tot, max(steps, 1))
+    q_d, k_d, v_d = dev_bf16(t["q_text"]), dev_bf16(t["k"]), dev_bf16(t["v"])
+    buf.evict(q_d, k_d, v_d, skip_text_only_layers=skip_text_only)
+    outs = []
+    for st in range(steps):
+        buf.decode(st, dev_bf16(dec["q"][st]), dev_bf16(dec["k_new"][st]), dev_bf16(dec["v_new"][st]))
+        outs.append(host(buf.out).copy())
+    torch.cuda.synchronize()
+
+    g = 1 if head_mode == 0 else cfg.heads_kv
+    budgets = host(buf.budgets)
+    io, so = host(buf.idx_offsets), host(buf.seg_offsets)
+    idx = host(buf.idx)
+    kc, vc = bf16_host_bits(buf.kc), bf16_host_bits(buf.vc)
+    tv = host(buf.tv_mass)
+    nf = len(O.forced_positions(N, *forced))
+    swaps = flips = 0
+    tau = 1.0 / np.sqrt(cfg.head_dim)
+    D, Hkv = cfg.head_dim, cfg.heads_kv
+    for b in range(B):
+        qf = bf16_bits_to_f32(t["q_text"][b])
+        kf = bf16_bits_to_f32(t["k"][b])
+        scores, ob, oidx = O.evict_sequence(qf, kf, cfg.n_sys, cfg.n_vis, cfg.n_qst, tot, None, head_mode,
+                                            *forced)
+        assert budgets[b].sum() == tot
+        ok_b = budget_allowed(budgets[b], ob, [s["tv_mass"] for s in scores], tot, N, nf)
+        assert ok_b, (b, budgets[b], ob)
+        flips += int(np.abs(budgets[b] - ob).sum()) // 2
+        for l in range(L):
+            sc = scores[l]
+            assert_close_rel("tv_mass", tv[b, l], sc["tv_mass"])
+            assert_close_rel("s_txt", host(buf.s_txt[b, l]), sc["s_txt"])
+            assert_close_rel("w_txt", host(buf.w_txt[b, l]), sc["w_txt"])
+            needs_vis = budgets[b, l] > cfg.n_text + 0
+            if needs_vis or not skip_text_only:
+                assert_close_rel("s_vis", host(buf.s_vis[b, l]), sc["s_vis"])
+            if budgets[b, l] != ob[l]:
+                continue  # a rounding-cut trade: this layer's set is legitimately different
+            bl = b * L + l
+            bsz = int(budgets[b, l])
+            agree = True
+            for gg in range(g):
+                gidx = idx[io[bl] + gg * bsz: io[bl] + (gg + 1) * bsz]
+                s_ = idx_allowed(gidx, oidx[l][gg], sc["s_vis"][gg], sc["s_txt"][gg], bsz, cfg, *forced)
+                swaps += s_
+                agree = agree and s_ == 0
+            if not agree:
+                continue
+            # compacted cache is bit-exact for the agreed sets; then decode against the oracle
+            cap = bsz + max(steps, 1)
+            Kc, Vc = [], []
+            for h in range(Hkv):
+                sel = oidx[l][0 if head_mode == 0 else h]
+                base = (int(so[bl]) * Hkv + h * cap) * D
+                got_k = kc[base: base + bsz * D].reshape(bsz, D)
+                got_v = vc[base: base + bsz * D].reshape(bsz, D)
+                assert np.array_equal(got_k, t["k"][b, l, h][sel]) and np.array_equal(got_v, t["v"][b, l, h][sel])
+                Kc.append(bf16_bits_to_f32(t["k"][b, l, h][sel]))
+                Vc.append(bf16_bits_to_f32(t["v"][b, l, h][sel]))
+            if steps:
+                ref = O.decode_reference(bf16_bits_to_f32(dec["q"][:, b, l]), bf16_bits_to_f32(dec["k_new"][:, b, l]),
+                                         bf16_bits_to_f32(dec["v_new"][:, b, l]), Kc, Vc, tau)
+                for st in range(steps):
+                    err = np.abs(outs[st][b, l] - ref[st]).max()
+                    assert err <= DECODE_ATOL, (b, l, st, err)
+    log(f"  budgets flips={flips} boundary swaps={swaps}")
+    return buf
+
+
+@pytest.mark.parametrize("head_mode", [0, 1])
+@pytest.mark.parametrize("forced", [(0, 0), (4, 1)])
+def test_small_ragged(lib, head_mode, forced):
+    cfg = custom_config(batch=2, layers=4, heads_q=8, heads_kv=4, head_dim=128, n_sys=6, n_vis=230, n_qst=21)
+    for rho in (0.05, 0.2, 0.6, 1.0):
+        run_and_check(cfg, rho, head_mode, forced, steps=3, seed=1)
+
+
+def test_gqa_video_small(lib):
+    cfg = custom_config(name="vid", batch=2, layers=3, heads_q=28, heads_kv=4, head_dim=128, n_sys=16, n_vis=512,
+                        n_qst=48, frames=4)
+    for rho in (0.05, 0.1):
+        run_and_check(cfg, rho, 0, steps=3, seed=2)
+
+
+@pytest.mark.parametrize("rho", CONFIGS["tiny"].rhos)
+def test_tiny_config(lib, rho):
+    run_and_check(CONFIGS["tiny"], rho, steps=1, seed=0)
+
+
+@pytest.mark.parametrize("rho", CONFIGS["llava15"].rhos)
+def test_llava15_config(lib, rho):
+    run_and_check(CONFIGS["llava15"], rho, steps=8, seed=0)
+
+
+def test_llava15_all_layers_scored(lib):
+    run_and_check(CONFIGS["llava15"], 0.05, steps=0, seed=4, skip_text_only=False)
+
+
+def test_edge_shapes(lib):
+    # no question text (no text->vision mass: uniform budgets, position ties), no vision, no system text
+    run_and_check(custom_config(name="noq", batch=1, layers=3, heads_q=4, heads_kv=2, n_sys=9, n_vis=70, n_qst=0),
+                  0.3, steps=2)
+    run_and_check(custom_config(name="nov", batch=1, layers=3, heads_q=4, heads_kv=2, n_sys=9, n_vis=0, n_qst=12),
+                  0.5, steps=2)
+    run_and_check(custom_config(name="nos", batch=1, layers=3, heads_q=4, heads_kv=4, head_dim=64, n_sys=0, n_vis=90,
+                                n_qst=17), 0.25, steps=2)
+    # budget 0 everywhere, then decode over the appended tokens only
+    run_and_check(custom_config(name="zero", batch=1, layers=2, heads_q=4, heads_kv=4, n_sys=3, n_vis=40, n_qst=5),
+                  0.0, steps=3)
