@@ -16,7 +16,8 @@ from workloads.configs import CONFIGS, custom_config
 pytestmark = pytest.mark.gpu
 
 
-def run_and_check(cfg, rho, head_mode=0, forced=(0, 0), steps=2, seed=0, skip_text_only=True):
+def run_and_check(cfg, rho, head_mode=0, forced=(0, 0), steps=2, seed=0, skip_text_only=True, check_seqs=None,
+                  decode_seqs=None):
     import torch
     log(f"e2e {cfg.name} rho={rho} mode={head_mode} forced={forced} steps={steps}")
     t = make_prefill_tensors(cfg, seed=seed)
@@ -44,7 +45,10 @@ def run_and_check(cfg, rho, head_mode=0, forced=(0, 0), steps=2, seed=0, skip_te
     swaps = flips = 0
     tau = 1.0 / np.sqrt(cfg.head_dim)
     D, Hkv = cfg.head_dim, cfg.heads_kv
-    for b in range(B):
+    assert np.all(budgets.sum(axis=1) == tot)
+    check_seqs = range(B) if check_seqs is None else check_seqs
+    decode_seqs = set(range(B) if decode_seqs is None else decode_seqs)
+    for b in check_seqs:
         qf = bf16_bits_to_f32(t["q_text"][b])
         kf = bf16_bits_to_f32(t["k"][b])
         scores, ob, oidx = O.evict_sequence(qf, kf, cfg.n_sys, cfg.n_vis, cfg.n_qst, tot, None, head_mode,
@@ -84,7 +88,7 @@ def run_and_check(cfg, rho, head_mode=0, forced=(0, 0), steps=2, seed=0, skip_te
                 assert np.array_equal(got_k, t["k"][b, l, h][sel]) and np.array_equal(got_v, t["v"][b, l, h][sel])
                 Kc.append(bf16_bits_to_f32(t["k"][b, l, h][sel]))
                 Vc.append(bf16_bits_to_f32(t["v"][b, l, h][sel]))
-            if steps:
+            if steps and b in decode_seqs:
                 ref = O.decode_reference(bf16_bits_to_f32(dec["q"][:, b, l]), bf16_bits_to_f32(dec["k_new"][:, b, l]),
                                          bf16_bits_to_f32(dec["v_new"][:, b, l]), Kc, Vc, tau)
                 for st in range(steps):
