@@ -48,9 +48,17 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target length of the oracle sample")
-    ap.add_argument("--score-all-layers", action="store_true",
-                    help="compute vision scores for every layer (by default layers whose budget only "
-                         "covers text skip them)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="instead of the benchmark, copy a 1 GiB buffer 5 times (a plain copy kernel of known "
+                         "size, to scale rocprofv3 FETCH_SIZE / WRITE_SIZE counters to bytes)")
+    ap.add_argument("--ingest-counters", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV",
+                                                            "COPY_WRITE_CSV"),
+                    help="turn rocprofv3 --pmc counter files of a bench run and of a --calibrate-copy run into "
+                         "profiles/hbm_counters.json (HBM bytes per launch of each kernel)")
+    ap.add_argument("--schedule", default="auto", choices=("auto", "two_step", "phases", "fused", "fused_text"),
+                    help="scoring schedule: vision scores after the budgets only for layers that need them "
+                         "(auto, two_step), one launch per phase for every layer (phases), or the persistent "
+                         "fused kernel (fused, fused_text)")
     return ap.parse_args()
 
 
@@ -63,14 +71,14 @@ def source_hash(files):
 
 
 KERNEL_SOURCES = {
-    "score_stats": ["score.hip", "tgvkv_device.h"],
-    "score_vision": ["score.hip", "tgvkv_device.h"],
+    "score_stats": ["score.hip", "score_core.h", "tgvkv_device.h"],
+    "score_vision": ["score.hip", "score_core.h", "tgvkv_device.h"],
     "compact": ["compact.hip", "tgvkv_device.h"],
     "decode": ["decode.hip", "tgvkv_device.h"],
 }
 
 
-def traffic_for(kernel, workload, launches_bytes_unit=None):
+def traffic_for(kernel, workload, decode_steps=None):
     """HBM bytes per launch from committed rocprofv3 counters, if they match the current source."""
     try:
         with open(COUNTERS) as f:
@@ -80,6 +88,8 @@ def traffic_for(kernel, workload, launches_bytes_unit=None):
     rec = data.get(workload, {}).get(kernel)
     if not rec or rec.get("source_hash") != source_hash(KERNEL_SOURCES[kernel]):
         return None
+    if kernel == "decode" and rec.get("decode_steps") != decode_steps:
+        return None  # per-launch decode bytes depend on how many steps were averaged
     return rec.get("bytes_per_launch")
 
 
@@ -130,8 +140,78 @@ def cpu_baseline(cfg, t, dec, tot, budget_s):
     }
 
 
+COPY_BYTES = 1 << 30
+KERNEL_NAMES = {"score_stats": "score_stats_kernel", "score_vision": "score_vision_kernel",
+                "compact": "compact_kernel", "decode": "decode_kernel"}
+
+
+def calibrate_copy():
+    import torch
+    a = torch.empty(COPY_BYTES, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(5):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibration": "copy", "bytes_read": COPY_BYTES, "bytes_written": COPY_BYTES, "launches": 5}))
+
+
+def _counter_rows(path):
+    import csv
+    with open(path) as f:
+        return list(csv.DictReader(f))
+
+
+def _per_kernel_kib(rows, counter):
+    """Mean counter value per dispatch, grouped by kernel-name substring."""
+    acc = {}
+    for r in rows:
+        if r.get("Counter_Name") != counter:
+            continue
+        name = r.get("Kernel_Name", "")
+        acc.setdefault(name, []).append(float(r["Counter_Value"]))
+    return {k: sum(v) / len(v) for k, v in acc.items()}
+
+
+def ingest_counters(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, workload):
+    fetch = _per_kernel_kib(_counter_rows(fetch_csv), "FETCH_SIZE")
+    write = _per_kernel_kib(_counter_rows(write_csv), "WRITE_SIZE")
+    cf = _per_kernel_kib(_counter_rows(copy_fetch_csv), "FETCH_SIZE")
+    cw = _per_kernel_kib(_counter_rows(copy_write_csv), "WRITE_SIZE")
+    copy_f = max(cf.values())       # the 1 GiB copy dominates the calibration run
+    copy_w = max(cw.values())
+    scale_f = COPY_BYTES / copy_f   # bytes per counter unit, from the copy of known size
+    scale_w = COPY_BYTES / copy_w
+    out = {"_calibration": {"copy_bytes": COPY_BYTES, "fetch_size_per_copy": copy_f, "write_size_per_copy": copy_w,
+                            "fetch_scale": scale_f, "write_scale": scale_w}}
+    rec = {}
+    for key, kname in KERNEL_NAMES.items():
+        fk = [v for n, v in fetch.items() if kname in n]
+        wk = [v for n, v in write.items() if kname in n]
+        if not fk or not wk:
+            continue
+        fb, wb = max(fk) * scale_f, max(wk) * scale_w
+        rec[key] = {"fetch_bytes": fb, "write_bytes": wb, "bytes_per_launch": fb + wb,
+                    "source_hash": source_hash(KERNEL_SOURCES[key])}
+    try:
+        with open(COUNTERS) as f:
+            data = json.load(f)
+    except (OSError, ValueError):
+        data = {}
+    data[workload] = rec
+    data["_calibration"] = out["_calibration"]
+    with open(COUNTERS, "w") as f:
+        json.dump(data, f, indent=1)
+    print(json.dumps(data[workload]))
+
+
 def main():
     args = parse()
+    if args.ingest_counters:
+        ingest_counters(*args.ingest_counters, workload=args.workload)
+        return
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py runs on one GPU only: the eviction pass shards by sequence with no communication, "
@@ -166,81 +246,80 @@ def main():
     dq, dk, dv = dev(dec["q"]), dev(dec["k_new"]), dev(dec["v_new"])
     p = bd.problem_from(cfg)
     buf = bd.EvictionBuffers(p, None, tot, max(T, 1))
-    skip = not args.score_all_layers
     stream = torch.cuda.current_stream()
-    STAGES = ["score_stats", "score_text", "budget", "score_vision", "select", "compact"]
 
     def one_step(events=None):
-        rec = (lambda i: events[i].record(stream)) if events is not None else (lambda i: None)
-        rec(0)
-        buf.score(q_d, k_d, bd.SCORE_STATS)
-        rec(1)
-        buf.score(q_d, k_d, bd.SCORE_TEXT)
-        rec(2)
-        buf.budget()
-        rec(3)
-        buf.score(q_d, k_d, bd.SCORE_VISION, budgets=buf.budgets if skip else None)
-        rec(4)
-        buf.select()
-        rec(5)
-        buf.compact(k_d, v_d)
-        rec(6)
-        for s in range(T):
-            buf.decode(s, dq[s], dk[s], dv[s])
-            rec(7 + s)
+        names = []
+
+        def mark(name):
+            names.append(name)
+            if events is not None:
+                ev = torch.cuda.Event(enable_timing=True)
+                ev.record(stream)
+                events.append((name, ev))
+
+        mark("start")
+        sched = buf.evict(q_d, k_d, v_d, schedule=args.schedule, marks=mark)
+        for s_ in range(T):
+            buf.decode(s_, dq[s_], dk[s_], dv[s_])
+            mark("decode")
+        return sched
 
     for _ in range(args.warmup):
-        one_step()
+        sched = one_step()
     torch.cuda.synchronize()
-    nev = 7 + T
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
+    timed = [[] for _ in range(args.steps)]
     w0 = time.perf_counter()
     for k in range(args.steps):
-        one_step(evs[k])
+        sched = one_step(timed[k])
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
 
-    stage_ms = {s: 0.0 for s in STAGES}
+    stage_ms = {}
     dec_ms = 0.0
     step_ms = 0.0
-    for k in range(args.steps):
-        e = evs[k]
-        for i, s in enumerate(STAGES):
-            stage_ms[s] += e[i].elapsed_time(e[i + 1]) / args.steps
-        if T:
-            dec_ms += e[6].elapsed_time(e[6 + T]) / args.steps / T
-        step_ms += e[0].elapsed_time(e[nev - 1]) / args.steps
+    for evs in timed:
+        for (n0, e0), (n1, e1) in zip(evs[:-1], evs[1:]):
+            ms = e0.elapsed_time(e1) / args.steps
+            if n1 == "decode":
+                dec_ms += ms / max(T, 1)
+            else:
+                stage_ms[n1] = stage_ms.get(n1, 0.0) + ms
+        step_ms += evs[0][1].elapsed_time(evs[-1][1]) / args.steps
     evict_ms = sum(stage_ms.values())
     tokens_per_s = B * N / (evict_ms * 1e-3)
 
-    # algorithmic bytes per launch (K/V, queries and outputs read or written once)
+    # algorithmic bytes per launch: what the method must move, each once (K and the text
+    # queries for scoring, the retained K/V read and written for compaction, the pruned
+    # cache plus new tokens for a decode step), not what an implementation re-reads
     H, Hkv, D, Nq, Nv = cfg.heads_q, cfg.heads_kv, cfg.head_dim, cfg.n_qst, cfg.n_vis
     budgets = buf.budgets.cpu().numpy()
-    vis_layers = int((budgets > cfg.n_text).sum()) if skip else B * L
-    qq = B * L * H * Nq * D * 2
+    thr = buf.forced_or_text()
+    vis_layers = int((budgets > thr).sum()) if sched in ("two_step", "fused_text") else B * L
+    k_bytes = B * L * Hkv * N * D * 2
+    q_bytes = B * L * H * cfg.n_text * D * 2
     alg = {
-        "score_stats": B * L * Hkv * N * D * 2 + qq + B * L * H * Nq * 8,
-        "score_vision": vis_layers * (Hkv * Nv * D * 2 + H * Nq * D * 2 + 2 * Hkv * Nv * 4 + Nv * 4),
+        "score": k_bytes + q_bytes,
+        "score_text": k_bytes + q_bytes,
+        "score_stats": k_bytes + B * L * H * Nq * D * 2,
+        "score_vision": vis_layers * (Hkv * Nv * D * 2 + H * Nq * D * 2),
         "compact": 4 * B * tot * Hkv * D * 2,
         "decode": (B * tot + B * L * (T + 1) / 2.0) * Hkv * D * 4 + B * L * (H * D * 2 + 2 * Hkv * D * 2 + H * D * 4),
     }
-    per_launch_ms = {"score_stats": stage_ms["score_stats"], "score_vision": stage_ms["score_vision"],
-                     "compact": stage_ms["compact"], "decode": dec_ms}
-    launches = {"score_stats": 1, "score_vision": 1, "compact": 1, "decode": T}
     roofs = {}
-    for kname, ms in per_launch_ms.items():
+    for kname in ("score", "score_text", "score_stats", "score_vision", "compact", "decode"):
+        ms = dec_ms if kname == "decode" else stage_ms.get(kname, 0.0)
         if ms <= 0:
             continue
         gbs = alg[kname] / (ms * 1e-3) / 1e9
-        tr = traffic_for(kname, cfg.name)
         roofs[kname] = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                        "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": tr, "kernel": kname,
-                        "alg_bytes_per_launch": int(alg[kname]), "avg_launch_ms": round(ms, 4),
-                        "ms_per_step": round(ms * launches[kname], 4)}
+                        "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic_for(kname, cfg.name, T),
+                        "kernel": kname, "alg_bytes_per_launch": int(alg[kname]), "avg_launch_ms": round(ms, 4),
+                        "ms_per_step": round(ms * (T if kname == "decode" else 1), 4)}
     dominant = max(roofs, key=lambda k: roofs[k]["ms_per_step"])
+    score_ms = stage_ms.get("score", stage_ms.get("score_stats", 0.0))
     flops = 2.0 * B * L * H * D * (Nq * (cfg.n_sys + Nv) + Nq * (Nq + 1) / 2)
-    mfma_pct = flops / (stage_ms["score_stats"] * 1e-3) / (BF16_PEAK_TFLOPS * 1e12)
+    mfma_frac = flops / (score_ms * 1e-3) / (BF16_PEAK_TFLOPS * 1e12) if score_ms > 0 else None
 
     line = {
         "metric": METRIC,
@@ -259,11 +338,12 @@ def main():
                                f"{cfg.n_sys}+{Nv}+{Nq} tokens, retention {rho:g}, {T} decode steps",
                    "batch": B, "layers": L, "heads_q": H, "heads_kv": Hkv, "head_dim": D,
                    "n_sys": cfg.n_sys, "n_vis": Nv, "n_qst": Nq, "retention": rho, "total_budget_per_seq": tot,
-                   "decode_steps": T, "vision_scored_layers": vis_layers},
+                   "decode_steps": T, "vision_scored_layers": vis_layers, "schedule": sched},
         "evict_ms": round(evict_ms, 4),
         "decode_us_per_step": round(dec_ms * 1e3, 2),
         "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},
-        "score_stats_mfma_frac_of_peak": round(mfma_pct, 4),
+        "schedule": sched,
+        "scoring_mfma_frac_of_peak": None if mfma_frac is None else round(mfma_frac, 4),
         "roofline": roofs[dominant],
         "roofline_kernels": roofs,
         "wall_ms_per_step": round(wall / args.steps * 1e3, 3),

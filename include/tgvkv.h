@@ -84,7 +84,9 @@ enum {
     TGVKV_SCORE_STATS  = 1,  /* question-row softmax statistics over all visible keys        */
     TGVKV_SCORE_TEXT   = 2,  /* text scores s^T, weights w~, per-layer text->vision mass      */
     TGVKV_SCORE_VISION = 4,  /* text-weighted vision scores s^V                               */
-    TGVKV_SCORE_ALL    = 7
+    TGVKV_SCORE_ALL    = 7,
+    TGVKV_SCORE_FUSED  = 8   /* with ALL or STATS|TEXT: one persistent launch instead of one
+                                per phase (needs budgets_or_null == NULL)                     */
 };
 
 /* Which call a workspace is sized for. */
@@ -112,10 +114,15 @@ enum { TGVKV_CALL_SCORE = 0, TGVKV_CALL_DECODE = 1 };
  * budgets_or_null  int32 [B][L]: if given, the VISION phase skips every layer
  *                  whose budget leaves no room for vision tokens (budget <=
  *                  |forced U T|); s_vis of skipped layers is left untouched.
- * phases  any non-empty OR of TGVKV_SCORE_*.  Phases must run in the order
- *         STATS, TEXT, VISION, with the same workspace and outputs; a later
- *         phase reads what the earlier ones left there.  Pointers of phases
- *         not requested may be NULL (lse is needed by all three, w_txt by VISION).
+ * phases  any non-empty OR of STATS, TEXT, VISION, optionally with FUSED.
+ *         Phases must run in the order STATS, TEXT, VISION, with the same
+ *         workspace and outputs; a later phase reads what the earlier ones left
+ *         there.  Pointers of phases not requested may be NULL (lse is needed by
+ *         all three, w_txt by VISION).  FUSED (with ALL or STATS|TEXT, no budgets)
+ *         runs the phases as one persistent kernel whose workgroups take key
+ *         splits in ticket order; it is bit-for-bit a different summation order
+ *         of the same quantities and is slower on gfx950 than the per-phase
+ *         kernels, so it is never chosen implicitly.
  * workspace / workspace_bytes  >= tgvkv_workspace_size(p, o, TGVKV_CALL_SCORE).
  */
 tgvkv_status tgvkv_score(const tgvkv_problem* problem, const tgvkv_opts* opts, int32_t phases,

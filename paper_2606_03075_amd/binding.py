@@ -18,7 +18,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libtgvkv.so")
 
 TGVKV_OK, TGVKV_E_INVAL, TGVKV_E_UNSUPPORTED, TGVKV_E_WORKSPACE, TGVKV_E_CAPACITY, TGVKV_E_HIP = 0, -1, -2, -3, -4, -5
-SCORE_STATS, SCORE_TEXT, SCORE_VISION, SCORE_ALL = 1, 2, 4, 7
+SCORE_STATS, SCORE_TEXT, SCORE_VISION, SCORE_ALL, SCORE_FUSED = 1, 2, 4, 7, 8
 CALL_SCORE, CALL_DECODE = 0, 1
 
 EXPORTS = ("tgvkv_score", "tgvkv_budget", "tgvkv_select", "tgvkv_compact", "tgvkv_decode_attn",
@@ -248,14 +248,68 @@ class EvictionBuffers:
         tgvkv_compact(self.problem, self.opts, k, v, self.idx, self.budgets, self.idx_offsets, self.seg_offsets,
                       self.total_budget, self.decode_reserve, self.kc, self.vc, stream)
 
-    def evict(self, q_text, k, v, skip_text_only_layers=True, stream=None):
-        """Score (text stats, then budgets, then vision scores only where needed), select, compact."""
-        self.score(q_text, k, SCORE_STATS | SCORE_TEXT, stream=stream)
-        self.budget(stream)
-        self.score(q_text, k, SCORE_VISION, budgets=self.budgets if skip_text_only_layers else None,
-                   stream=stream)
+    def forced_or_text(self) -> int:
+        """|forced U T|: a layer needs vision scores only when its budget exceeds this."""
+        p, o = self.problem, self.opts
+        N = p.n_sys + p.n_vis + p.n_qst
+        n_sink = o.n_sink if o is not None else 0
+        n_recent = o.n_recent if o is not None else 0
+        fs = min(n_sink, N)
+        fr = max(N - n_recent, fs)
+        v0, v1 = p.n_sys, p.n_sys + p.n_vis
+        fv = max(0, min(fs, v1) - v0) + max(0, v1 - max(fr, v0))
+        return p.n_sys + p.n_qst + fv
+
+    def schedule(self) -> str:
+        """'two_step': text statistics and text scores, budgets, then vision scores only for the
+        layers whose budget reaches past the text (never more work than scoring every layer)."""
+        return "two_step"
+
+    def evict(self, q_text, k, v, schedule="auto", stream=None, marks=None):
+        """Score, budget, select and compact.
+
+        schedule: 'auto' (= 'two_step'), 'two_step', 'phases' (every scoring phase as its own
+        launch, vision scores for every layer), 'fused' (one persistent scoring launch) or
+        'fused_text' (persistent text pass, then vision scores where needed).  marks(name) is
+        called after each stage (for event timing).
+        """
+        mark = marks if marks is not None else (lambda name: None)
+        sched = self.schedule() if schedule == "auto" else schedule
+        if sched == "fused":
+            self.score(q_text, k, SCORE_ALL | SCORE_FUSED, stream=stream)
+            mark("score")
+            self.budget(stream)
+            mark("budget")
+        elif sched == "fused_text":
+            self.score(q_text, k, SCORE_STATS | SCORE_TEXT | SCORE_FUSED, stream=stream)
+            mark("score_text")
+            self.budget(stream)
+            mark("budget")
+            self.score(q_text, k, SCORE_VISION, budgets=self.budgets, stream=stream)
+            mark("score_vision")
+        elif sched == "two_step":
+            self.score(q_text, k, SCORE_STATS | SCORE_TEXT, stream=stream)
+            mark("score_text")
+            self.budget(stream)
+            mark("budget")
+            self.score(q_text, k, SCORE_VISION, budgets=self.budgets, stream=stream)
+            mark("score_vision")
+        elif sched == "phases":
+            self.score(q_text, k, SCORE_STATS, stream=stream)
+            mark("score_stats")
+            self.score(q_text, k, SCORE_TEXT, stream=stream)
+            mark("score_text")
+            self.budget(stream)
+            mark("budget")
+            self.score(q_text, k, SCORE_VISION, stream=stream)
+            mark("score_vision")
+        else:
+            raise ValueError(f"unknown schedule {schedule!r}")
         self.select(stream)
+        mark("select")
         self.compact(k, v, stream)
+        mark("compact")
+        return sched
 
     def decode(self, step, q, k_new, v_new, stream=None):
         tgvkv_decode_attn(self.problem, self.opts, self.kc, self.vc, self.budgets, self.seg_offsets,

@@ -5,6 +5,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdint>
+#include <cstdlib>
 #include <cstring>
 
 #include "tgvkv.h"
@@ -88,6 +89,8 @@ struct ScoreWs {
     float* colsum;
     float* vmh;
     float* part;
+    float* part_stats;  // fused path: per-split row statistics
+    int* sync;          // fused path: ticket, error word and completion counters
     size_t bytes;
 };
 
@@ -103,7 +106,17 @@ ScoreWs score_workspace(const Shape& s, const RowPlan& rp, void* base) {
     w.vmh = reinterpret_cast<float*>(b ? b + off : nullptr);
     off = align_up(off + sizeof(float) * bl * s.H);
     w.part = reinterpret_cast<float*>(b ? b + off : nullptr);
-    off = align_up(off + sizeof(float) * bl * s.Hkv * (size_t)rp.rowgroups * s.Nv);
+    off = align_up(off + sizeof(float) * bl * s.Hkv * (size_t)std::max(rp.rowgroups, 1) * s.Nv);
+    w.part_stats = nullptr;
+    w.sync = nullptr;
+    if (tgvkv::fused_eligible(s, rp)) {
+        const tgvkv::FusedPlan fp = tgvkv::plan_fused(s, true);
+        const size_t rows = (size_t)s.G * ((s.Nq + 15) / 16) * 16;
+        w.part_stats = reinterpret_cast<float*>(b ? b + off : nullptr);
+        off = align_up(off + sizeof(float) * bl * s.Hkv * (size_t)fp.sa * rows * 3);
+        w.sync = reinterpret_cast<int*>(b ? b + off : nullptr);
+        off = align_up(off + sizeof(int) * (size_t)tgvkv::fused_sync_words(s));
+    }
     w.bytes = off;
     return w;
 }
@@ -151,7 +164,12 @@ tgvkv_status tgvkv_score(const tgvkv_problem* problem, const tgvkv_opts* opts, i
     Shape s;
     tgvkv_status st = make_shape(problem, opts, &s);
     if (st != TGVKV_OK) return st;
+    const bool want_fused = (phases & TGVKV_SCORE_FUSED) != 0;
+    phases &= ~TGVKV_SCORE_FUSED;
     if (phases < 1 || phases > TGVKV_SCORE_ALL) return TGVKV_E_INVAL;
+    if (want_fused && (budgets_or_null != nullptr ||
+                       (phases != TGVKV_SCORE_ALL && phases != (TGVKV_SCORE_STATS | TGVKV_SCORE_TEXT))))
+        return TGVKV_E_INVAL;
     if (s.B == 0) return TGVKV_OK;
     const bool text_rows = s.Nt > 0;
     if (q_text == nullptr && text_rows) return TGVKV_E_INVAL;
@@ -169,6 +187,14 @@ tgvkv_status tgvkv_score(const tgvkv_problem* problem, const tgvkv_opts* opts, i
     const uint16_t* q = static_cast<const uint16_t*>(q_text);
     const uint16_t* kk = static_cast<const uint16_t*>(k);
     const int32_t vthr = forced_or_text_count(s);
+
+    // One persistent kernel when asked for and the shape allows it (one row group per unit).
+    if (want_fused && w.sync != nullptr) {
+        tgvkv::FusedPlan fp = tgvkv::plan_fused(s, (phases & TGVKV_SCORE_VISION) != 0);
+        if (const char* lag = std::getenv("TGVKV_FUSED_LAG")) fp.lag = std::max(0, std::atoi(lag));
+        tgvkv::FusedPtrs fptr{q, kk, lse, s_txt, w_txt, tv_mass, s_vis, w.part_stats, w.colsum, w.vmh, w.part, w.sync};
+        return hip_status(tgvkv::launch_score_fused(s, rp, fp, fptr, stream));
+    }
 
     hipError_t e = hipSuccess;
     if ((phases & TGVKV_SCORE_STATS) && e == hipSuccess) e = tgvkv::launch_score_stats(s, rp, q, kk, lse, w.vm, stream);

@@ -5,10 +5,14 @@
 // counts that retention (Eq. (10)) compares with N_t come from: a per-layer
 // floor (forced tokens) given first; the rest water-filled in proportion to
 // the shares with a cap of N per layer; largest-remainder rounding with ties to
-// the lower layer.  One thread per sequence runs the whole computation in
-// float64 with no contraction, in a fixed order, so the result is a pure
-// function of the float32 masses.  L is small (tens of layers): this is a
-// latency-bound kernel by construction.
+// the lower layer.
+//
+// One workgroup per sequence, layers spread over the threads.  Every float64
+// sum runs on one thread in layer order and no operation is contracted, so the
+// budgets are a pure function of the float32 masses (element-wise steps are
+// order-free).  The largest-remainder step ranks each eligible layer by
+// (fraction desc, layer asc) with an all-pairs count, which gives the same set
+// as sorting.
 #pragma clang fp contract(off)
 
 #include "tgvkv_device.h"
@@ -18,16 +22,18 @@ namespace tgvkv {
 namespace {
 
 constexpr int kMaxLayers = 512;
+constexpr int kThreads = 256;
 
-__global__ __launch_bounds__(64) void budget_kernel(Shape s, const float* __restrict__ tv_mass, long long total,
-                                                    int reserve, int n_forced, int32_t* __restrict__ budgets,
-                                                    int64_t* __restrict__ idx_off, int64_t* __restrict__ seg_off) {
+__global__ __launch_bounds__(kThreads) void budget_kernel(Shape s, const float* __restrict__ tv_mass, long long total,
+                                                          int reserve, int n_forced, int32_t* __restrict__ budgets,
+                                                          int64_t* __restrict__ idx_off,
+                                                          int64_t* __restrict__ seg_off) {
     __shared__ double f[kMaxLayers];
     __shared__ double x[kMaxLayers];
     __shared__ long long bcount[kMaxLayers];
     __shared__ unsigned char active[kMaxLayers];
-    __shared__ unsigned char taken[kMaxLayers];
-    if (threadIdx.x != 0) return;
+    __shared__ double sh_sum;
+    const int tid = threadIdx.x;
     const int b = blockIdx.x;
     const int L = s.L;
     const long long N = s.N;
@@ -37,80 +43,102 @@ __global__ __launch_bounds__(64) void budget_kernel(Shape s, const float* __rest
     if (N < F) F = N;
     const long long cap = N - F;
     const long long R = total - (long long)L * F;
-
-    double S = 0.0;
-    for (int l = 0; l < L; ++l) {
-        const float mv = tv_mass[(size_t)b * L + l];
-        const double m = (isfinite(mv) && mv > 0.f) ? (double)mv : 0.0;
-        x[l] = m;  // masses, temporarily
-        S += m;
-    }
-    for (int l = 0; l < L; ++l) f[l] = S > 0.0 ? x[l] / S : 1.0 / (double)L;
-
-    for (int l = 0; l < L; ++l) active[l] = 1;
-    int n_active = L;
-    double remaining = (double)R;
     const double capd = (double)cap;
+
+    for (int l = tid; l < L; l += kThreads) {
+        const float mv = tv_mass[(size_t)b * L + l];
+        x[l] = (isfinite(mv) && mv > 0.f) ? (double)mv : 0.0;  // masses, for now
+        active[l] = 1;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        double S = 0.0;
+        for (int l = 0; l < L; ++l) S += x[l];
+        sh_sum = S;
+    }
+    __syncthreads();
+    const double S = sh_sum;
+    for (int l = tid; l < L; l += kThreads) f[l] = S > 0.0 ? x[l] / S : 1.0 / (double)L;
+    __syncthreads();
+
+    // water-fill: capped layers are fixed and the remainder is re-shared
+    double remaining = (double)R;
+    int n_active = L;
     while (n_active > 0) {
-        double Fa = 0.0;
-        for (int l = 0; l < L; ++l)
-            if (active[l]) Fa += f[l];
-        for (int l = 0; l < L; ++l)
-            if (active[l]) x[l] = Fa > 0.0 ? (remaining * f[l]) / Fa : remaining / (double)n_active;
-        bool any = false;
-        for (int l = 0; l < L; ++l) {
-            taken[l] = active[l] && x[l] > capd;
-            any = any || taken[l];
+        if (tid == 0) {
+            double Fa = 0.0;
+            for (int l = 0; l < L; ++l)
+                if (active[l]) Fa += f[l];
+            sh_sum = Fa;
         }
-        if (!any) break;
-        for (int l = 0; l < L; ++l) {
-            if (taken[l]) {
-                x[l] = capd;
-                active[l] = 0;
-                remaining -= capd;
-                --n_active;
+        __syncthreads();
+        const double Fa = sh_sum;
+        int over = 0;
+        for (int l = tid; l < L; l += kThreads) {
+            if (active[l]) {
+                x[l] = Fa > 0.0 ? (remaining * f[l]) / Fa : remaining / (double)n_active;
+                over += x[l] > capd;
             }
         }
+        const int n_over = __syncthreads_count(over);
+        if (n_over == 0) break;
+        for (int l = tid; l < L; l += kThreads) {
+            if (active[l] && x[l] > capd) {
+                x[l] = capd;
+                active[l] = 0;
+            }
+        }
+        // remaining and cap are integers below 2^53: the subtraction is exact in any order
+        remaining -= capd * (double)n_over;
+        n_active -= n_over;
+        __syncthreads();
     }
 
-    long long sum = 0;
-    for (int l = 0; l < L; ++l) {
+    int part = 0;
+    for (int l = tid; l < L; l += kThreads) {
         const double fl = floor(x[l]);
         long long base = (long long)fl;
         if (base > cap) base = cap;
         bcount[l] = F + base;
-        x[l] = x[l] - fl;  // fractional part
-        taken[l] = 0;
-        sum += bcount[l];
+        x[l] = x[l] - fl;  // fractional part from here on
+        part += (int)base;
     }
-    long long r = total - sum;
-    // +1 to the r layers with the largest fractional parts (ties: lower layer), below the cap
-    while (r > 0) {
-        int best = -1;
-        for (int l = 0; l < L; ++l) {
-            if (taken[l] || bcount[l] >= N) continue;
-            if (best < 0 || x[l] > x[best]) best = l;
-        }
-        if (best < 0) break;  // cannot happen when total <= L*N
-        taken[best] = 1;
-        ++bcount[best];
-        --r;
-    }
+    __shared__ long long sh_base;
+    if (tid == 0) sh_base = 0;
+    __syncthreads();
+    atomicAdd(reinterpret_cast<unsigned long long*>(&sh_base), (unsigned long long)part);
+    __syncthreads();
+    const long long r = total - ((long long)L * F + sh_base);
 
-    const long long g = s.ngroups;
-    long long io = (long long)b * total * g;
-    long long so = (long long)b * (total + (long long)L * reserve);
-    for (int l = 0; l < L; ++l) {
-        const size_t bl = (size_t)b * L + l;
-        budgets[bl] = (int32_t)bcount[l];
-        idx_off[bl] = io;
-        seg_off[bl] = so;
-        io += g * bcount[l];
-        so += bcount[l] + reserve;
+    // +1 to the r eligible layers ranked first by (fraction desc, layer asc)
+    for (int l = tid; l < L; l += kThreads) {
+        if (bcount[l] >= N) continue;
+        const double fr = x[l];
+        int rank = 0;
+        for (int j = 0; j < L; ++j) {
+            if (bcount[j] >= N) continue;
+            rank += (x[j] > fr) || (x[j] == fr && j < l);
+        }
+        if (rank < r) bcount[l] += 1;
     }
-    if (b == s.B - 1) {
-        idx_off[(size_t)s.B * L] = (long long)s.B * total * g;
-        seg_off[(size_t)s.B * L] = (long long)s.B * (total + (long long)L * reserve);
+    __syncthreads();
+
+    if (tid == 0) {
+        const long long g = s.ngroups;
+        long long io = (long long)b * total * g;
+        long long so = (long long)b * (total + (long long)L * reserve);
+        for (int l = 0; l < L; ++l) {
+            const size_t bl = (size_t)b * L + l;
+            budgets[bl] = (int32_t)bcount[l];
+            idx_off[bl] = io;
+            seg_off[bl] = so;
+            io += g * bcount[l];
+            so += bcount[l] + reserve;
+        }
+        if (b == s.B - 1) {
+            idx_off[(size_t)s.B * L] = (long long)s.B * total * g;
+            seg_off[(size_t)s.B * L] = (long long)s.B * (total + (long long)L * reserve);
+        }
     }
 }
 
@@ -119,8 +147,8 @@ __global__ __launch_bounds__(64) void budget_kernel(Shape s, const float* __rest
 hipError_t launch_budget(const Shape& s, const float* tv_mass, int64_t total, int32_t reserve, int32_t n_forced,
                          int32_t* budgets, int64_t* idx_off, int64_t* seg_off, hipStream_t st) {
     if (s.B == 0) return hipSuccess;
-    hipLaunchKernelGGL(budget_kernel, dim3(s.B), dim3(64), 0, st, s, tv_mass, (long long)total, reserve, n_forced,
-                       budgets, idx_off, seg_off);
+    hipLaunchKernelGGL(budget_kernel, dim3(s.B), dim3(kThreads), 0, st, s, tv_mass, (long long)total, reserve,
+                       n_forced, budgets, idx_off, seg_off);
     return hipGetLastError();
 }
 

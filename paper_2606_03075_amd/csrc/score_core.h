@@ -1,0 +1,448 @@
+// Device building blocks of the TWR / TVB scoring passes, shared by the
+// phase-by-phase kernels (score.hip) and the fused persistent kernel
+// (score_fused.hip).
+//
+// A "unit" is one (sequence b, layer l, KV head) slice: bl = b * L + l.  Its
+// question rows (query heads sharing the KV head x question tokens) are cut into
+// 16-row blocks, QB = ceil(N_q / 16) per head; block rb covers head rb / QB and
+// question indices (rb % QB) * 16 .. + 15.  The 4 waves of a workgroup split the
+// blocks into RSETS row sets of up to NSLOT blocks each and, when there are few
+// blocks, each 64-key tile into KS key parts (RSETS * KS = 4).
+//
+// MFMA layout: v_mfma_f32_16x16x32_bf16.  A 64-key tile of K sits in LDS with
+// rows padded by 16 bytes (the 16 lanes reading one 16-byte column chunk of 16
+// consecutive keys then hit distinct banks); the question rows stay in
+// registers for the whole sweep.  The statistics sweep computes C[key][row]
+// (keys on the M side) so that each lane owns one row and keeps its running
+// max / sum with no cross-lane traffic in the loop; the vision sweep computes
+// C[row][key] so that each lane owns one key and sums its column in registers.
+#pragma once
+
+#include "tgvkv_device.h"
+#include "tgvkv_shape.h"
+
+namespace tgvkv {
+namespace core {
+
+constexpr int kThreads = 256;
+constexpr int kTile = 64;  // keys per LDS tile
+
+template <int D>
+struct Geo {
+    static constexpr int KSTEPS = D / 32;                  // MFMA k-steps over the head dim
+    static constexpr int CPR = D / 8;                      // 16-byte chunks per key row
+    static constexpr int ROWB = D * 2 + 16;                // padded LDS row, bytes
+    static constexpr int TILE_BYTES = kTile * ROWB;
+    static constexpr int LOADS = kTile * CPR / kThreads;   // 16-byte loads per thread per tile
+};
+
+template <int D>
+__device__ __forceinline__ void load_tile_regs(u32x4 (&r)[Geo<D>::LOADS], const uint16_t* kbase, int key0,
+                                               int key_last, int tid) {
+#pragma unroll
+    for (int it = 0; it < Geo<D>::LOADS; ++it) {
+        const int c = it * kThreads + tid;
+        const int row = c / Geo<D>::CPR, cc = c % Geo<D>::CPR;
+        const int key = min(key0 + row, key_last);
+        r[it] = load16(kbase + (size_t)key * D + cc * 8);
+    }
+}
+
+template <int D>
+__device__ __forceinline__ void store_tile_lds(char* buf, const u32x4 (&r)[Geo<D>::LOADS], int tid) {
+#pragma unroll
+    for (int it = 0; it < Geo<D>::LOADS; ++it) {
+        const int c = it * kThreads + tid;
+        const int row = c / Geo<D>::CPR, cc = c % Geo<D>::CPR;
+        store16(buf + row * Geo<D>::ROWB + cc * 16, r[it]);
+    }
+}
+
+__device__ __forceinline__ bf16x8 zero_frag() {
+    u32x4 z = {0u, 0u, 0u, 0u};
+    return as_bf16x8(z);
+}
+
+template <int D>
+__device__ __forceinline__ void load_kfrag(bf16x8 (&kf)[Geo<D>::KSTEPS], const char* buf, int kb, int lane) {
+    const char* src = buf + (kb * 16 + (lane & 15)) * Geo<D>::ROWB + (lane >> 4) * 16;
+#pragma unroll
+    for (int ks = 0; ks < Geo<D>::KSTEPS; ++ks) kf[ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(src + ks * 64));
+}
+
+// Question-row fragments of the row set of this wave (lane: row lane & 15 of each block).
+template <int D, int NSLOT, int KS>
+__device__ __forceinline__ void load_qrows(const Shape& s, const uint16_t* q_text, int bl, int kvh, int rb0,
+                                           bf16x8 (&qf)[NSLOT][Geo<D>::KSTEPS], int (&qrow)[NSLOT]) {
+    constexpr int RSETS = 4 / KS;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int rs = wave % RSETS;
+    const int QB = (s.Nq + 15) >> 4;
+    const int NB = s.G * QB;
+#pragma unroll
+    for (int sl = 0; sl < NSLOT; ++sl) {
+        const int rb = rb0 + rs + sl * RSETS;
+        const int g = rb / QB;
+        const int qi = (rb % QB) * 16 + (lane & 15);
+        qrow[sl] = qi;
+        const bool valid = rb < NB && qi < s.Nq;
+        const uint16_t* qp = q_text + (((size_t)bl * s.H + kvh * s.G + (valid ? g : 0)) * s.Nt + s.Ns +
+                                       (valid ? qi : 0)) * D + (lane >> 4) * 8;
+#pragma unroll
+        for (int ks = 0; ks < Geo<D>::KSTEPS; ++ks)
+            qf[sl][ks] = valid ? as_bf16x8(load16(qp + ks * 32)) : zero_frag();
+    }
+}
+
+// Statistics sweep over keys [kbeg, kend) of one unit (kbeg a multiple of kTile):
+// per question row the running max (base-2 units), the sum of exp over visible
+// keys and the same sum over vision keys.  On return the key-part-0 waves hold,
+// in lanes 0..15, the merged statistics of their rows; the workgroup is synced.
+template <int D, int NSLOT, int KS>
+__device__ void stats_sweep(const Shape& s, const uint16_t* kbase, int kbeg, int kend,
+                            const bf16x8 (&qf)[NSLOT][Geo<D>::KSTEPS], const int (&qrow)[NSLOT], int rb0, int NB,
+                            char (*tiles)[Geo<D>::TILE_BYTES], float (&m)[NSLOT], float (&lsum)[NSLOT],
+                            float (&vsum)[NSLOT]) {
+    using GG = Geo<D>;
+    constexpr int RSETS = 4 / KS;
+    constexpr int KBW = 4 / KS;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int rs = wave % RSETS, kp = wave / RSETS;
+    const int vis0 = s.Ns, vis1 = s.Ns + s.Nv;
+#pragma unroll
+    for (int sl = 0; sl < NSLOT; ++sl) {
+        m[sl] = kNegInf;
+        lsum[sl] = 0.f;
+        vsum[sl] = 0.f;
+    }
+    const int ntiles = (kend - kbeg + kTile - 1) / kTile;
+    u32x4 pre[GG::LOADS];
+    if (ntiles > 0) {
+        load_tile_regs<D>(pre, kbase, kbeg, kend - 1, tid);
+        store_tile_lds<D>(tiles[0], pre, tid);
+    }
+    __syncthreads();
+    for (int t = 0; t < ntiles; ++t) {
+        const char* buf = tiles[t & 1];
+        const int key0 = kbeg + t * kTile;
+        if (t + 1 < ntiles) load_tile_regs<D>(pre, kbase, key0 + kTile, kend - 1, tid);
+        const bool pure_vis = key0 >= vis0 && key0 + kTile <= vis1 && key0 + kTile <= kend;
+#pragma unroll
+        for (int kbi = 0; kbi < KBW; ++kbi) {
+            const int kb = kp + kbi * KS;
+            bf16x8 kf[GG::KSTEPS];
+            load_kfrag<D>(kf, buf, kb, lane);
+            const int kfirst = key0 + kb * 16 + (lane >> 4) * 4;  // key of accumulator element 0
+#pragma unroll
+            for (int sl = 0; sl < NSLOT; ++sl) {
+                if (rb0 + rs + sl * RSETS >= NB) continue;
+                f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(kf[ks], qf[sl][ks], acc);
+                if (pure_vis) {
+                    const float z0 = acc[0] * s.scale2, z1 = acc[1] * s.scale2;
+                    const float z2 = acc[2] * s.scale2, z3 = acc[3] * s.scale2;
+                    const float mx = fmaxf(fmaxf(z0, z1), fmaxf(z2, z3));
+                    if (mx > m[sl]) {
+                        const float sc = fast_exp2(m[sl] - mx);
+                        lsum[sl] *= sc;
+                        vsum[sl] *= sc;
+                        m[sl] = mx;
+                    }
+                    const float e = (fast_exp2(z0 - m[sl]) + fast_exp2(z1 - m[sl])) +
+                                    (fast_exp2(z2 - m[sl]) + fast_exp2(z3 - m[sl]));
+                    lsum[sl] += e;
+                    vsum[sl] += e;
+                } else {
+                    float z[4];
+                    bool ok[4], isv[4];
+                    float mx = kNegInf;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const int key = kfirst + j;
+                        ok[j] = key < kend && (key < vis1 || key - vis1 <= qrow[sl]);
+                        isv[j] = key >= vis0 && key < vis1;
+                        z[j] = ok[j] ? acc[j] * s.scale2 : kNegInf;
+                        mx = fmaxf(mx, z[j]);
+                    }
+                    if (mx > m[sl]) {
+                        const float sc = fast_exp2(m[sl] - mx);
+                        lsum[sl] *= sc;
+                        vsum[sl] *= sc;
+                        m[sl] = mx;
+                    }
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        if (ok[j]) {
+                            const float e = fast_exp2(z[j] - m[sl]);
+                            lsum[sl] += e;
+                            if (isv[j]) vsum[sl] += e;
+                        }
+                    }
+                }
+            }
+        }
+        if (t + 1 < ntiles) store_tile_lds<D>(tiles[(t + 1) & 1], pre, tid);
+        __syncthreads();
+    }
+    // the four lane quarters of a wave saw different keys of the same rows
+#pragma unroll
+    for (int sl = 0; sl < NSLOT; ++sl) {
+#pragma unroll
+        for (int off = 16; off < 64; off <<= 1) {
+            const float m2 = shfl_xor(m[sl], off), l2 = shfl_xor(lsum[sl], off), v2 = shfl_xor(vsum[sl], off);
+            merge_stats(m[sl], lsum[sl], vsum[sl], m2, l2, v2);
+        }
+    }
+    if (KS > 1) {
+        // waves of other key parts hand their partials to the key-part-0 wave of their row set
+        float* red = reinterpret_cast<float*>(tiles[0]);  // [wave][NSLOT][16][3]
+        if (kp > 0 && lane < 16) {
+#pragma unroll
+            for (int sl = 0; sl < NSLOT; ++sl) {
+                float* r = red + ((wave * NSLOT + sl) * 16 + lane) * 3;
+                r[0] = m[sl];
+                r[1] = lsum[sl];
+                r[2] = vsum[sl];
+            }
+        }
+        __syncthreads();
+        if (kp == 0 && lane < 16) {
+            for (int p = 1; p < KS; ++p) {
+                const int w2 = p * RSETS + rs;
+#pragma unroll
+                for (int sl = 0; sl < NSLOT; ++sl) {
+                    const float* r = red + ((w2 * NSLOT + sl) * 16 + lane) * 3;
+                    merge_stats(m[sl], lsum[sl], vsum[sl], r[0], r[1], r[2]);
+                }
+            }
+        }
+        __syncthreads();
+    }
+}
+
+// Per-lane row coefficients of the vision sweep: the accumulator rows of a lane
+// are 4*(lane/16) + j of each block; lse2 in base-2 units, coef = w~_i / heads.
+template <int NSLOT, int KS>
+__device__ __forceinline__ void load_row_coefs(const Shape& s, int bl, int kvh, int rb0, const float* lse,
+                                               const float* w_txt, float (&lse2)[NSLOT][4],
+                                               float (&coef)[NSLOT][4]) {
+    constexpr int RSETS = 4 / KS;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int rs = wave % RSETS;
+    const int QB = (s.Nq + 15) >> 4;
+    const int NB = s.G * QB;
+    const float inv_heads = s.head_mode == 0 ? 1.0f / (float)s.H : 1.0f / (float)s.G;
+    const size_t wrow = s.head_mode == 0 ? (size_t)bl * s.Nt : ((size_t)bl * s.Hkv + kvh) * s.Nt;
+#pragma unroll
+    for (int sl = 0; sl < NSLOT; ++sl) {
+        const int rb = rb0 + rs + sl * RSETS;
+        const int g = rb / QB;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int qj = (rb % QB) * 16 + (lane >> 4) * 4 + j;
+            lse2[sl][j] = 0.f;
+            coef[sl][j] = 0.f;
+            if (rb < NB && qj < s.Nq) {
+                const size_t head = (size_t)bl * s.H + kvh * s.G + g;
+                lse2[sl][j] = lse[head * s.Nt + s.Ns + qj] * kLog2e;
+                coef[sl][j] = w_txt[wrow + s.Ns + qj] * inv_heads;
+            }
+        }
+    }
+}
+
+// Vision sweep over vision keys [vbeg, vend) (vbeg a multiple of kTile; kvis
+// points at the first vision key of the unit): out[j] = sum over this
+// workgroup's rows of coef * exp(z - lse), for every key j of the range.
+template <int D, int NSLOT, int KS>
+__device__ void vision_sweep(const Shape& s, const uint16_t* kvis, int vbeg, int vend,
+                             const bf16x8 (&qf)[NSLOT][Geo<D>::KSTEPS], const float (&lse2)[NSLOT][4],
+                             const float (&coef)[NSLOT][4], int rb0, int NB, char (*tiles)[Geo<D>::TILE_BYTES],
+                             float (*red)[4 / KS][kTile], float* out) {
+    using GG = Geo<D>;
+    constexpr int RSETS = 4 / KS;
+    constexpr int KBW = 4 / KS;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int rs = wave % RSETS, kp = wave / RSETS;
+    const int ntiles = (vend - vbeg + kTile - 1) / kTile;
+    u32x4 pre[GG::LOADS];
+    if (ntiles > 0) {
+        load_tile_regs<D>(pre, kvis, vbeg, vend - 1, tid);
+        store_tile_lds<D>(tiles[0], pre, tid);
+    }
+    __syncthreads();
+    for (int t = 0; t < ntiles; ++t) {
+        const char* buf = tiles[t & 1];
+        const int key0 = vbeg + t * kTile;
+        if (t + 1 < ntiles) load_tile_regs<D>(pre, kvis, key0 + kTile, vend - 1, tid);
+#pragma unroll
+        for (int kbi = 0; kbi < KBW; ++kbi) {
+            const int kb = kp + kbi * KS;
+            bf16x8 kf[GG::KSTEPS];
+            load_kfrag<D>(kf, buf, kb, lane);
+            float col = 0.f;
+#pragma unroll
+            for (int sl = 0; sl < NSLOT; ++sl) {
+                if (rb0 + rs + sl * RSETS >= NB) continue;
+                f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(qf[sl][ks], kf[ks], acc);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) col += coef[sl][j] * fast_exp2(acc[j] * s.scale2 - lse2[sl][j]);
+            }
+            col += shfl_xor(col, 16);
+            col += shfl_xor(col, 32);
+            if (lane < 16) red[t & 1][rs][kb * 16 + lane] = col;
+        }
+        if (t + 1 < ntiles) store_tile_lds<D>(tiles[(t + 1) & 1], pre, tid);
+        __syncthreads();
+        if (tid < kTile) {
+            const int key = key0 + tid;
+            if (key < vend) {
+                float a = 0.f;
+#pragma unroll
+                for (int r = 0; r < RSETS; ++r) a += red[t & 1][r][tid];
+                out[key] = a;
+            }
+        }
+    }
+    __syncthreads();
+}
+
+// Text x text pass of one unit.  lse2s [G][N_t] (LDS, base-2 units) must hold the
+// question rows' normalisers.  Computes the system rows' normalisers (system
+// rows see only system keys, causally) into lse2s and lse, then the column sums
+// of the text->text probabilities per query head into ws_colsum [.., N_t].
+template <int D>
+__device__ void text_pass(const Shape& s, int bl, int kvh, const uint16_t* __restrict__ q_text,
+                          const uint16_t* __restrict__ k, float* __restrict__ lse, float* lse2s,
+                          float* __restrict__ ws_colsum) {
+    using GG = Geo<D>;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const size_t head0 = (size_t)bl * s.H + kvh * s.G;
+    const uint16_t* kbase = k + ((size_t)bl * s.Hkv + kvh) * (size_t)s.N * D;
+    const int koff = (lane >> 4) * 8;
+
+    const int SB = (s.Ns + 15) >> 4;
+    for (int item = wave; item < s.G * SB; item += 4) {
+        const int g = item / SB, rb = item % SB;
+        const int i = rb * 16 + (lane & 15);
+        const bool rv = i < s.Ns;
+        bf16x8 qf[GG::KSTEPS];
+        const uint16_t* qp = q_text + ((head0 + g) * s.Nt + (rv ? i : 0)) * D + koff;
+#pragma unroll
+        for (int ks = 0; ks < GG::KSTEPS; ++ks) qf[ks] = rv ? as_bf16x8(load16(qp + ks * 32)) : zero_frag();
+        float m = kNegInf, l = 0.f, dummy = 0.f;
+        for (int kb = 0; kb <= rb; ++kb) {
+            const int jc = min(kb * 16 + (lane & 15), s.Ns - 1);
+            bf16x8 kf[GG::KSTEPS];
+#pragma unroll
+            for (int ks = 0; ks < GG::KSTEPS; ++ks)
+                kf[ks] = as_bf16x8(load16(kbase + (size_t)jc * D + koff + ks * 32));
+            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(kf[ks], qf[ks], acc);
+            float z[4];
+            float mx = kNegInf;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int key = kb * 16 + (lane >> 4) * 4 + j;
+                z[j] = (key <= i && key < s.Ns) ? acc[j] * s.scale2 : kNegInf;
+                mx = fmaxf(mx, z[j]);
+            }
+            if (mx > m) {
+                l *= fast_exp2(m - mx);
+                m = mx;
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (z[j] != kNegInf) l += fast_exp2(z[j] - m);
+        }
+#pragma unroll
+        for (int off = 16; off < 64; off <<= 1) {
+            const float m2 = shfl_xor(m, off), l2 = shfl_xor(l, off), d2 = shfl_xor(dummy, off);
+            merge_stats(m, l, dummy, m2, l2, d2);
+        }
+        if (lane < 16 && rv) {
+            const float L2 = m + log2f(l);
+            lse2s[g * s.Nt + i] = L2;
+            lse[(head0 + g) * s.Nt + i] = L2 * kLn2;
+        }
+    }
+    __syncthreads();
+
+    const int TB = (s.Nt + 15) >> 4;
+    for (int item = wave; item < s.G * TB; item += 4) {
+        const int g = item / TB, kb = item % TB;
+        const int j = kb * 16 + (lane & 15);
+        const int jc = min(j, s.Nt - 1);
+        const int pos = jc < s.Ns ? jc : jc + s.Nv;
+        bf16x8 kf[GG::KSTEPS];
+#pragma unroll
+        for (int ks = 0; ks < GG::KSTEPS; ++ks)
+            kf[ks] = as_bf16x8(load16(kbase + (size_t)pos * D + koff + ks * 32));
+        float col = 0.f;
+        for (int rb = kb; rb < TB; ++rb) {
+            const int i = rb * 16 + (lane & 15);
+            const bool rv = i < s.Nt;
+            bf16x8 qf[GG::KSTEPS];
+            const uint16_t* qp = q_text + ((head0 + g) * s.Nt + (rv ? i : 0)) * D + koff;
+#pragma unroll
+            for (int ks = 0; ks < GG::KSTEPS; ++ks) qf[ks] = rv ? as_bf16x8(load16(qp + ks * 32)) : zero_frag();
+            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(qf[ks], kf[ks], acc);
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+                const int ii = rb * 16 + (lane >> 4) * 4 + jj;
+                if (ii < s.Nt && j <= ii) col += fast_exp2(acc[jj] * s.scale2 - lse2s[g * s.Nt + ii]);
+            }
+        }
+        col += shfl_xor(col, 16);
+        col += shfl_xor(col, 32);
+        if (lane < 16 && j < s.Nt) ws_colsum[(head0 + g) * s.Nt + j] = col;
+    }
+    __syncthreads();
+}
+
+// Head means of one (sequence, layer, group): s^T (Eq. (9)), w and w~ (Eq. (7)),
+// and for group 0 the layer's text->vision mass (Eq. (5)-(6)).  red: 256 floats of LDS.
+__device__ inline void finalize_group(const Shape& s, int bl, int gi, const float* ws_colsum, const float* ws_vmh,
+                                      float* s_txt, float* w_txt, float* tv_mass, float* red) {
+    const int tid = threadIdx.x;
+    const int h0 = s.head_mode == 0 ? 0 : gi * s.G;
+    const int hn = s.head_mode == 0 ? s.H : s.G;
+    const float inv = 1.0f / (float)hn;
+    const float* cs = ws_colsum + ((size_t)bl * s.H + h0) * s.Nt;
+    const size_t obase = ((size_t)bl * s.ngroups + gi) * s.Nt;
+    float part = 0.f;
+    for (int j = tid; j < s.Nt; j += kThreads) {
+        float a = 0.f;
+        for (int h = 0; h < hn; ++h) a += cs[(size_t)h * s.Nt + j];
+        const float st = a * inv;
+        s_txt[obase + j] = st;
+        part += st / (float)(s.Nt - j);
+    }
+    red[tid] = part;
+    __syncthreads();
+    for (int o = kThreads / 2; o > 0; o >>= 1) {
+        if (tid < o) red[tid] += red[tid + o];
+        __syncthreads();
+    }
+    const float W = red[0];
+    for (int j = tid; j < s.Nt; j += kThreads) {
+        const float w = s_txt[obase + j] / (float)(s.Nt - j);
+        w_txt[obase + j] = W > 0.f ? w / W : 0.f;
+    }
+    if (gi == 0 && tid == 0) {
+        float a = 0.f;
+        if (s.Nt > 0)
+            for (int h = 0; h < s.H; ++h) a += ws_vmh[(size_t)bl * s.H + h];
+        tv_mass[bl] = a / (float)s.H;
+    }
+    __syncthreads();
+}
+
+}  // namespace core
+}  // namespace tgvkv

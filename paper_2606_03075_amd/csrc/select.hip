@@ -2,12 +2,14 @@
 //
 // One workgroup per (sequence, layer, group).  The retained set is forced
 // positions first (first n_sink, last n_recent), then either the top text tokens
-// by s^T (budget does not cover the remaining text) or all text and the top
+// by s^T (the budget does not cover the remaining text) or all text and the top
 // vision tokens by s^V.  The top-k is an exact radix select on order-preserving
-// 32-bit keys (4 passes of 8 bits with an LDS histogram), which yields the k-th
+// 32-bit keys (4 passes of 8 bits with an LDS histogram; the digit holding the
+// k-th key is found by a wave-wide scan of the histogram), which yields the k-th
 // largest key and how many of its ties to take; ties go to the lower position.
 // A single ordered scan over all N positions then emits the retained positions
-// already in ascending order, with no sort.
+// already in ascending order, with no sort.  Candidate keys are read from global
+// memory once and kept in LDS when the row fits (N <= kLdsKeys).
 #include "tgvkv_device.h"
 #include "tgvkv_shape.h"
 
@@ -15,7 +17,9 @@ namespace tgvkv {
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kLdsKeys = 12288;  // 48 KB of LDS keys per workgroup
 enum { MODE_FORCED = 0, MODE_TEXT = 1, MODE_VIS = 2 };
+constexpr uint32_t kNotCand = 0u;  // keys of real candidates have the top bit or are >= 1
 
 struct RowCtx {
     int N, Ns, Nv, Nt, fs, fr;  // forced = [0, fs) U [fr, N)
@@ -24,21 +28,16 @@ struct RowCtx {
     const float* st;            // s_txt row (N_t)
     __device__ bool forced(int p) const { return p < fs || p >= fr; }
     __device__ bool is_vis(int p) const { return p >= Ns && p < Ns + Nv; }
-    // candidate of the top-k in this mode, and its key
-    __device__ bool cand(int p, uint32_t& key) const {
-        if (mode == MODE_FORCED) {
-            key = 0u;
-            return forced(p);
-        }
+    __device__ bool cand(int p) const {
+        if (mode == MODE_FORCED) return forced(p);
         if (forced(p)) return false;
-        if (mode == MODE_VIS) {
-            if (!is_vis(p)) return false;
-            key = ordered_key(sv[p - Ns]);
-            return true;
-        }
-        if (is_vis(p)) return false;
-        key = ordered_key(st[p < Ns ? p : p - Nv]);
-        return true;
+        return mode == MODE_VIS ? is_vis(p) : !is_vis(p);
+    }
+    // key of a candidate (only called when cand(p))
+    __device__ uint32_t key(int p) const {
+        if (mode == MODE_FORCED) return 0u;
+        if (mode == MODE_VIS) return ordered_key(sv[p - Ns]);
+        return ordered_key(st[p < Ns ? p : p - Nv]);
     }
     // kept without competing (forced in the text/vision modes, all text in the vision mode)
     __device__ bool kept_outright(int p) const {
@@ -48,7 +47,7 @@ struct RowCtx {
     }
 };
 
-// Exclusive scan of one int per thread across the block; returns the prefix, total in *tot.
+// Exclusive scan of one int per thread across the block; the total goes to *tot.
 __device__ int block_exclusive_scan(int v, int* tot, int* sh) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     int x = v;
@@ -71,6 +70,42 @@ __device__ int block_exclusive_scan(int v, int* tot, int* sh) {
     return before + x - v;
 }
 
+// Wave 0 finds the digit d (scanning 255 down to 0) where the running count of
+// larger digits first reaches kr; writes d and kr minus the count above d.
+__device__ void find_digit(const int* hist, int kr, uint32_t* sel) {
+    const int lane = threadIdx.x & 63;
+    // lane j owns digits 255-4j .. 252-4j
+    int c[4];
+    int tot = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        c[i] = hist[255 - 4 * lane - i];
+        tot += c[i];
+    }
+    int incl = tot;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(incl, o, 64);
+        if (lane >= o) incl += y;
+    }
+    const int excl = incl - tot;
+    const unsigned long long hit = __ballot(incl >= kr);
+    const int first = hit ? __ffsll((long long)hit) - 1 : 63;
+    if (lane == first) {
+        int above = excl, d = 252 - 4 * lane;
+        for (int i = 0; i < 4; ++i) {
+            if (above + c[i] >= kr) {
+                d = 255 - 4 * lane - i;
+                break;
+            }
+            above += c[i];
+        }
+        sel[0] = (uint32_t)d;
+        sel[1] = (uint32_t)(kr - above);
+    }
+}
+
+template <bool LDS_KEYS>
 __global__ __launch_bounds__(kThreads) void select_kernel(Shape s, const float* __restrict__ s_vis,
                                                           const float* __restrict__ s_txt,
                                                           const int32_t* __restrict__ budgets,
@@ -78,7 +113,8 @@ __global__ __launch_bounds__(kThreads) void select_kernel(Shape s, const float* 
                                                           int32_t* __restrict__ idx) {
     __shared__ int hist[256];
     __shared__ int sh[8];
-    __shared__ uint32_t sel[2];  // threshold key, remaining count
+    __shared__ uint32_t sel[2];
+    __shared__ uint32_t keys[LDS_KEYS ? kLdsKeys : 1];
     const int tid = threadIdx.x;
     const int gi = blockIdx.x % s.ngroups;
     const int bl = blockIdx.x / s.ngroups;
@@ -95,15 +131,11 @@ __global__ __launch_bounds__(kThreads) void select_kernel(Shape s, const float* 
     c.sv = s_vis + ((size_t)bl * s.ngroups + gi) * s.Nv;
     c.st = s_txt + ((size_t)bl * s.ngroups + gi) * s.Nt;
 
-    // counts: forced, text not forced
-    int nf = 0, ntf = 0;
-    for (int p = tid; p < s.N; p += kThreads) {
-        if (c.forced(p)) ++nf;
-        else if (!c.is_vis(p)) ++ntf;
-    }
+    // counts of forced positions and of non-forced text, from the layout alone
+    const int nf = c.fs + (s.N - c.fr);
+    int ntf = 0;
+    for (int p = tid; p < s.N; p += kThreads) ntf += !c.forced(p) && !c.is_vis(p);
     int tot;
-    block_exclusive_scan(nf, &tot, sh);
-    nf = tot;
     block_exclusive_scan(ntf, &tot, sh);
     ntf = tot;
 
@@ -111,15 +143,14 @@ __global__ __launch_bounds__(kThreads) void select_kernel(Shape s, const float* 
     if (bgt <= nf) { c.mode = MODE_FORCED; k = bgt; }
     else if (bgt - nf <= ntf) { c.mode = MODE_TEXT; k = bgt - nf; }
     else { c.mode = MODE_VIS; k = bgt - nf - ntf; }
+    const int nc = c.mode == MODE_FORCED ? nf : (c.mode == MODE_TEXT ? ntf : s.N - nf - ntf);
 
-    // candidate count
-    int nc = 0;
-    for (int p = tid; p < s.N; p += kThreads) {
-        uint32_t key;
-        if (c.cand(p, key)) ++nc;
+    // key lookup: from LDS when the row fits, else re-read
+    auto key_at = [&](int p) -> uint32_t { return LDS_KEYS ? keys[p] : c.key(p); };
+    if (LDS_KEYS) {
+        for (int p = tid; p < s.N; p += kThreads) keys[p] = c.cand(p) ? c.key(p) : kNotCand;
+        __syncthreads();
     }
-    block_exclusive_scan(nc, &tot, sh);
-    nc = tot;
 
     uint32_t thr;
     int take_ties;
@@ -132,19 +163,12 @@ __global__ __launch_bounds__(kThreads) void select_kernel(Shape s, const float* 
             hist[tid] = 0;
             __syncthreads();
             for (int p = tid; p < s.N; p += kThreads) {
-                uint32_t key;
-                if (c.cand(p, key) && (key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1);
+                if (!c.cand(p)) continue;
+                const uint32_t key = key_at(p);
+                if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1);
             }
             __syncthreads();
-            if (tid == 0) {
-                int above = 0, d = 255;
-                for (; d > 0; --d) {
-                    if (above + hist[d] >= kr) break;
-                    above += hist[d];
-                }
-                sel[0] = (uint32_t)d;
-                sel[1] = (uint32_t)(kr - above);
-            }
+            if (tid < 64) find_digit(hist, kr, sel);
             __syncthreads();
             prefix |= sel[0] << shift;
             mask |= 0xFFu << shift;
@@ -159,18 +183,15 @@ __global__ __launch_bounds__(kThreads) void select_kernel(Shape s, const float* 
     const int chunk = (s.N + kThreads - 1) / kThreads;
     const int p0 = min(tid * chunk, s.N), p1 = min(p0 + chunk, s.N);
     int nties = 0;
-    for (int p = p0; p < p1; ++p) {
-        uint32_t key;
-        if (c.cand(p, key) && key == thr) ++nties;
-    }
-    int tie_rank = block_exclusive_scan(nties, &tot, sh);
+    for (int p = p0; p < p1; ++p) nties += c.cand(p) && key_at(p) == thr;
+    const int tie_rank = block_exclusive_scan(nties, &tot, sh);
     int nkeep = 0;
     {
         int tr = tie_rank;
         for (int p = p0; p < p1; ++p) {
-            uint32_t key;
             bool keep = c.kept_outright(p);
-            if (!keep && c.cand(p, key)) {
+            if (!keep && c.cand(p)) {
+                const uint32_t key = key_at(p);
                 if (key > thr) keep = true;
                 else if (key == thr) keep = (tr++ < take_ties);
             }
@@ -181,9 +202,9 @@ __global__ __launch_bounds__(kThreads) void select_kernel(Shape s, const float* 
     {
         int tr = tie_rank;
         for (int p = p0; p < p1; ++p) {
-            uint32_t key;
             bool keep = c.kept_outright(p);
-            if (!keep && c.cand(p, key)) {
+            if (!keep && c.cand(p)) {
+                const uint32_t key = key_at(p);
                 if (key > thr) keep = true;
                 else if (key == thr) keep = (tr++ < take_ties);
             }
@@ -198,8 +219,12 @@ hipError_t launch_select(const Shape& s, const float* s_vis, const float* s_txt,
                          const int64_t* idx_off, int32_t* idx, hipStream_t st) {
     const long long nblk = (long long)s.B * s.L * s.ngroups;
     if (nblk == 0) return hipSuccess;
-    hipLaunchKernelGGL(select_kernel, dim3((unsigned)nblk), dim3(kThreads), 0, st, s, s_vis, s_txt, budgets,
-                       idx_off, idx);
+    if (s.N <= kLdsKeys)
+        hipLaunchKernelGGL(select_kernel<true>, dim3((unsigned)nblk), dim3(kThreads), 0, st, s, s_vis, s_txt, budgets,
+                           idx_off, idx);
+    else
+        hipLaunchKernelGGL(select_kernel<false>, dim3((unsigned)nblk), dim3(kThreads), 0, st, s, s_vis, s_txt,
+                           budgets, idx_off, idx);
     return hipGetLastError();
 }
 

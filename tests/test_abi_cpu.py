@@ -87,6 +87,11 @@ def test_validation_before_any_launch(lib):
     # phases, null and misaligned pointers, workspace
     assert lib.tgvkv_score(ok, None, 0, fake, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
     assert lib.tgvkv_score(ok, None, 8, fake, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
+    # the persistent variant takes only ALL or STATS|TEXT, and no budgets
+    assert lib.tgvkv_score(ok, None, 8 | 4, fake, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
+    assert lib.tgvkv_score(ok, None, 8 | 1, fake, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
+    assert lib.tgvkv_score(ok, None, 8 | 7, fake, fake, fake, fake, fake, fake, fake, fake, fake, big, s) == -1
+    assert lib.tgvkv_score(ok, None, 16, fake, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
     assert lib.tgvkv_score(ok, None, 7, None, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
     assert lib.tgvkv_score(ok, None, 7, odd, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
     assert lib.tgvkv_score(ok, None, 2, fake, fake, fake, None, fake, fake, fake, None, fake, big, s) == -1

@@ -17,7 +17,7 @@ pytestmark = pytest.mark.gpu
 
 
 def run_and_check(cfg, rho, head_mode=0, forced=(0, 0), steps=2, seed=0, skip_text_only=True, check_seqs=None,
-                  decode_seqs=None):
+                  decode_seqs=None, schedule="auto"):
     import torch
     log(f"e2e {cfg.name} rho={rho} mode={head_mode} forced={forced} steps={steps}")
     t = make_prefill_tensors(cfg, seed=seed)
@@ -28,7 +28,8 @@ def run_and_check(cfg, rho, head_mode=0, forced=(0, 0), steps=2, seed=0, skip_te
     o = bd.make_opts(head_mode=head_mode, n_sink=forced[0], n_recent=forced[1])
     buf = bd.EvictionBuffers(p, o, tot, max(steps, 1))
     q_d, k_d, v_d = dev_bf16(t["q_text"]), dev_bf16(t["k"]), dev_bf16(t["v"])
-    buf.evict(q_d, k_d, v_d, skip_text_only_layers=skip_text_only)
+    sched = buf.evict(q_d, k_d, v_d, schedule=schedule if skip_text_only else "phases")
+    log(f"  schedule {sched}")
     outs = []
     for st in range(steps):
         buf.decode(st, dev_bf16(dec["q"][st]), dev_bf16(dec["k_new"][st]), dev_bf16(dec["v_new"][st]))
@@ -62,8 +63,8 @@ def run_and_check(cfg, rho, head_mode=0, forced=(0, 0), steps=2, seed=0, skip_te
             assert_close_rel("tv_mass", tv[b, l], sc["tv_mass"])
             assert_close_rel("s_txt", host(buf.s_txt[b, l]), sc["s_txt"])
             assert_close_rel("w_txt", host(buf.w_txt[b, l]), sc["w_txt"])
-            needs_vis = budgets[b, l] > cfg.n_text + 0
-            if needs_vis or not skip_text_only:
+            needs_vis = budgets[b, l] > buf.forced_or_text()
+            if needs_vis or sched in ("fused", "phases"):
                 assert_close_rel("s_vis", host(buf.s_vis[b, l]), sc["s_vis"])
             if budgets[b, l] != ob[l]:
                 continue  # a rounding-cut trade: this layer's set is legitimately different
@@ -98,12 +99,13 @@ def run_and_check(cfg, rho, head_mode=0, forced=(0, 0), steps=2, seed=0, skip_te
     return buf
 
 
+@pytest.mark.parametrize("schedule", ["auto", "phases", "fused", "fused_text"])
 @pytest.mark.parametrize("head_mode", [0, 1])
 @pytest.mark.parametrize("forced", [(0, 0), (4, 1)])
-def test_small_ragged(lib, head_mode, forced):
+def test_small_ragged(lib, head_mode, forced, schedule):
     cfg = custom_config(batch=2, layers=4, heads_q=8, heads_kv=4, head_dim=128, n_sys=6, n_vis=230, n_qst=21)
     for rho in (0.05, 0.2, 0.6, 1.0):
-        run_and_check(cfg, rho, head_mode, forced, steps=3, seed=1)
+        run_and_check(cfg, rho, head_mode, forced, steps=3, seed=1, schedule=schedule)
 
 
 def test_gqa_video_small(lib):

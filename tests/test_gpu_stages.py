@@ -238,18 +238,20 @@ SCORE_SHAPES = {
 }
 
 
+@pytest.mark.parametrize("fused", [False, True])
 @pytest.mark.parametrize("name", sorted(SCORE_SHAPES))
 @pytest.mark.parametrize("head_mode", [0, 1])
-def test_score_matches_oracle(lib, name, head_mode):
+def test_score_matches_oracle(lib, name, head_mode, fused):
     torch = _torch()
     cfg = SCORE_SHAPES[name]
-    log(f"score {name} mode={head_mode}")
+    log(f"score {name} mode={head_mode} fused={fused}")
+    phases = bd.SCORE_ALL | (bd.SCORE_FUSED if fused else 0)
     t = make_prefill_tensors(cfg, seed=3, names=("q_text", "k"))
     p = bd.problem_from(cfg)
     o = bd.make_opts(head_mode=head_mode)
     buf = bd.EvictionBuffers(p, o, 0, 1)
     q_d, k_d = dev_bf16(t["q_text"]), dev_bf16(t["k"])
-    buf.score(q_d, k_d, bd.SCORE_ALL)
+    buf.score(q_d, k_d, phases)
     torch.cuda.synchronize()
     worst = {}
     for b in range(cfg.batch):
@@ -263,7 +265,7 @@ def test_score_matches_oracle(lib, name, head_mode):
     log(f"  max rel err: {worst}")
     # determinism: a second run gives identical bits
     s1 = host(buf.s_vis).copy(), host(buf.s_txt).copy(), host(buf.tv_mass).copy()
-    buf.score(q_d, k_d, bd.SCORE_ALL)
+    buf.score(q_d, k_d, phases)
     torch.cuda.synchronize()
     assert np.array_equal(s1[0], host(buf.s_vis)) and np.array_equal(s1[1], host(buf.s_txt))
     assert np.array_equal(s1[2], host(buf.tv_mass))
