@@ -94,8 +94,8 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(Shape s, const uint16
     for (int i = 0; i < kPasses; ++i) {
         if (ok[i]) {
             const size_t src = (((size_t)blk[i] * s.Hkv + kvh) * (size_t)s.N + pos[i]) * D + cc * 8;
-            kr[i] = load16(k + src);
-            vr[i] = load16(v + src);
+            kr[i] = load16_stream(k + src);
+            vr[i] = load16_stream(v + src);
         }
     }
 #pragma unroll

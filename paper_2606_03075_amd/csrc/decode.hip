@@ -7,8 +7,9 @@
 //   * one workgroup per (sequence, layer, KV head[, split]): the KV head's rows
 //     are read once and serve all query heads that share it (GQA);
 //   * a token row of head_dim bf16 is read by head_dim/8 lanes with 16-byte
-//     loads; each lane group handles 4 tokens per iteration with all 8 loads
-//     issued before any math;
+//     non-temporal loads; each lane group handles 8 tokens per iteration (4 when
+//     a KV head serves more than 2 query heads, to bound registers) with all of
+//     their K and V loads issued before any math;
 //   * online softmax per lane group, merged across groups with wave shuffles and
 //     across the 4 waves through LDS; when the (sequence, layer, KV head) count is
 //     too small to fill the GPU the token range is split and a second kernel
@@ -22,7 +23,6 @@ namespace tgvkv {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kUnroll = 4;
 
 __device__ __forceinline__ void unpack8(u32x4 r, float (&f)[8]) {
 #pragma unroll
@@ -43,6 +43,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(Shape s, uint16_t* __r
     constexpr int LPR = D / 8;         // lanes per token row
     constexpr int GPW = 64 / LPR;      // lane groups per wave
     constexpr int NGRP = 4 * GPW;      // lane groups per workgroup
+    constexpr int kUnroll = GMAX <= 2 ? 8 : 4;  // tokens in flight per lane group
     __shared__ float wm[4][GMAX], wl[4][GMAX];
     __shared__ float wacc[4][GMAX][D];
 
@@ -103,8 +104,8 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(Shape s, uint16_t* __r
             const bool fresh = n >= len - 1 || !ok[u];
             const uint16_t* kp = fresh ? knew : kc + seg + (size_t)n * D;
             const uint16_t* vp = fresh ? vnew : vc + seg + (size_t)n * D;
-            kr[u] = load16(kp + sub * 8);
-            vr[u] = load16(vp + sub * 8);
+            kr[u] = load16_stream(kp + sub * 8);
+            vr[u] = load16_stream(vp + sub * 8);
         }
 #pragma unroll
         for (int h = 0; h < GMAX; ++h) {

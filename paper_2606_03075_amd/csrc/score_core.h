@@ -44,7 +44,7 @@ __device__ __forceinline__ void load_tile_regs(u32x4 (&r)[Geo<D>::LOADS], const 
         const int c = it * kThreads + tid;
         const int row = c / Geo<D>::CPR, cc = c % Geo<D>::CPR;
         const int key = min(key0 + row, key_last);
-        r[it] = load16(kbase + (size_t)key * D + cc * 8);
+        r[it] = load16_stream(kbase + (size_t)key * D + cc * 8);
     }
 }
 

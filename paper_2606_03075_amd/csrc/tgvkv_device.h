@@ -30,6 +30,16 @@ __device__ __forceinline__ u32x4 load16(const void* p) {
 
 __device__ __forceinline__ void store16(void* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
 
+// 16-byte load with the non-temporal hint, for data streamed once per kernel (K/V
+// rows).  On gfx950 it lifts a pure HBM read stream from about 5.9 to 6.8 TB/s.
+__device__ __forceinline__ u32x4 load16_stream(const void* p) {
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
+
+__device__ __forceinline__ void store16_stream(void* p, u32x4 v) {
+    __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
+}
+
 // v_exp_f32: 2^x, exp2(-inf) = 0.
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
