@@ -197,10 +197,16 @@ tgvkv_status tgvkv_score(const tgvkv_problem* problem, const tgvkv_opts* opts, i
     }
 
     hipError_t e = hipSuccess;
-    if ((phases & TGVKV_SCORE_STATS) && e == hipSuccess) e = tgvkv::launch_score_stats(s, rp, q, kk, lse, w.vm, stream);
-    if ((phases & TGVKV_SCORE_TEXT) && e == hipSuccess) {
-        e = tgvkv::launch_score_text(s, q, kk, lse, w.vm, w.colsum, w.vmh, stream);
+    const bool both = (phases & TGVKV_SCORE_STATS) && (phases & TGVKV_SCORE_TEXT);
+    if (both && tgvkv::stats_text_eligible(s, rp)) {
+        e = tgvkv::launch_score_stats_text(s, rp, q, kk, lse, w.vm, w.colsum, w.vmh, stream);
         if (e == hipSuccess) e = tgvkv::launch_score_fin(s, w.colsum, w.vmh, s_txt, w_txt, tv_mass, stream);
+    } else {
+        if (phases & TGVKV_SCORE_STATS) e = tgvkv::launch_score_stats(s, rp, q, kk, lse, w.vm, stream);
+        if ((phases & TGVKV_SCORE_TEXT) && e == hipSuccess) {
+            e = tgvkv::launch_score_text(s, q, kk, lse, w.vm, w.colsum, w.vmh, stream);
+            if (e == hipSuccess) e = tgvkv::launch_score_fin(s, w.colsum, w.vmh, s_txt, w_txt, tv_mass, stream);
+        }
     }
     if ((phases & TGVKV_SCORE_VISION) && e == hipSuccess && s.Nv > 0) {
         e = tgvkv::launch_score_vision(s, rp, q, kk, lse, w_txt, budgets_or_null, vthr, w.part, stream);
@@ -254,7 +260,7 @@ tgvkv_status tgvkv_compact(const tgvkv_problem* problem, const tgvkv_opts* opts,
         return TGVKV_E_INVAL;
     if (!aligned16(k) || !aligned16(v) || !aligned16(kc) || !aligned16(vc)) return TGVKV_E_INVAL;
     const int64_t rows = (int64_t)s.B * total_budget;
-    if ((rows + 63) / 64 > kMaxBlocks || s.Hkv > 65535) return TGVKV_E_UNSUPPORTED;
+    if ((int64_t)s.B * s.L * 16 > kMaxBlocks || s.Hkv > 65535) return TGVKV_E_UNSUPPORTED;
     return hip_status(tgvkv::launch_compact(s, static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), idx,
                                             budgets, idx_offsets, seg_offsets, decode_reserve, rows,
                                             static_cast<uint16_t*>(kc), static_cast<uint16_t*>(vc), stream));

@@ -3,13 +3,14 @@
 // After eviction every layer keeps b_l tokens (Eq. (10)); the cache of Sec. 3.1
 // holds only those rows, in ascending position, followed by decode_reserve free
 // slots that decode (Eq. (3)-(4)) fills.  The work is a pure HBM stream: read
-// and write each retained row once.  The grid runs over the flat list of
-// retained rows (known on the host: B * B_tot per KV head), so it is sized by
-// the bytes moved, not by the largest layer.  A row of head_dim bf16 is moved
-// by head_dim/8 lanes with 16-byte accesses; each thread moves kPasses rows and
-// issues every load (index, K, V) before any store.  The (sequence, layer) of
-// the workgroup's first row is found once by binary search over the offsets;
-// the other rows advance from it through an LDS copy of the following offsets.
+// and write each retained row once.  One workgroup moves the rows of one
+// (sequence, layer, KV head), or a contiguous share of them when there are too
+// few such units to fill the GPU, so its metadata is three independent loads and
+// no search.  A row of head_dim bf16 is moved by head_dim/8 lanes with 16-byte
+// accesses (non-temporal loads); each thread keeps kPasses rows in flight, and
+// the positions of the next rows are fetched while the current ones are moved.
+#include <algorithm>
+
 #include "tgvkv_device.h"
 #include "tgvkv_shape.h"
 
@@ -17,8 +18,7 @@ namespace tgvkv {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kPasses = 4;
-constexpr int kWindow = 128;  // offsets cached in LDS after the first row's block
+constexpr int kPasses = 8;
 
 template <int D>
 __global__ __launch_bounds__(kThreads) void compact_kernel(Shape s, const uint16_t* __restrict__ k,
@@ -27,87 +27,65 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(Shape s, const uint16
                                                            const int32_t* __restrict__ budgets,
                                                            const int64_t* __restrict__ idx_off,
                                                            const int64_t* __restrict__ seg_off, int reserve,
-                                                           long long rows_total, uint16_t* __restrict__ kc,
+                                                           int nsplit, uint16_t* __restrict__ kc,
                                                            uint16_t* __restrict__ vc) {
     constexpr int CPR = D / 8;             // lanes per row
     constexpr int RPP = kThreads / CPR;    // rows per pass
-    constexpr int ROWS = RPP * kPasses;    // rows per workgroup
-    __shared__ long long win[kWindow + 1];  // per-group row offsets of blocks bl0 .. bl0 + kWindow
-    __shared__ int sh_bl0;
+    constexpr int ROWS = RPP * kPasses;    // rows per iteration
     const int kvh = blockIdx.y;
-    const long long g = s.ngroups;
-    const int nbl = s.B * s.L;
-    const int cc = threadIdx.x % CPR;
-    const long long r0 = (long long)blockIdx.x * ROWS;
+    const int split = blockIdx.x % nsplit;
+    const int bl = blockIdx.x / nsplit;
+    const int bsz = budgets[bl];
+    const long long ioff = idx_off[bl] + (s.head_mode == 0 ? 0 : (long long)kvh * bsz);
+    const long long soff = seg_off[bl];
+    const int per = (bsz + nsplit - 1) / nsplit;
+    const int r_beg = min(split * per, bsz), r_end = min(r_beg + per, bsz);
+    const int cc = threadIdx.x % CPR, rl = threadIdx.x / CPR;
+    const size_t src0 = ((size_t)bl * s.Hkv + kvh) * (size_t)s.N * D + cc * 8;
+    const size_t dst0 = ((size_t)soff * s.Hkv + (size_t)kvh * (bsz + reserve)) * D + cc * 8;
 
-    if (threadIdx.x == 0) {
-        int lo = 0, hi = nbl - 1;  // largest bl with idx_off[bl] / g <= r0
-        while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (idx_off[mid] / g <= r0) lo = mid;
-            else hi = mid - 1;
-        }
-        sh_bl0 = lo;
-    }
-    __syncthreads();
-    const int bl0 = sh_bl0;
-    for (int i = threadIdx.x; i <= kWindow; i += kThreads) {
-        const int bl = min(bl0 + i, nbl);
-        win[i] = idx_off[bl] / g;
-    }
-    __syncthreads();
-
-    long long f[kPasses];
-    int blk[kPasses], pos[kPasses];
-    bool ok[kPasses];
+    // positions come from tgvkv_select; clamp so a corrupt index can never read outside the slice
+    int pos[kPasses];
 #pragma unroll
     for (int i = 0; i < kPasses; ++i) {
-        f[i] = r0 + i * RPP + threadIdx.x / CPR;
-        ok[i] = f[i] < rows_total;
-        int w = 0;
-        while (w < kWindow && bl0 + w + 1 < nbl && win[w + 1] <= f[i]) ++w;
-        int bl = bl0 + w;
-        if (w == kWindow) {  // beyond the cached window (many empty blocks): search
-            int lo = bl, hi = nbl - 1;
-            while (lo < hi) {
-                const int mid = (lo + hi + 1) >> 1;
-                if (idx_off[mid] / g <= f[i]) lo = mid;
-                else hi = mid - 1;
+        const int r = r_beg + i * RPP + rl;
+        pos[i] = r < r_end ? min(max(idx[ioff + r], 0), s.N - 1) : -1;
+    }
+    for (int r0 = r_beg; r0 < r_end; r0 += ROWS) {
+        u32x4 kr[kPasses], vr[kPasses];
+#pragma unroll
+        for (int i = 0; i < kPasses; ++i) {
+            if (pos[i] >= 0) {
+                kr[i] = load16_stream(k + src0 + (size_t)pos[i] * D);
+                vr[i] = load16_stream(v + src0 + (size_t)pos[i] * D);
             }
-            bl = lo;
         }
-        blk[i] = bl;
-    }
+        int cur[kPasses];
 #pragma unroll
-    for (int i = 0; i < kPasses; ++i) {
-        pos[i] = 0;
-        if (ok[i]) {
-            const int bl = blk[i];
-            const long long n = f[i] - idx_off[bl] / g;
-            const int bsz = budgets[bl];
-            // positions come from tgvkv_select; clamp so a corrupt index can never read outside the slice
-            pos[i] = min(max(idx[idx_off[bl] + (s.head_mode == 0 ? 0 : (long long)kvh * bsz) + n], 0), s.N - 1);
+        for (int i = 0; i < kPasses; ++i) {
+            cur[i] = pos[i];
+            const int r = r0 + ROWS + i * RPP + rl;
+            pos[i] = r < r_end ? min(max(idx[ioff + r], 0), s.N - 1) : -1;
         }
-    }
-    u32x4 kr[kPasses], vr[kPasses];
 #pragma unroll
-    for (int i = 0; i < kPasses; ++i) {
-        if (ok[i]) {
-            const size_t src = (((size_t)blk[i] * s.Hkv + kvh) * (size_t)s.N + pos[i]) * D + cc * 8;
-            kr[i] = load16_stream(k + src);
-            vr[i] = load16_stream(v + src);
+        for (int i = 0; i < kPasses; ++i) {
+            if (cur[i] >= 0) {
+                const size_t dst = dst0 + (size_t)(r0 + i * RPP + rl) * D;
+                store16(kc + dst, kr[i]);
+                store16(vc + dst, vr[i]);
+            }
         }
     }
-#pragma unroll
-    for (int i = 0; i < kPasses; ++i) {
-        if (ok[i]) {
-            const int bl = blk[i];
-            const long long n = f[i] - idx_off[bl] / g;
-            const size_t dst = ((size_t)seg_off[bl] * s.Hkv + (size_t)kvh * (budgets[bl] + reserve) + n) * D + cc * 8;
-            store16(kc + dst, kr[i]);
-            store16(vc + dst, vr[i]);
-        }
-    }
+}
+
+// Workgroups per (sequence, layer, KV head): enough units to fill the GPU, but
+// not fewer than about 64 rows per workgroup on average.
+int compact_splits(const Shape& s, int64_t rows_total) {
+    const long long units = (long long)s.B * s.L * s.Hkv;
+    if (units <= 0 || rows_total <= 0) return 1;
+    const long long avg_rows = rows_total / ((long long)s.B * s.L);  // retained rows per (sequence, layer)
+    long long n = std::min<long long>(2048 / units, avg_rows / 64);
+    return (int)std::max<long long>(1, std::min<long long>(n, 16));
 }
 
 }  // namespace
@@ -116,14 +94,14 @@ hipError_t launch_compact(const Shape& s, const uint16_t* k, const uint16_t* v, 
                           const int32_t* budgets, const int64_t* idx_off, const int64_t* seg_off, int32_t reserve,
                           int64_t rows_total, uint16_t* kc, uint16_t* vc, hipStream_t st) {
     if (rows_total <= 0 || s.B * s.L == 0) return hipSuccess;
-    const int rows_per_block = (kThreads / (s.D / 8)) * kPasses;
-    dim3 grid((unsigned)((rows_total + rows_per_block - 1) / rows_per_block), (unsigned)s.Hkv);
+    const int nsplit = compact_splits(s, rows_total);
+    dim3 grid((unsigned)((long long)s.B * s.L * nsplit), (unsigned)s.Hkv);
     if (s.D == 128)
         hipLaunchKernelGGL(compact_kernel<128>, grid, dim3(kThreads), 0, st, s, k, v, idx, budgets, idx_off, seg_off,
-                           reserve, (long long)rows_total, kc, vc);
+                           reserve, nsplit, kc, vc);
     else
         hipLaunchKernelGGL(compact_kernel<64>, grid, dim3(kThreads), 0, st, s, k, v, idx, budgets, idx_off, seg_off,
-                           reserve, (long long)rows_total, kc, vc);
+                           reserve, nsplit, kc, vc);
     return hipGetLastError();
 }
 

@@ -9,6 +9,8 @@
 //
 //   score_stats   sweep 1: question rows x all visible keys -> row log-sum-exp
 //                 and vision mass, online (one K read);
+//   score_stats_text  sweep 1 followed by the unit's text pass in the same
+//                 workgroup, when one workgroup holds all of a unit's question rows;
 //   score_text    text rows x text keys: system-row normalisers, then the
 //                 text->text probabilities' column sums per head (Eq. (9));
 //   score_fin     head means -> s^T, w, w~ (Eq. (7), (9)) and the layer's
@@ -66,6 +68,64 @@ __global__ __launch_bounds__(kThreads) void score_stats_kernel(Shape s, int rowg
     }
 }
 
+// Sweep 1 and the text pass of one unit in one workgroup, for shapes where one
+// workgroup holds all question rows of a (sequence, layer, KV head): the text
+// pass is latency-bound, so running it as each unit's sweep ends hides it behind
+// the other workgroups' key streams, and the question rows' normalisers go to
+// the text pass through LDS.  Results are bit-identical to score_stats followed
+// by score_text (same operations in the same order).
+template <int D, int NSLOT, int KS>
+__global__ __launch_bounds__(kThreads) void score_stats_text_kernel(Shape s, const uint16_t* __restrict__ q_text,
+                                                                    const uint16_t* __restrict__ k,
+                                                                    float* __restrict__ lse,
+                                                                    float* __restrict__ ws_vm,
+                                                                    float* __restrict__ ws_colsum,
+                                                                    float* __restrict__ ws_vmh) {
+    constexpr int RSETS = 4 / KS;
+    __shared__ __attribute__((aligned(16))) char tiles[2][Geo<D>::TILE_BYTES];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int rs = wave % RSETS, kp = wave / RSETS;
+    const int kvh = blockIdx.x % s.Hkv;
+    const int bl = blockIdx.x / s.Hkv;
+    const int QB = (s.Nq + 15) >> 4;
+    const int NB = s.G * QB;
+    const size_t head0 = (size_t)bl * s.H + kvh * s.G;
+
+    bf16x8 qf[NSLOT][Geo<D>::KSTEPS];
+    int qrow[NSLOT];
+    load_qrows<D, NSLOT, KS>(s, q_text, bl, kvh, 0, qf, qrow);
+    float m[NSLOT], lsum[NSLOT], vsum[NSLOT];
+    const uint16_t* kbase = k + ((size_t)bl * s.Hkv + kvh) * (size_t)s.N * D;
+    stats_sweep<D, NSLOT, KS>(s, kbase, 0, s.N, qf, qrow, 0, NB, tiles, m, lsum, vsum);
+
+    // the key tiles are free now: [G][N_t] normalisers (base 2), then [G][N_q] vision masses
+    float* lse2s = reinterpret_cast<float*>(&tiles[0][0]);
+    float* vms = lse2s + (size_t)s.G * s.Nt;
+    if (kp == 0 && lane < 16) {
+#pragma unroll
+        for (int sl = 0; sl < NSLOT; ++sl) {
+            const int rb = rs + sl * RSETS;
+            const int qi = qrow[sl];
+            if (rb < NB && qi < s.Nq) {
+                const int g = rb / QB;
+                const float ln = (m[sl] + log2f(lsum[sl])) * kLn2;
+                const float vm = vsum[sl] / lsum[sl];
+                lse[(head0 + g) * s.Nt + s.Ns + qi] = ln;
+                ws_vm[(head0 + g) * s.Nq + qi] = vm;
+                lse2s[g * s.Nt + s.Ns + qi] = ln * kLog2e;
+                vms[g * s.Nq + qi] = vm;
+            }
+        }
+    }
+    __syncthreads();
+    if (tid < s.G) {
+        float a = 0.f;
+        for (int qi = 0; qi < s.Nq; ++qi) a += vms[tid * s.Nq + qi];
+        ws_vmh[head0 + tid] = a;
+    }
+    text_pass<D>(s, bl, kvh, q_text, k, lse, lse2s, ws_colsum);
+}
+
 template <int D>
 __global__ __launch_bounds__(kThreads) void score_text_kernel(Shape s, const uint16_t* __restrict__ q_text,
                                                               const uint16_t* __restrict__ k,
@@ -113,24 +173,34 @@ __global__ __launch_bounds__(kThreads) void score_vision_kernel(Shape s, int row
     constexpr int RSETS = 4 / KS;
     __shared__ __attribute__((aligned(16))) char tiles[2][Geo<D>::TILE_BYTES];
     __shared__ float red[2][RSETS][kTile];
+    __shared__ float obuf[kOutTiles * kTile];
     int bid = blockIdx.x;
     const int rg = bid % rowgroups;
     bid /= rowgroups;
     const int kvh = bid % s.Hkv;
     const int bl = bid / s.Hkv;
-    if (budgets != nullptr && budgets[bl] <= vis_threshold) return;
     const int QB = (s.Nq + 15) >> 4;
     const int NB = s.G * QB;
     const int rb0 = rg * RSETS * NSLOT;
 
+    // the row loads are issued before the budget test so that their latencies overlap
     bf16x8 qf[NSLOT][Geo<D>::KSTEPS];
     int qrow[NSLOT];
-    load_qrows<D, NSLOT, KS>(s, q_text, bl, kvh, rb0, qf, qrow);
+    load_qrows<D, NSLOT, KS, false>(s, q_text, bl, kvh, rb0, qf, qrow);
     float lse2[NSLOT][4], coef[NSLOT][4];
-    load_row_coefs<NSLOT, KS>(s, bl, kvh, rb0, lse, w_txt, lse2, coef);
+    load_row_coefs<NSLOT, KS, false>(s, bl, kvh, rb0, lse, w_txt, lse2, coef);
+    if (budgets != nullptr && budgets[bl] <= vis_threshold) return;
+    settle_qrows<D, NSLOT>(qf);
+#pragma unroll
+    for (int sl = 0; sl < NSLOT; ++sl)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            settle(lse2[sl][j]);
+            settle(coef[sl][j]);
+        }
     const uint16_t* kvis = k + (((size_t)bl * s.Hkv + kvh) * (size_t)s.N + s.Ns) * D;
     float* out = ws_part + (((size_t)bl * s.Hkv + kvh) * rowgroups + rg) * (size_t)s.Nv;
-    vision_sweep<D, NSLOT, KS>(s, kvis, 0, s.Nv, qf, lse2, coef, rb0, NB, tiles, red, out);
+    vision_sweep<D, NSLOT, KS>(s, kvis, 0, s.Nv, qf, lse2, coef, rb0, NB, tiles, red, obuf, out);
 }
 
 __global__ __launch_bounds__(kThreads) void score_vis_reduce_kernel(Shape s, int rowgroups,
@@ -190,6 +260,27 @@ hipError_t launch_score_stats(const Shape& s, const RowPlan& rp, const uint16_t*
         TGVKV_ROWPLAN_DISPATCH(score_stats_kernel, 128, rp, grid, block, 0, st, s, rp.rowgroups, q_text, k, lse, ws_vm);
     else
         TGVKV_ROWPLAN_DISPATCH(score_stats_kernel, 64, rp, grid, block, 0, st, s, rp.rowgroups, q_text, k, lse, ws_vm);
+    return hipGetLastError();
+}
+
+bool stats_text_eligible(const Shape& s, const RowPlan& rp) {
+    if (rp.rowgroups != 1 || s.Nt == 0) return false;
+    const long long floats = (long long)s.G * (s.Nt + s.Nq);
+    const long long tile_bytes = 2LL * kTile * (2 * s.D + 16);
+    return floats * 4 <= tile_bytes;
+}
+
+hipError_t launch_score_stats_text(const Shape& s, const RowPlan& rp, const uint16_t* q_text, const uint16_t* k,
+                                   float* lse, float* ws_vm, float* ws_colsum, float* ws_vmh, hipStream_t st) {
+    const long long nblk = (long long)s.B * s.L * s.Hkv;
+    if (nblk == 0) return hipSuccess;
+    dim3 grid((unsigned)nblk), block(kThreads);
+    if (s.D == 128)
+        TGVKV_ROWPLAN_DISPATCH(score_stats_text_kernel, 128, rp, grid, block, 0, st, s, q_text, k, lse, ws_vm,
+                               ws_colsum, ws_vmh);
+    else
+        TGVKV_ROWPLAN_DISPATCH(score_stats_text_kernel, 64, rp, grid, block, 0, st, s, q_text, k, lse, ws_vm,
+                               ws_colsum, ws_vmh);
     return hipGetLastError();
 }
 

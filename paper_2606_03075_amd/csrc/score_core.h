@@ -26,6 +26,7 @@ namespace core {
 
 constexpr int kThreads = 256;
 constexpr int kTile = 64;  // keys per LDS tile
+constexpr int kOutTiles = 8;  // vision-score tiles buffered in LDS per burst of global writes
 
 template <int D>
 struct Geo {
@@ -58,6 +59,79 @@ __device__ __forceinline__ void store_tile_lds(char* buf, const u32x4 (&r)[Geo<D
     }
 }
 
+// Streams the 64-key tiles of keys [kbeg, kend) through the two LDS buffers.
+// With DEPTH 2 two tiles are in flight per workgroup: while tile t is consumed
+// from LDS, tile t+1 waits in registers and tile t+2 is being fetched (costs
+// one more tile of registers); with DEPTH 1 only tile t+1 is fetched meanwhile.
+// compute(buf, key0, t) runs on tile t; post(key0, t) runs after the barrier
+// that ends tile t.  Returns right after the last post (no barrier after it).
+// Every barrier is reached by all threads (the tile count is uniform).
+template <int D, int DEPTH, typename Compute, typename Post>
+__device__ __forceinline__ void tile_pipeline(const uint16_t* kbase, int kbeg, int kend,
+                                              char (*tiles)[Geo<D>::TILE_BYTES], Compute&& compute, Post&& post) {
+    static_assert(DEPTH == 1 || DEPTH == 2, "tile pipeline depth");
+    const int tid = threadIdx.x;
+    const int ntiles = (kend - kbeg + kTile - 1) / kTile;
+    if (DEPTH == 1) {
+        u32x4 pre[Geo<D>::LOADS];
+        if (ntiles > 0) {
+            load_tile_regs<D>(pre, kbase, kbeg, kend - 1, tid);
+            store_tile_lds<D>(tiles[0], pre, tid);
+        }
+        __syncthreads();
+        for (int t = 0; t < ntiles; ++t) {
+            const int key0 = kbeg + t * kTile;
+            if (t + 1 < ntiles) load_tile_regs<D>(pre, kbase, key0 + kTile, kend - 1, tid);
+            compute(tiles[t & 1], key0, t);
+            if (t + 1 < ntiles) store_tile_lds<D>(tiles[(t + 1) & 1], pre, tid);
+            __syncthreads();
+            post(key0, t);
+        }
+        return;
+    }
+    // Loads past the last tile are issued anyway (their key index is clamped to
+    // the last key, so they re-read one cached row): with a fixed number of loads
+    // per step the compiler's wait before each LDS store counts only that tile's
+    // loads instead of draining the one fetched behind it.
+    if (ntiles <= 0) {
+        __syncthreads();
+        return;
+    }
+    u32x4 ra[Geo<D>::LOADS], rb[Geo<D>::LOADS];
+    load_tile_regs<D>(ra, kbase, kbeg, kend - 1, tid);
+    store_tile_lds<D>(tiles[0], ra, tid);
+    load_tile_regs<D>(rb, kbase, kbeg + kTile, kend - 1, tid);
+    load_tile_regs<D>(ra, kbase, kbeg + 2 * kTile, kend - 1, tid);
+    __syncthreads();
+    // An odd tile count runs one more half-step without compute or post (its load
+    // and store touch only clamped rows and the free buffer), so the loop has no
+    // exit in the middle; with one, the compiler's wait counting loses track of
+    // the loads in flight at the loop head and drains them all.
+    for (int t = 0; t < ntiles; t += 2) {
+        // tile t in tiles[0], tile t+1 in rb, tile t+2 in ra; tiles[1] is free
+        const int key0 = kbeg + t * kTile;
+        compute(tiles[0], key0, t);
+        store_tile_lds<D>(tiles[1], rb, tid);
+        load_tile_regs<D>(rb, kbase, key0 + 3 * kTile, kend - 1, tid);
+        __syncthreads();
+        post(key0, t);
+        // tile t+1 in tiles[1], tile t+2 in ra, tile t+3 in rb; tiles[0] is free
+        const bool more = t + 1 < ntiles;
+        if (more) compute(tiles[1], key0 + kTile, t + 1);
+        store_tile_lds<D>(tiles[0], ra, tid);
+        load_tile_regs<D>(ra, kbase, key0 + 4 * kTile, kend - 1, tid);
+        __syncthreads();
+        if (more) post(key0 + kTile, t + 1);
+    }
+}
+
+// Tiles in flight per workgroup for a row plan: two while the question rows
+// leave room in registers.
+template <int NSLOT>
+struct PipeDepth {
+    static constexpr int value = NSLOT <= 2 ? 2 : 1;
+};
+
 __device__ __forceinline__ bf16x8 zero_frag() {
     u32x4 z = {0u, 0u, 0u, 0u};
     return as_bf16x8(z);
@@ -70,8 +144,16 @@ __device__ __forceinline__ void load_kfrag(bf16x8 (&kf)[Geo<D>::KSTEPS], const c
     for (int ks = 0; ks < Geo<D>::KSTEPS; ++ks) kf[ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(src + ks * 64));
 }
 
+template <int D, int NSLOT>
+__device__ __forceinline__ void settle_qrows(const bf16x8 (&qf)[NSLOT][Geo<D>::KSTEPS]) {
+#pragma unroll
+    for (int sl = 0; sl < NSLOT; ++sl)
+#pragma unroll
+        for (int ks = 0; ks < Geo<D>::KSTEPS; ++ks) settle(qf[sl][ks]);
+}
+
 // Question-row fragments of the row set of this wave (lane: row lane & 15 of each block).
-template <int D, int NSLOT, int KS>
+template <int D, int NSLOT, int KS, bool SETTLE = true>
 __device__ __forceinline__ void load_qrows(const Shape& s, const uint16_t* q_text, int bl, int kvh, int rb0,
                                            bf16x8 (&qf)[NSLOT][Geo<D>::KSTEPS], int (&qrow)[NSLOT]) {
     constexpr int RSETS = 4 / KS;
@@ -92,6 +174,7 @@ __device__ __forceinline__ void load_qrows(const Shape& s, const uint16_t* q_tex
         for (int ks = 0; ks < Geo<D>::KSTEPS; ++ks)
             qf[sl][ks] = valid ? as_bf16x8(load16(qp + ks * 32)) : zero_frag();
     }
+    if (SETTLE) settle_qrows<D, NSLOT>(qf);
 }
 
 // Statistics sweep over keys [kbeg, kend) of one unit (kbeg a multiple of kTile):
@@ -115,76 +198,67 @@ __device__ void stats_sweep(const Shape& s, const uint16_t* kbase, int kbeg, int
         lsum[sl] = 0.f;
         vsum[sl] = 0.f;
     }
-    const int ntiles = (kend - kbeg + kTile - 1) / kTile;
-    u32x4 pre[GG::LOADS];
-    if (ntiles > 0) {
-        load_tile_regs<D>(pre, kbase, kbeg, kend - 1, tid);
-        store_tile_lds<D>(tiles[0], pre, tid);
-    }
-    __syncthreads();
-    for (int t = 0; t < ntiles; ++t) {
-        const char* buf = tiles[t & 1];
-        const int key0 = kbeg + t * kTile;
-        if (t + 1 < ntiles) load_tile_regs<D>(pre, kbase, key0 + kTile, kend - 1, tid);
-        const bool pure_vis = key0 >= vis0 && key0 + kTile <= vis1 && key0 + kTile <= kend;
+    tile_pipeline<D, PipeDepth<NSLOT>::value>(
+        kbase, kbeg, kend, tiles,
+        [&](const char* buf, int key0, int) {
+            const bool pure_vis = key0 >= vis0 && key0 + kTile <= vis1 && key0 + kTile <= kend;
 #pragma unroll
-        for (int kbi = 0; kbi < KBW; ++kbi) {
-            const int kb = kp + kbi * KS;
-            bf16x8 kf[GG::KSTEPS];
-            load_kfrag<D>(kf, buf, kb, lane);
-            const int kfirst = key0 + kb * 16 + (lane >> 4) * 4;  // key of accumulator element 0
+            for (int kbi = 0; kbi < KBW; ++kbi) {
+                const int kb = kp + kbi * KS;
+                bf16x8 kf[GG::KSTEPS];
+                load_kfrag<D>(kf, buf, kb, lane);
+                const int kfirst = key0 + kb * 16 + (lane >> 4) * 4;  // key of accumulator element 0
 #pragma unroll
-            for (int sl = 0; sl < NSLOT; ++sl) {
-                if (rb0 + rs + sl * RSETS >= NB) continue;
-                f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+                for (int sl = 0; sl < NSLOT; ++sl) {
+                    if (rb0 + rs + sl * RSETS >= NB) continue;
+                    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(kf[ks], qf[sl][ks], acc);
-                if (pure_vis) {
-                    const float z0 = acc[0] * s.scale2, z1 = acc[1] * s.scale2;
-                    const float z2 = acc[2] * s.scale2, z3 = acc[3] * s.scale2;
-                    const float mx = fmaxf(fmaxf(z0, z1), fmaxf(z2, z3));
-                    if (mx > m[sl]) {
-                        const float sc = fast_exp2(m[sl] - mx);
-                        lsum[sl] *= sc;
-                        vsum[sl] *= sc;
-                        m[sl] = mx;
-                    }
-                    const float e = (fast_exp2(z0 - m[sl]) + fast_exp2(z1 - m[sl])) +
-                                    (fast_exp2(z2 - m[sl]) + fast_exp2(z3 - m[sl]));
-                    lsum[sl] += e;
-                    vsum[sl] += e;
-                } else {
-                    float z[4];
-                    bool ok[4], isv[4];
-                    float mx = kNegInf;
+                    for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(kf[ks], qf[sl][ks], acc);
+                    if (pure_vis) {
+                        const float z0 = acc[0] * s.scale2, z1 = acc[1] * s.scale2;
+                        const float z2 = acc[2] * s.scale2, z3 = acc[3] * s.scale2;
+                        const float mx = fmaxf(fmaxf(z0, z1), fmaxf(z2, z3));
+                        if (mx > m[sl]) {
+                            const float sc = fast_exp2(m[sl] - mx);
+                            lsum[sl] *= sc;
+                            vsum[sl] *= sc;
+                            m[sl] = mx;
+                        }
+                        const float e = (fast_exp2(z0 - m[sl]) + fast_exp2(z1 - m[sl])) +
+                                        (fast_exp2(z2 - m[sl]) + fast_exp2(z3 - m[sl]));
+                        lsum[sl] += e;
+                        vsum[sl] += e;
+                    } else {
+                        float z[4];
+                        bool ok[4], isv[4];
+                        float mx = kNegInf;
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        const int key = kfirst + j;
-                        ok[j] = key < kend && (key < vis1 || key - vis1 <= qrow[sl]);
-                        isv[j] = key >= vis0 && key < vis1;
-                        z[j] = ok[j] ? acc[j] * s.scale2 : kNegInf;
-                        mx = fmaxf(mx, z[j]);
-                    }
-                    if (mx > m[sl]) {
-                        const float sc = fast_exp2(m[sl] - mx);
-                        lsum[sl] *= sc;
-                        vsum[sl] *= sc;
-                        m[sl] = mx;
-                    }
+                        for (int j = 0; j < 4; ++j) {
+                            const int key = kfirst + j;
+                            ok[j] = key < kend && (key < vis1 || key - vis1 <= qrow[sl]);
+                            isv[j] = key >= vis0 && key < vis1;
+                            z[j] = ok[j] ? acc[j] * s.scale2 : kNegInf;
+                            mx = fmaxf(mx, z[j]);
+                        }
+                        if (mx > m[sl]) {
+                            const float sc = fast_exp2(m[sl] - mx);
+                            lsum[sl] *= sc;
+                            vsum[sl] *= sc;
+                            m[sl] = mx;
+                        }
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        if (ok[j]) {
-                            const float e = fast_exp2(z[j] - m[sl]);
-                            lsum[sl] += e;
-                            if (isv[j]) vsum[sl] += e;
+                        for (int j = 0; j < 4; ++j) {
+                            if (ok[j]) {
+                                const float e = fast_exp2(z[j] - m[sl]);
+                                lsum[sl] += e;
+                                if (isv[j]) vsum[sl] += e;
+                            }
                         }
                     }
                 }
             }
-        }
-        if (t + 1 < ntiles) store_tile_lds<D>(tiles[(t + 1) & 1], pre, tid);
-        __syncthreads();
-    }
+        },
+        [](int, int) {});
     // the four lane quarters of a wave saw different keys of the same rows
 #pragma unroll
     for (int sl = 0; sl < NSLOT; ++sl) {
@@ -223,7 +297,7 @@ __device__ void stats_sweep(const Shape& s, const uint16_t* kbase, int kbeg, int
 
 // Per-lane row coefficients of the vision sweep: the accumulator rows of a lane
 // are 4*(lane/16) + j of each block; lse2 in base-2 units, coef = w~_i / heads.
-template <int NSLOT, int KS>
+template <int NSLOT, int KS, bool SETTLE = true>
 __device__ __forceinline__ void load_row_coefs(const Shape& s, int bl, int kvh, int rb0, const float* lse,
                                                const float* w_txt, float (&lse2)[NSLOT][4],
                                                float (&coef)[NSLOT][4]) {
@@ -234,79 +308,100 @@ __device__ __forceinline__ void load_row_coefs(const Shape& s, int bl, int kvh, 
     const int NB = s.G * QB;
     const float inv_heads = s.head_mode == 0 ? 1.0f / (float)s.H : 1.0f / (float)s.G;
     const size_t wrow = s.head_mode == 0 ? (size_t)bl * s.Nt : ((size_t)bl * s.Hkv + kvh) * s.Nt;
+    // every load is issued (invalid rows read row 0 of the unit) so that they are all
+    // in flight together; invalid rows then get zero coefficients
+    float lv[NSLOT][4], wv[NSLOT][4];
+    bool ok[NSLOT][4];
 #pragma unroll
     for (int sl = 0; sl < NSLOT; ++sl) {
         const int rb = rb0 + rs + sl * RSETS;
-        const int g = rb / QB;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int qj = (rb % QB) * 16 + (lane >> 4) * 4 + j;
-            lse2[sl][j] = 0.f;
-            coef[sl][j] = 0.f;
-            if (rb < NB && qj < s.Nq) {
-                const size_t head = (size_t)bl * s.H + kvh * s.G + g;
-                lse2[sl][j] = lse[head * s.Nt + s.Ns + qj] * kLog2e;
-                coef[sl][j] = w_txt[wrow + s.Ns + qj] * inv_heads;
-            }
+            ok[sl][j] = rb < NB && qj < s.Nq;
+            const int g = ok[sl][j] ? rb / QB : 0;
+            const int qc = ok[sl][j] ? qj : 0;
+            const size_t head = (size_t)bl * s.H + kvh * s.G + g;
+            lv[sl][j] = lse[head * s.Nt + s.Ns + qc];
+            wv[sl][j] = w_txt[wrow + s.Ns + qc];
         }
+    }
+#pragma unroll
+    for (int sl = 0; sl < NSLOT; ++sl)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            lse2[sl][j] = ok[sl][j] ? lv[sl][j] * kLog2e : 0.f;
+            coef[sl][j] = ok[sl][j] ? wv[sl][j] * inv_heads : 0.f;
+        }
+    if (SETTLE) {
+#pragma unroll
+        for (int sl = 0; sl < NSLOT; ++sl)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                settle(lse2[sl][j]);
+                settle(coef[sl][j]);
+            }
     }
 }
 
 // Vision sweep over vision keys [vbeg, vend) (vbeg a multiple of kTile; kvis
 // points at the first vision key of the unit): out[j] = sum over this
 // workgroup's rows of coef * exp(z - lse), for every key j of the range.
+// obuf: kOutTiles * kTile floats of LDS.
 template <int D, int NSLOT, int KS>
 __device__ void vision_sweep(const Shape& s, const uint16_t* kvis, int vbeg, int vend,
                              const bf16x8 (&qf)[NSLOT][Geo<D>::KSTEPS], const float (&lse2)[NSLOT][4],
                              const float (&coef)[NSLOT][4], int rb0, int NB, char (*tiles)[Geo<D>::TILE_BYTES],
-                             float (*red)[4 / KS][kTile], float* out) {
+                             float (*red)[4 / KS][kTile], float* obuf, float* out) {
     using GG = Geo<D>;
     constexpr int RSETS = 4 / KS;
     constexpr int KBW = 4 / KS;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int rs = wave % RSETS, kp = wave / RSETS;
     const int ntiles = (vend - vbeg + kTile - 1) / kTile;
-    u32x4 pre[GG::LOADS];
-    if (ntiles > 0) {
-        load_tile_regs<D>(pre, kvis, vbeg, vend - 1, tid);
-        store_tile_lds<D>(tiles[0], pre, tid);
-    }
-    __syncthreads();
-    for (int t = 0; t < ntiles; ++t) {
-        const char* buf = tiles[t & 1];
-        const int key0 = vbeg + t * kTile;
-        if (t + 1 < ntiles) load_tile_regs<D>(pre, kvis, key0 + kTile, vend - 1, tid);
+    tile_pipeline<D, PipeDepth<NSLOT>::value>(
+        kvis, vbeg, vend, tiles,
+        [&](const char* buf, int key0, int t) {
 #pragma unroll
-        for (int kbi = 0; kbi < KBW; ++kbi) {
-            const int kb = kp + kbi * KS;
-            bf16x8 kf[GG::KSTEPS];
-            load_kfrag<D>(kf, buf, kb, lane);
-            float col = 0.f;
+            for (int kbi = 0; kbi < KBW; ++kbi) {
+                const int kb = kp + kbi * KS;
+                bf16x8 kf[GG::KSTEPS];
+                load_kfrag<D>(kf, buf, kb, lane);
+                float col = 0.f;
 #pragma unroll
-            for (int sl = 0; sl < NSLOT; ++sl) {
-                if (rb0 + rs + sl * RSETS >= NB) continue;
-                f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+                for (int sl = 0; sl < NSLOT; ++sl) {
+                    if (rb0 + rs + sl * RSETS >= NB) continue;
+                    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(qf[sl][ks], kf[ks], acc);
+                    for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(qf[sl][ks], kf[ks], acc);
 #pragma unroll
-                for (int j = 0; j < 4; ++j) col += coef[sl][j] * fast_exp2(acc[j] * s.scale2 - lse2[sl][j]);
+                    for (int j = 0; j < 4; ++j) col += coef[sl][j] * fast_exp2(acc[j] * s.scale2 - lse2[sl][j]);
+                }
+                col += shfl_xor(col, 16);
+                col += shfl_xor(col, 32);
+                if (lane < 16) red[t & 1][rs][kb * 16 + lane] = col;
             }
-            col += shfl_xor(col, 16);
-            col += shfl_xor(col, 32);
-            if (lane < 16) red[t & 1][rs][kb * 16 + lane] = col;
-        }
-        if (t + 1 < ntiles) store_tile_lds<D>(tiles[(t + 1) & 1], pre, tid);
-        __syncthreads();
-        if (tid < kTile) {
-            const int key = key0 + tid;
-            if (key < vend) {
+        },
+        [&](int, int t) {
+            // Each of the first 64 threads parks its key's score in its own LDS slot and
+            // writes kOutTiles of them at once, then waits for the writes: a global store
+            // pending among the tile loads would make the compiler drain every load in
+            // flight at each tile, not once per kOutTiles tiles.
+            if (tid < kTile) {
                 float a = 0.f;
 #pragma unroll
                 for (int r = 0; r < RSETS; ++r) a += red[t & 1][r][tid];
-                out[key] = a;
+                const int slot = t % kOutTiles;
+                obuf[slot * kTile + tid] = a;
+                if (slot == kOutTiles - 1 || t == ntiles - 1) {
+                    for (int i = 0; i <= slot; ++i) {
+                        const int key = vbeg + (t - slot + i) * kTile + tid;
+                        if (key < vend) out[key] = obuf[i * kTile + tid];
+                    }
+                    wait_vmem_all();
+                }
             }
-        }
-    }
+        });
     __syncthreads();
 }
 
@@ -314,6 +409,9 @@ __device__ void vision_sweep(const Shape& s, const uint16_t* kvis, int vbeg, int
 // question rows' normalisers.  Computes the system rows' normalisers (system
 // rows see only system keys, causally) into lse2s and lse, then the column sums
 // of the text->text probabilities per query head into ws_colsum [.., N_t].
+// The work is small and latency-bound: each wave walks its items with the next
+// block's 16-byte fragments fetched while the current block is used (two
+// register sets, loads clamped into the unit so that every one is issued).
 template <int D>
 __device__ void text_pass(const Shape& s, int bl, int kvh, const uint16_t* __restrict__ q_text,
                           const uint16_t* __restrict__ k, float* __restrict__ lse, float* lse2s,
@@ -323,23 +421,23 @@ __device__ void text_pass(const Shape& s, int bl, int kvh, const uint16_t* __res
     const size_t head0 = (size_t)bl * s.H + kvh * s.G;
     const uint16_t* kbase = k + ((size_t)bl * s.Hkv + kvh) * (size_t)s.N * D;
     const int koff = (lane >> 4) * 8;
+    auto load_frag = [&](bf16x8 (&f)[GG::KSTEPS], const uint16_t* row) {
+#pragma unroll
+        for (int ks = 0; ks < GG::KSTEPS; ++ks) f[ks] = as_bf16x8(load16(row + koff + ks * 32));
+    };
 
+    // system rows x system keys: row normalisers (C[key][row]: a lane owns row i)
     const int SB = (s.Ns + 15) >> 4;
     for (int item = wave; item < s.G * SB; item += 4) {
         const int g = item / SB, rb = item % SB;
         const int i = rb * 16 + (lane & 15);
         const bool rv = i < s.Ns;
-        bf16x8 qf[GG::KSTEPS];
-        const uint16_t* qp = q_text + ((head0 + g) * s.Nt + (rv ? i : 0)) * D + koff;
-#pragma unroll
-        for (int ks = 0; ks < GG::KSTEPS; ++ks) qf[ks] = rv ? as_bf16x8(load16(qp + ks * 32)) : zero_frag();
+        bf16x8 qf[GG::KSTEPS], ka[GG::KSTEPS], kb2[GG::KSTEPS];
+        load_frag(qf, q_text + ((head0 + g) * s.Nt + min(i, s.Ns - 1)) * D);
+        auto krow = [&](int kb) { return kbase + (size_t)min(kb * 16 + (lane & 15), s.Ns - 1) * D; };
+        load_frag(ka, krow(0));
         float m = kNegInf, l = 0.f, dummy = 0.f;
-        for (int kb = 0; kb <= rb; ++kb) {
-            const int jc = min(kb * 16 + (lane & 15), s.Ns - 1);
-            bf16x8 kf[GG::KSTEPS];
-#pragma unroll
-            for (int ks = 0; ks < GG::KSTEPS; ++ks)
-                kf[ks] = as_bf16x8(load16(kbase + (size_t)jc * D + koff + ks * 32));
+        auto step = [&](const bf16x8 (&kf)[GG::KSTEPS], int kb) {
             f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(kf[ks], qf[ks], acc);
@@ -358,6 +456,13 @@ __device__ void text_pass(const Shape& s, int bl, int kvh, const uint16_t* __res
 #pragma unroll
             for (int j = 0; j < 4; ++j)
                 if (z[j] != kNegInf) l += fast_exp2(z[j] - m);
+        };
+        // key blocks 0..rb; a block past rb is masked out by key <= i
+        for (int kb = 0; kb <= rb; kb += 2) {
+            load_frag(kb2, krow(kb + 1));
+            step(ka, kb);
+            load_frag(ka, krow(kb + 2));
+            step(kb2, kb + 1);
         }
 #pragma unroll
         for (int off = 16; off < 64; off <<= 1) {
@@ -372,24 +477,19 @@ __device__ void text_pass(const Shape& s, int bl, int kvh, const uint16_t* __res
     }
     __syncthreads();
 
+    // all text rows x text keys: column sums (C[row][key]: a lane owns key j)
     const int TB = (s.Nt + 15) >> 4;
     for (int item = wave; item < s.G * TB; item += 4) {
         const int g = item / TB, kb = item % TB;
         const int j = kb * 16 + (lane & 15);
         const int jc = min(j, s.Nt - 1);
         const int pos = jc < s.Ns ? jc : jc + s.Nv;
-        bf16x8 kf[GG::KSTEPS];
-#pragma unroll
-        for (int ks = 0; ks < GG::KSTEPS; ++ks)
-            kf[ks] = as_bf16x8(load16(kbase + (size_t)pos * D + koff + ks * 32));
+        auto qrow = [&](int rb) { return q_text + ((head0 + g) * s.Nt + min(rb * 16 + (lane & 15), s.Nt - 1)) * D; };
+        bf16x8 kf[GG::KSTEPS], qa[GG::KSTEPS], qb[GG::KSTEPS];
+        load_frag(kf, kbase + (size_t)pos * D);
+        load_frag(qa, qrow(kb));
         float col = 0.f;
-        for (int rb = kb; rb < TB; ++rb) {
-            const int i = rb * 16 + (lane & 15);
-            const bool rv = i < s.Nt;
-            bf16x8 qf[GG::KSTEPS];
-            const uint16_t* qp = q_text + ((head0 + g) * s.Nt + (rv ? i : 0)) * D + koff;
-#pragma unroll
-            for (int ks = 0; ks < GG::KSTEPS; ++ks) qf[ks] = rv ? as_bf16x8(load16(qp + ks * 32)) : zero_frag();
+        auto step = [&](const bf16x8 (&qf)[GG::KSTEPS], int rb) {
             f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(qf[ks], kf[ks], acc);
@@ -398,6 +498,13 @@ __device__ void text_pass(const Shape& s, int bl, int kvh, const uint16_t* __res
                 const int ii = rb * 16 + (lane >> 4) * 4 + jj;
                 if (ii < s.Nt && j <= ii) col += fast_exp2(acc[jj] * s.scale2 - lse2s[g * s.Nt + ii]);
             }
+        };
+        // row blocks kb..TB-1; a block past the last is masked out by ii < N_t
+        for (int rb = kb; rb < TB; rb += 2) {
+            load_frag(qb, qrow(rb + 1));
+            step(qa, rb);
+            load_frag(qa, qrow(rb + 2));
+            step(qb, rb + 1);
         }
         col += shfl_xor(col, 16);
         col += shfl_xor(col, 32);

@@ -77,6 +77,7 @@ __global__ __launch_bounds__(kThreads) void score_fused_kernel(
     constexpr int RSETS = 4 / KS;
     __shared__ __attribute__((aligned(16))) char tiles[2][Geo<D>::TILE_BYTES];
     __shared__ float red[2][RSETS][kTile];
+    __shared__ float obuf[kOutTiles * kTile];
     __shared__ float fin_red[kThreads];
     __shared__ float vm_s[kMaxQRows];
     __shared__ int sh_ticket, sh_flag;
@@ -215,7 +216,7 @@ __global__ __launch_bounds__(kThreads) void score_fused_kernel(
                     const uint16_t* kvis = k + ((size_t)u * s.N + s.Ns) * D;
                     const int vb = sp * fp.cv, ve = min(s.Nv, vb + fp.cv);
                     float* out = s.head_mode == 0 ? ws_part + (size_t)u * s.Nv : s_vis + (size_t)u * s.Nv;
-                    vision_sweep<D, NSLOT, KS>(s, kvis, vb, ve, qf, lse2, coef, 0, NB, tiles, red, out);
+                    vision_sweep<D, NSLOT, KS>(s, kvis, vb, ve, qf, lse2, coef, 0, NB, tiles, red, obuf, out);
                 }
                 if (s.head_mode == 0) {
                     if (tid == 0) {

@@ -40,6 +40,20 @@ __device__ __forceinline__ void store16_stream(void* p, u32x4 v) {
     __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
 }
 
+// Waits here for the load that produced v.  Values loaded before a loop and read
+// inside it otherwise get their wait inside the loop, where the compiler cannot
+// tell them apart from loads issued by earlier iterations and waits for every
+// outstanding load (vmcnt(0)), which would stall each iteration on its own
+// prefetch.
+template <typename T>
+__device__ __forceinline__ void settle(const T& v) {
+    asm volatile("" ::"v"(v));
+}
+
+// s_waitcnt vmcnt(0) (expcnt and lgkmcnt left at their maxima, gfx9 encoding):
+// waits for every vector memory access of the wave, stores included.
+__device__ __forceinline__ void wait_vmem_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
 // v_exp_f32: 2^x, exp2(-inf) = 0.
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 

@@ -50,6 +50,9 @@ hipError_t launch_score_fused(const Shape& s, const RowPlan& rp, const FusedPlan
 // Score phases.
 hipError_t launch_score_stats(const Shape& s, const RowPlan& rp, const uint16_t* q_text,
                               const uint16_t* k, float* lse, float* ws_vm, hipStream_t st);
+bool stats_text_eligible(const Shape& s, const RowPlan& rp);
+hipError_t launch_score_stats_text(const Shape& s, const RowPlan& rp, const uint16_t* q_text, const uint16_t* k,
+                                   float* lse, float* ws_vm, float* ws_colsum, float* ws_vmh, hipStream_t st);
 hipError_t launch_score_text(const Shape& s, const uint16_t* q_text, const uint16_t* k, float* lse,
                              const float* ws_vm, float* ws_colsum, float* ws_vmh, hipStream_t st);
 hipError_t launch_score_fin(const Shape& s, const float* ws_colsum, const float* ws_vmh, float* s_txt,
