@@ -71,6 +71,7 @@ def source_hash(files):
 
 
 KERNEL_SOURCES = {
+    "score_text": ["score.hip", "score_core.h", "tgvkv_device.h"],
     "score_stats": ["score.hip", "score_core.h", "tgvkv_device.h"],
     "score_vision": ["score.hip", "score_core.h", "tgvkv_device.h"],
     "compact": ["compact.hip", "tgvkv_device.h"],
@@ -141,8 +142,10 @@ def cpu_baseline(cfg, t, dec, tot, budget_s):
 
 
 COPY_BYTES = 1 << 30
-KERNEL_NAMES = {"score_stats": "score_stats_kernel", "score_vision": "score_vision_kernel",
-                "compact": "compact_kernel", "decode": "decode_kernel"}
+# bench stage -> the kernel whose counters stand for it ("score_text" is sweep 1 with the
+# text pass, the kernel the two-step schedule runs for that stage)
+KERNEL_NAMES = {"score_text": "score_stats_text_kernel", "score_stats": "score_stats_kernel",
+                "score_vision": "score_vision_kernel", "compact": "compact_kernel", "decode": "decode_kernel"}
 
 
 def calibrate_copy():
@@ -172,7 +175,7 @@ def _per_kernel_kib(rows, counter):
     return {k: sum(v) / len(v) for k, v in acc.items()}
 
 
-def ingest_counters(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, workload):
+def ingest_counters(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, workload, decode_steps):
     fetch = _per_kernel_kib(_counter_rows(fetch_csv), "FETCH_SIZE")
     write = _per_kernel_kib(_counter_rows(write_csv), "WRITE_SIZE")
     cf = _per_kernel_kib(_counter_rows(copy_fetch_csv), "FETCH_SIZE")
@@ -192,6 +195,8 @@ def ingest_counters(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, worklo
         fb, wb = max(fk) * scale_f, max(wk) * scale_w
         rec[key] = {"fetch_bytes": fb, "write_bytes": wb, "bytes_per_launch": fb + wb,
                     "source_hash": source_hash(KERNEL_SOURCES[key])}
+        if key == "decode":
+            rec[key]["decode_steps"] = decode_steps  # the counter run's mean over its steps
     try:
         with open(COUNTERS) as f:
             data = json.load(f)
@@ -207,7 +212,9 @@ def ingest_counters(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, worklo
 def main():
     args = parse()
     if args.ingest_counters:
-        ingest_counters(*args.ingest_counters, workload=args.workload)
+        from workloads import CONFIGS
+        T = CONFIGS[args.workload].decode_steps if args.decode_steps is None else args.decode_steps
+        ingest_counters(*args.ingest_counters, workload=args.workload, decode_steps=T)
         return
     if args.calibrate_copy:
         calibrate_copy()
