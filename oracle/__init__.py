@@ -8,6 +8,7 @@ from .tgvkv_oracle import (  # noqa: F401
     evict_sequence,
     flat_offsets,
     forced_positions,
+    forced_vision_count,
     head_average,
     layer_budgets,
     score_slice,
@@ -18,5 +19,6 @@ from .tgvkv_oracle import (  # noqa: F401
     tpr_select,
     tv_mass,
     vision_positions,
+    vision_only_budgets,
     vision_scores,
 )

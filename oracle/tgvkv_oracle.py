@@ -225,6 +225,28 @@ def layer_budgets(masses: Sequence[float], total_budget: int, n_tokens: int, n_f
     return out
 
 
+def forced_vision_count(n_sys: int, n_vis: int, n_qst: int, n_sink: int = 0, n_recent: int = 0) -> int:
+    """Number of forced positions (first n_sink, last n_recent) that are vision tokens."""
+    f = forced_positions(n_sys + n_vis + n_qst, n_sink, n_recent)
+    return int(np.count_nonzero((f >= n_sys) & (f < n_sys + n_vis)))
+
+
+def vision_only_budgets(masses: Sequence[float], vision_budget: int, n_text: int, n_vis: int,
+                        n_floor: int = 0) -> np.ndarray:
+    """Per-layer kept-token counts of vision-only eviction (App. B.3).
+
+    In this mode every layer keeps all of its N_t text tokens and the retention
+    ratio counts vision tokens only.  The per-sequence vision budget V_tot is
+    shared out over the layers by TVB exactly as the full budget is in
+    layer_budgets (Eq. (5)-(6)), with the per-layer cap n_vis and, as floor, the
+    forced positions that are vision tokens; layer l keeps b_l = N_t + v_l tokens.
+    Retention then always falls in the first case of Eq. (10).  Returns int64 [L].
+    """
+    if vision_budget < 0 or vision_budget > len(masses) * n_vis:
+        raise ValueError("vision budget outside [0, L*n_vis]")
+    return int(n_text) + layer_budgets(masses, vision_budget, n_vis, n_floor)
+
+
 # --------------------------------------------------------------------------- retention
 def tpr_select(s_vis: np.ndarray, s_txt: np.ndarray, budget: int, n_sys: int, n_vis: int,
                n_qst: int, n_sink: int = 0, n_recent: int = 0) -> np.ndarray:
@@ -297,12 +319,14 @@ def decode_attention(q: np.ndarray, Kc: Sequence[np.ndarray], Vc: Sequence[np.nd
 # --------------------------------------------------------------------------- whole slices
 def evict_sequence(q_text_seq, k_seq, n_sys, n_vis, n_qst, total_budget_per_seq, sm_scale=None,
                    head_mode=0, n_sink=0, n_recent=0, layers: Optional[Sequence[int]] = None,
-                   keep_P: bool = False):
+                   keep_P: bool = False, vision_only: bool = False):
     """Score, budget and select every layer of one sequence.
 
     q_text_seq [L][H][N_t][d], k_seq [L][H_kv][N][d] (any float dtype; used in float64).
-    Returns per-layer score dicts, the budgets [L] and the retained positions
-    per layer and group.
+    total_budget_per_seq is B_tot, or the vision budget V_tot with vision_only
+    (App. B.3; see vision_only_budgets).  Returns per-layer score dicts, the
+    budgets [L] (tokens kept per layer) and the retained positions per layer and
+    group.
     """
     L = len(k_seq)
     H_kv, N, d = np.shape(k_seq[0])
@@ -313,8 +337,13 @@ def evict_sequence(q_text_seq, k_seq, n_sys, n_vis, n_qst, total_budget_per_seq,
         if not keep_P:
             sc.pop("P")
         scores.append(sc)
-    nf = len(forced_positions(N, n_sink, n_recent))
-    budgets = layer_budgets([s["tv_mass"] for s in scores], total_budget_per_seq, N, nf)
+    masses = [s["tv_mass"] for s in scores]
+    if vision_only:
+        nfv = forced_vision_count(n_sys, n_vis, n_qst, n_sink, n_recent)
+        budgets = vision_only_budgets(masses, total_budget_per_seq, n_sys + n_qst, n_vis, nfv)
+    else:
+        nf = len(forced_positions(N, n_sink, n_recent))
+        budgets = layer_budgets(masses, total_budget_per_seq, N, nf)
     idx = []
     for l in range(L):
         g = scores[l]["s_vis"].shape[0]

@@ -358,6 +358,58 @@ def check_compact_and_decode(O, seed=7):
         assert np.array_equal(out0[0][h], vn[0][h // G])
 
 
+def check_vision_only(O, seed=8):
+    """Vision-only eviction (App. B.3): all text kept, the budget counts vision tokens."""
+    rng = np.random.default_rng(seed)
+    for L, nt, nv in [(1, 4, 10), (4, 3, 7), (32, 75, 576), (5, 0, 9)]:
+        for _ in range(4):
+            m = rng.random(L) * rng.choice([1e-3, 1.0, 50.0])
+            for V in sorted({0, 1, L * nv // 3, L * nv - 1, L * nv}):
+                b = O.vision_only_budgets(m, V, nt, nv)
+                # every layer keeps its text, the vision part respects the vision cap, sums add up
+                assert b.sum() == L * nt + V and b.min() >= nt and (b - nt).max() <= nv, (L, nt, nv, V, b)
+        # rho = 1 keeps every token, rho = 0 keeps exactly the text
+        assert np.all(O.vision_only_budgets(rng.random(L), L * nv, nt, nv) == nt + nv)
+        assert np.all(O.vision_only_budgets(rng.random(L), 0, nt, nv) == nt)
+    # equal masses: vision shares differ by at most one, extras on the lowest layers
+    L, nt, nv, V = 32, 99, 2880, 4608 + 7
+    b = O.vision_only_budgets([0.5] * L, V, nt, nv)
+    q, r = divmod(V, L)
+    assert list(b - nt) == [q + 1] * r + [q] * (L - r)
+    # the cap is the vision count, not the sequence length: a dominant layer stops at n_vis
+    assert list(O.vision_only_budgets([100.0, 1.0, 1.0, 1.0], 20, 5, 10)) == [15, 9, 8, 8]
+    # forced vision positions (a sink at position 0 with no system text) are the floor
+    assert O.forced_vision_count(0, 12, 3, n_sink=4, n_recent=1) == 4
+    assert O.forced_vision_count(2, 12, 3, n_sink=4, n_recent=1) == 2
+    b = O.vision_only_budgets([1.0, 0.0, 0.0, 0.0], 20, 3, 12, n_floor=4)
+    assert list(b) == [3 + 8, 3 + 4, 3 + 4, 3 + 4]
+    # retention: all text, then exactly b_l - N_t vision tokens, the top ones by s^V (brute force)
+    for _ in range(100):
+        ns, nv, nq = int(rng.integers(0, 4)), int(rng.integers(1, 12)), int(rng.integers(0, 4))
+        n = ns + nv + nq
+        sv = np.round(rng.standard_normal(nv), 1)        # coarse grid: many ties
+        st = np.round(rng.random(ns + nq), 1)
+        v = int(rng.integers(0, nv + 1))
+        keep = O.tpr_select(sv, st, ns + nq + v, ns, nv, nq)
+        text = set(range(ns)) | set(range(ns + nv, n))
+        assert text <= set(keep.tolist()) and len(keep) == ns + nq + v
+        best = sorted(range(nv), key=lambda j: (-sv[j], j))[:v]
+        assert sorted(set(keep.tolist()) - text) == sorted(ns + j for j in best)
+    # whole sequence: budgets and sets of every layer
+    ns, nv, nq, L = 3, 20, 4, 3
+    q, k = [], []
+    for _ in range(L):
+        qq, kk = _tiny_inputs(rng, n_sys=ns, n_vis=nv, n_qst=nq)
+        q.append(qq)
+        k.append(kk)
+    V = 17
+    scores, b, idx = O.evict_sequence(q, k, ns, nv, nq, V, vision_only=True)
+    assert b.sum() == L * (ns + nq) + V
+    text = set(range(ns)) | set(range(ns + nv, ns + nv + nq))
+    for l in range(L):
+        assert text <= set(idx[l][0].tolist()) and len(idx[l][0]) == b[l]
+
+
 ALL_CHECKS = [
     check_softmax_rows,
     check_mass_split,
@@ -368,4 +420,5 @@ ALL_CHECKS = [
     check_efficiency_memory,
     check_tpr,
     check_compact_and_decode,
+    check_vision_only,
 ]

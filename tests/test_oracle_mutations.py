@@ -14,7 +14,7 @@ from tests import oracle_pins as pins
 
 _orig = {name: getattr(O, name) for name in
          ("text_row_softmax", "text_scores", "text_weights", "vision_scores", "tv_mass",
-          "head_average", "layer_budgets", "tpr_select", "decode_attention")}
+          "head_average", "layer_budgets", "tpr_select", "decode_attention", "vision_only_budgets")}
 
 
 def _softmax_mask_off_by_one(q_text, k, n_sys, n_vis, n_qst, sm_scale):
@@ -126,6 +126,16 @@ def _decode_no_scale(q, Kc, Vc, sm_scale):
     return _orig["decode_attention"](q, Kc, Vc, 1.0)
 
 
+def _vision_only_cap_at_sequence_length(masses, vision_budget, n_text, n_vis, n_floor=0):
+    # caps a layer's vision share at N (text + vision) instead of n_vis
+    return int(n_text) + O.layer_budgets(masses, vision_budget, n_vis + n_text, n_floor)
+
+
+def _vision_only_drops_text(masses, vision_budget, n_text, n_vis, n_floor=0):
+    # forgets that every layer also keeps its text tokens
+    return _orig["vision_only_budgets"](masses, vision_budget, 0, n_vis, n_floor)
+
+
 MUTANTS = {
     "softmax_mask_off_by_one": ("text_row_softmax", _softmax_mask_off_by_one),
     "softmax_wrong_kv_head": ("text_row_softmax", _softmax_wrong_kv_head),
@@ -143,6 +153,8 @@ MUTANTS = {
     "tpr_ties_to_higher_position": ("tpr_select", _tpr_ties_to_higher_position),
     "tpr_vision_first": ("tpr_select", _tpr_vision_first),
     "decode_no_scale": ("decode_attention", _decode_no_scale),
+    "vision_only_cap_at_sequence_length": ("vision_only_budgets", _vision_only_cap_at_sequence_length),
+    "vision_only_drops_text": ("vision_only_budgets", _vision_only_drops_text),
 }
 
 
