@@ -44,6 +44,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="llavanext")
     ap.add_argument("--rho", type=float, default=None, help="retention ratio (default: the workload's first)")
+    ap.add_argument("--vision-only", action="store_true",
+                    help="vision-only eviction (every layer keeps all text; rho is the retained share of the "
+                         "vision tokens) instead of eviction among all tokens")
     ap.add_argument("--decode-steps", type=int, default=None)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -79,6 +82,11 @@ KERNEL_SOURCES = {
 }
 
 
+def counter_key(workload, vision_only=False):
+    """Key of a workload's counters in profiles/hbm_counters.json (the eviction mode changes the bytes)."""
+    return workload + (":vision_only" if vision_only else "")
+
+
 def traffic_for(kernel, workload, decode_steps=None):
     """HBM bytes per launch from committed rocprofv3 counters, if they match the current source."""
     try:
@@ -94,7 +102,7 @@ def traffic_for(kernel, workload, decode_steps=None):
     return rec.get("bytes_per_launch")
 
 
-def cpu_baseline(cfg, t, dec, tot, budget_s):
+def cpu_baseline(cfg, t, dec, tot, budget_s, vision_only=False):
     """The fp64 oracle, as it stands, on whole sequences of the same inputs until ~budget_s seconds."""
     import numpy as np
     import oracle.tgvkv_oracle as O
@@ -110,7 +118,7 @@ def cpu_baseline(cfg, t, dec, tot, budget_s):
     for b in range(cfg.batch):
         q = bf16_bits_to_f32(t["q_text"][b])
         k = bf16_bits_to_f32(t["k"][b])
-        _, budgets, idx = O.evict_sequence(q, k, cfg.n_sys, cfg.n_vis, cfg.n_qst, tot)
+        _, budgets, idx = O.evict_sequence(q, k, cfg.n_sys, cfg.n_vis, cfg.n_qst, tot, vision_only=vision_only)
         for l in range(cfg.layers):
             O.compact_slice(t["k"][b, l], t["v"][b, l], idx[l], 0)
         if idx0 is None:
@@ -214,7 +222,7 @@ def main():
     if args.ingest_counters:
         from workloads import CONFIGS
         T = CONFIGS[args.workload].decode_steps if args.decode_steps is None else args.decode_steps
-        ingest_counters(*args.ingest_counters, workload=args.workload, decode_steps=T)
+        ingest_counters(*args.ingest_counters, workload=counter_key(args.workload, args.vision_only), decode_steps=T)
         return
     if args.calibrate_copy:
         calibrate_copy()
@@ -239,7 +247,8 @@ def main():
     rho = args.rho if args.rho is not None else cfg.rhos[0]
     T = cfg.decode_steps if args.decode_steps is None else args.decode_steps
     B, L, N = cfg.batch, cfg.layers, cfg.n_tokens
-    tot = total_budget(rho, N, L)
+    # vision-only: the budget counts vision tokens (no forced positions are used here)
+    tot = total_budget(rho, cfg.n_vis if args.vision_only else N, L)
 
     t0 = time.perf_counter()
     t = make_prefill_tensors(cfg, seed=args.seed)
@@ -252,7 +261,8 @@ def main():
     q_d, k_d, v_d = dev(t["q_text"]), dev(t["k"]), dev(t["v"])
     dq, dk, dv = dev(dec["q"]), dev(dec["k_new"]), dev(dec["v_new"])
     p = bd.problem_from(cfg)
-    buf = bd.EvictionBuffers(p, None, tot, max(T, 1))
+    opts = bd.make_opts(vision_only=args.vision_only)
+    buf = bd.EvictionBuffers(p, opts, tot, max(T, 1))
     stream = torch.cuda.current_stream()
 
     def one_step(events=None):
@@ -307,6 +317,7 @@ def main():
     budgets = buf.budgets.cpu().numpy()
     thr = buf.forced_or_text()
     vis_layers = int((budgets > thr).sum()) if sched in ("two_step", "fused_text") else B * L
+    kept = buf.kept  # tokens each sequence keeps
     k_bytes = B * L * Hkv * N * D * 2
     q_bytes = B * L * H * cfg.n_text * D * 2
     alg = {
@@ -314,8 +325,8 @@ def main():
         "score_text": k_bytes + q_bytes,
         "score_stats": k_bytes + B * L * H * Nq * D * 2,
         "score_vision": vis_layers * (Hkv * Nv * D * 2 + H * Nq * D * 2),
-        "compact": 4 * B * tot * Hkv * D * 2,
-        "decode": (B * tot + B * L * (T + 1) / 2.0) * Hkv * D * 4 + B * L * (H * D * 2 + 2 * Hkv * D * 2 + H * D * 4),
+        "compact": 4 * B * kept * Hkv * D * 2,
+        "decode": (B * kept + B * L * (T + 1) / 2.0) * Hkv * D * 4 + B * L * (H * D * 2 + 2 * Hkv * D * 2 + H * D * 4),
     }
     roofs = {}
     for kname in ("score", "score_text", "score_stats", "score_vision", "compact", "decode"):
@@ -324,7 +335,8 @@ def main():
             continue
         gbs = alg[kname] / (ms * 1e-3) / 1e9
         roofs[kname] = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                        "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic_for(kname, cfg.name, T),
+                        "frac": round(gbs / HBM_PEAK_GBS, 4),
+                        "traffic": traffic_for(kname, counter_key(cfg.name, args.vision_only), T),
                         "kernel": kname, "alg_bytes_per_launch": int(alg[kname]), "avg_launch_ms": round(ms, 4),
                         "ms_per_step": round(ms * (T if kname == "decode" else 1), 4)}
     dominant = max(roofs, key=lambda k: roofs[k]["ms_per_step"])
@@ -346,9 +358,11 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": f"{cfg.name}: batch {B}, {L} layers, {H} heads ({Hkv} KV), head_dim {D}, "
-                               f"{cfg.n_sys}+{Nv}+{Nq} tokens, retention {rho:g}, {T} decode steps",
+                               f"{cfg.n_sys}+{Nv}+{Nq} tokens, retention {rho:g}"
+                               f"{' of vision tokens (all text kept)' if args.vision_only else ''}, {T} decode steps",
                    "batch": B, "layers": L, "heads_q": H, "heads_kv": Hkv, "head_dim": D,
                    "n_sys": cfg.n_sys, "n_vis": Nv, "n_qst": Nq, "retention": rho, "total_budget_per_seq": tot,
+                   "vision_only": bool(args.vision_only),
                    "decode_steps": T, "vision_scored_layers": vis_layers, "schedule": sched},
         "evict_ms": round(evict_ms, 4),
         "decode_us_per_step": round(dec_ms * 1e3, 2),
@@ -361,7 +375,7 @@ def main():
         "wall_ms_per_step": round(wall / args.steps * 1e3, 3),
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(cfg, t, dec, tot, args.cpu_seconds)
+        line["cpu_baseline"] = cpu_baseline(cfg, t, dec, tot, args.cpu_seconds, args.vision_only)
     print(json.dumps(line), flush=True)
 
 

@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define TGVKV_ABI_VERSION 1
+#define TGVKV_ABI_VERSION 2
 
 typedef enum tgvkv_status {
     TGVKV_OK = 0,
@@ -71,12 +71,15 @@ typedef struct tgvkv_problem {
     int32_t n_qst;
 } tgvkv_problem;
 
-/* Options.  Passing NULL selects the defaults {0, 0, 0, 0}. */
+/* Options.  Passing NULL selects the defaults {0, 0, 0, 0, 0}. */
 typedef struct tgvkv_opts {
-    float   sm_scale;   /* logit scale; <= 0 selects 1/sqrt(head_dim)                        */
-    int32_t head_mode;  /* 0: per-layer retained set (paper); 1: per-KV-head retained sets   */
-    int32_t n_sink;     /* first n_sink positions are always kept (App. A.2 keeps 4)          */
-    int32_t n_recent;   /* last n_recent positions are always kept (App. A.2 keeps 1)         */
+    float   sm_scale;    /* logit scale; <= 0 selects 1/sqrt(head_dim)                       */
+    int32_t head_mode;   /* 0: per-layer retained set (paper); 1: per-KV-head retained sets  */
+    int32_t n_sink;      /* first n_sink positions are always kept (App. A.2 keeps 4)         */
+    int32_t n_recent;    /* last n_recent positions are always kept (App. A.2 keeps 1)        */
+    int32_t vision_only; /* 0: evict among all tokens (TPR, Eq. (10)); 1: vision-only eviction
+                            of App. B.3: every layer keeps all text, and the budget given to
+                            tgvkv_budget counts vision tokens only (see there)                */
 } tgvkv_opts;
 
 /* Score phases (bit mask for tgvkv_score). */
@@ -141,15 +144,25 @@ tgvkv_status tgvkv_score(const tgvkv_problem* problem, const tgvkv_opts* opts, i
  * masses count as 0); then largest-remainder rounding with ties to the lower
  * layer.  float64 throughout.  sum_l b_l == total for every sequence.
  *
+ * With opts.vision_only (App. B.3: all text kept, the retention ratio counts
+ * vision tokens) every layer keeps its N_t text tokens and its F_v forced vision
+ * positions; total_budget is the vision budget V_tot (e.g. round(rho * n_vis * L))
+ * over the other vision tokens, shared out the same way with N replaced by
+ * n_vis - F_v and no floor; layer l keeps b_l = N_t + F_v + v_l tokens, so
+ * sum_l b_l == L*(N_t + F_v) + V_tot.
+ *
  * tv_mass        f32   [B][L]     per-layer masses (from tgvkv_score)
- * total_budget   per-sequence budget B_tot (e.g. round(rho * N * L)), 0 <= B_tot <= L*N
+ * total_budget   per-sequence budget B_tot (e.g. round(rho * N * L)), 0 <= B_tot <= L*N;
+ *                with vision_only V_tot, 0 <= V_tot <= L*(n_vis - F_v)
  * decode_reserve token slots reserved after each layer's retained tokens for decode (>= 0)
  * budgets        int32 [B][L]     out
  * idx_offsets    int64 [B*L + 1]  out: start of each (b, l) block of tgvkv_select's output,
- *                                 block size g * b_l; idx_offsets[B*L] = B * B_tot * g
+ *                                 block size g * b_l; idx_offsets[B*L] = B * K * g, where
+ *                                 K = B_tot (K = L*(N_t + F_v) + V_tot with vision_only) is the
+ *                                 number of tokens each sequence keeps
  * seg_offsets    int64 [B*L + 1]  out: start of each (b, l) cache segment, in units of
  *                                 heads_kv * head_dim elements; segment size b_l + reserve;
- *                                 seg_offsets[B*L] = B * (B_tot + L * reserve)
+ *                                 seg_offsets[B*L] = B * (K + L * reserve)
  */
 tgvkv_status tgvkv_budget(const tgvkv_problem* problem, const tgvkv_opts* opts,
                           const float* tv_mass, int64_t total_budget, int32_t decode_reserve,
@@ -182,7 +195,7 @@ tgvkv_status tgvkv_select(const tgvkv_problem* problem, const tgvkv_opts* opts,
  * with cap = b_l + decode_reserve and I the (group of h's) retained set.  Same for v.
  * Bit-exact copy.  Slots b_l .. cap-1 are left for tgvkv_decode_attn.
  * total_budget / decode_reserve: the values given to tgvkv_budget (they size the
- * launch on the host: B * total_budget rows per KV head are moved).
+ * launch on the host: B * K rows per KV head are moved, K as in tgvkv_budget).
  * kc, vc  bf16, seg_offsets[B*L] * heads_kv * head_dim elements each.
  */
 tgvkv_status tgvkv_compact(const tgvkv_problem* problem, const tgvkv_opts* opts,

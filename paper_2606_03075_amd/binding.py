@@ -33,7 +33,7 @@ class TgvkvProblem(ctypes.Structure):
 
 class TgvkvOpts(ctypes.Structure):
     _fields_ = [("sm_scale", ctypes.c_float), ("head_mode", ctypes.c_int32), ("n_sink", ctypes.c_int32),
-                ("n_recent", ctypes.c_int32)]
+                ("n_recent", ctypes.c_int32), ("vision_only", ctypes.c_int32)]
 
 
 class TgvkvError(RuntimeError):
@@ -85,8 +85,32 @@ def problem_from(cfg) -> TgvkvProblem:
                         cfg.n_qst)
 
 
-def make_opts(sm_scale: float = 0.0, head_mode: int = 0, n_sink: int = 0, n_recent: int = 0) -> TgvkvOpts:
-    return TgvkvOpts(sm_scale, head_mode, n_sink, n_recent)
+def make_opts(sm_scale: float = 0.0, head_mode: int = 0, n_sink: int = 0, n_recent: int = 0,
+              vision_only: bool = False) -> TgvkvOpts:
+    return TgvkvOpts(sm_scale, head_mode, n_sink, n_recent, int(bool(vision_only)))
+
+
+def forced_or_text_count(problem, opts) -> int:
+    """|forced U T|: the text tokens plus the forced positions (first n_sink, last n_recent) that are vision."""
+    p, o = problem, opts
+    N = p.n_sys + p.n_vis + p.n_qst
+    n_sink = o.n_sink if o is not None else 0
+    n_recent = o.n_recent if o is not None else 0
+    fs = min(n_sink, N)
+    fr = max(N - n_recent, fs)
+    v0, v1 = p.n_sys, p.n_sys + p.n_vis
+    fv = max(0, min(fs, v1) - v0) + max(0, v1 - max(fr, v0))
+    return p.n_sys + p.n_qst + fv
+
+
+def kept_per_sequence(problem, opts, total_budget: int) -> int:
+    """Tokens one sequence keeps for a total_budget given to tgvkv_budget (its idx / cache sizing).
+
+    With vision-only eviction every layer also keeps its text and forced vision positions.
+    """
+    if opts is not None and opts.vision_only:
+        return int(total_budget) + problem.layers * forced_or_text_count(problem, opts)
+    return int(total_budget)
 
 
 def status_string(status: int) -> str:
@@ -222,8 +246,9 @@ class EvictionBuffers:
         self.budgets = torch.empty((B, L), dtype=torch.int32, device=device)
         self.idx_offsets = torch.empty((B * L + 1,), dtype=torch.int64, device=device)
         self.seg_offsets = torch.empty((B * L + 1,), dtype=torch.int64, device=device)
-        self.idx = torch.empty((max(1, B * self.total_budget * g),), dtype=torch.int32, device=device)
-        slots = B * (self.total_budget + L * self.decode_reserve)
+        self.kept = kept_per_sequence(p, opts, self.total_budget)
+        self.idx = torch.empty((max(1, B * self.kept * g),), dtype=torch.int32, device=device)
+        slots = B * (self.kept + L * self.decode_reserve)
         self.kc = torch.empty((max(1, slots * Hkv * D),), dtype=torch.bfloat16, device=device)
         self.vc = torch.empty_like(self.kc)
         self.out = torch.empty((B, L, H, D), **f32)
@@ -250,15 +275,7 @@ class EvictionBuffers:
 
     def forced_or_text(self) -> int:
         """|forced U T|: a layer needs vision scores only when its budget exceeds this."""
-        p, o = self.problem, self.opts
-        N = p.n_sys + p.n_vis + p.n_qst
-        n_sink = o.n_sink if o is not None else 0
-        n_recent = o.n_recent if o is not None else 0
-        fs = min(n_sink, N)
-        fr = max(N - n_recent, fs)
-        v0, v1 = p.n_sys, p.n_sys + p.n_vis
-        fv = max(0, min(fs, v1) - v0) + max(0, v1 - max(fr, v0))
-        return p.n_sys + p.n_qst + fv
+        return forced_or_text_count(self.problem, self.opts)
 
     def schedule(self) -> str:
         """'two_step': text statistics and text scores, budgets, then vision scores only for the

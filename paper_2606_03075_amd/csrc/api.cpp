@@ -38,6 +38,7 @@ tgvkv_status make_shape(const tgvkv_problem* p, const tgvkv_opts* o, Shape* s) {
     if (N < 1) return TGVKV_E_INVAL;
     if (d.head_mode != 0 && d.head_mode != 1) return TGVKV_E_INVAL;
     if (d.n_sink < 0 || d.n_recent < 0) return TGVKV_E_INVAL;
+    if (d.vision_only != 0 && d.vision_only != 1) return TGVKV_E_INVAL;
     if (!std::isfinite(d.sm_scale)) return TGVKV_E_INVAL;
     if (p->head_dim != 64 && p->head_dim != 128) return TGVKV_E_UNSUPPORTED;
     if (p->layers > kMaxLayers || N > kMaxTokens) return TGVKV_E_UNSUPPORTED;
@@ -61,6 +62,7 @@ tgvkv_status make_shape(const tgvkv_problem* p, const tgvkv_opts* o, Shape* s) {
     s->ngroups = d.head_mode == 0 ? 1 : p->heads_kv;
     s->n_sink = d.n_sink;
     s->n_recent = d.n_recent;
+    s->vision_only = d.vision_only;
     s->sm_scale = d.sm_scale > 0.f ? d.sm_scale : 1.0f / std::sqrt((float)p->head_dim);
     s->scale2 = s->sm_scale * 1.4426950408889634f;
     return TGVKV_OK;
@@ -73,15 +75,30 @@ int32_t forced_count(const Shape& s) {
     return (int32_t)(fs + (s.N - fr));
 }
 
-// |forced U T|: a layer needs vision scores only when its budget exceeds this.
-int32_t forced_or_text_count(const Shape& s) {
+// Forced positions that are vision tokens.
+int32_t forced_vision_count(const Shape& s) {
     const int64_t fs = std::min<int64_t>(s.n_sink, s.N);
     const int64_t fr = std::max<int64_t>(s.N - (int64_t)s.n_recent, fs);
     const int64_t v0 = s.Ns, v1 = (int64_t)s.Ns + s.Nv;
     int64_t fv = 0;
     fv += std::max<int64_t>(0, std::min(fs, v1) - v0);
     fv += std::max<int64_t>(0, v1 - std::max(fr, v0));
-    return (int32_t)(s.Nt + fv);
+    return (int32_t)fv;
+}
+
+// |forced U T|: a layer needs vision scores only when its budget exceeds this.
+int32_t forced_or_text_count(const Shape& s) { return s.Nt + forced_vision_count(s); }
+
+// Vision-only eviction (App. B.3): every layer keeps its text and its forced vision
+// positions; the budget shares out the other vision tokens.
+int32_t always_kept(const Shape& s) { return s.vision_only ? forced_or_text_count(s) : 0; }
+
+// Largest valid total_budget per sequence, and the tokens each sequence keeps for it.
+int64_t budget_capacity(const Shape& s) {
+    return (int64_t)s.L * (s.vision_only ? s.Nv - forced_vision_count(s) : s.N);
+}
+int64_t kept_per_sequence(const Shape& s, int64_t total_budget) {
+    return total_budget + (int64_t)s.L * always_kept(s);
 }
 
 struct ScoreWs {
@@ -222,13 +239,18 @@ tgvkv_status tgvkv_budget(const tgvkv_problem* problem, const tgvkv_opts* opts, 
     tgvkv_status st = make_shape(problem, opts, &s);
     if (st != TGVKV_OK) return st;
     if (decode_reserve < 0 || total_budget < 0) return TGVKV_E_INVAL;
-    if (total_budget > (int64_t)s.L * s.N) return TGVKV_E_CAPACITY;
+    if (total_budget > budget_capacity(s)) return TGVKV_E_CAPACITY;
     if (idx_offsets == nullptr || seg_offsets == nullptr) return TGVKV_E_INVAL;
     if (s.B > 0 && (tv_mass == nullptr || budgets == nullptr)) return TGVKV_E_INVAL;
-    const int64_t seg_total = (int64_t)s.B * (total_budget + (int64_t)s.L * decode_reserve);
+    const int64_t seg_total = (int64_t)s.B * (kept_per_sequence(s, total_budget) + (int64_t)s.L * decode_reserve);
     if (seg_total > (int64_t(1) << 40)) return TGVKV_E_UNSUPPORTED;
     if (s.B == 0) return TGVKV_OK;
-    return hip_status(tgvkv::launch_budget(s, tv_mass, total_budget, decode_reserve, forced_count(s), budgets,
+    // vision-only eviction (App. B.3): the budget is shared out over the vision tokens that
+    // are not forced, and every layer also keeps its text and forced vision positions
+    const int32_t cap = s.vision_only ? s.Nv - forced_vision_count(s) : s.N;
+    const int32_t add = always_kept(s);
+    const int32_t floor_n = s.vision_only ? 0 : forced_count(s);
+    return hip_status(tgvkv::launch_budget(s, tv_mass, total_budget, cap, add, decode_reserve, floor_n, budgets,
                                            idx_offsets, seg_offsets, stream));
 }
 
@@ -253,13 +275,14 @@ tgvkv_status tgvkv_compact(const tgvkv_problem* problem, const tgvkv_opts* opts,
     tgvkv_status st = make_shape(problem, opts, &s);
     if (st != TGVKV_OK) return st;
     if (decode_reserve < 0 || total_budget < 0) return TGVKV_E_INVAL;
-    if (total_budget > (int64_t)s.L * s.N) return TGVKV_E_CAPACITY;
-    if (s.B == 0 || total_budget == 0) return TGVKV_OK;
+    if (total_budget > budget_capacity(s)) return TGVKV_E_CAPACITY;
+    const int64_t kept = kept_per_sequence(s, total_budget);
+    if (s.B == 0 || kept == 0) return TGVKV_OK;
     if (k == nullptr || v == nullptr || idx == nullptr || budgets == nullptr || idx_offsets == nullptr ||
         seg_offsets == nullptr || kc == nullptr || vc == nullptr)
         return TGVKV_E_INVAL;
     if (!aligned16(k) || !aligned16(v) || !aligned16(kc) || !aligned16(vc)) return TGVKV_E_INVAL;
-    const int64_t rows = (int64_t)s.B * total_budget;
+    const int64_t rows = (int64_t)s.B * kept;
     if ((int64_t)s.B * s.L * 16 > kMaxBlocks || s.Hkv > 65535) return TGVKV_E_UNSUPPORTED;
     return hip_status(tgvkv::launch_compact(s, static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), idx,
                                             budgets, idx_offsets, seg_offsets, decode_reserve, rows,

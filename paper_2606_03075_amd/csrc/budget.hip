@@ -5,7 +5,8 @@
 // counts that retention (Eq. (10)) compares with N_t come from: a per-layer
 // floor (forced tokens) given first; the rest water-filled in proportion to
 // the shares with a cap of N per layer; largest-remainder rounding with ties to
-// the lower layer.
+// the lower layer.  Vision-only eviction (App. B.3) shares out a vision budget the
+// same way with the cap n_vis, and each layer then also keeps its N_t text tokens.
 //
 // One workgroup per sequence, layers spread over the threads.  Every float64
 // sum runs on one thread in layer order and no operation is contracted, so the
@@ -25,7 +26,8 @@ constexpr int kMaxLayers = 512;
 constexpr int kThreads = 256;
 
 __global__ __launch_bounds__(kThreads) void budget_kernel(Shape s, const float* __restrict__ tv_mass, long long total,
-                                                          int reserve, int n_forced, int32_t* __restrict__ budgets,
+                                                          int cap_tokens, int add, int reserve, int n_forced,
+                                                          int32_t* __restrict__ budgets,
                                                           int64_t* __restrict__ idx_off,
                                                           int64_t* __restrict__ seg_off) {
     __shared__ double f[kMaxLayers];
@@ -36,7 +38,7 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(Shape s, const float* 
     const int tid = threadIdx.x;
     const int b = blockIdx.x;
     const int L = s.L;
-    const long long N = s.N;
+    const long long N = cap_tokens;  // per-layer cap of the shared-out count
 
     long long F = n_forced;
     if (total / L < F) F = total / L;
@@ -125,30 +127,33 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(Shape s, const float* 
 
     if (tid == 0) {
         const long long g = s.ngroups;
-        long long io = (long long)b * total * g;
-        long long so = (long long)b * (total + (long long)L * reserve);
+        const long long kept = total + (long long)L * add;  // tokens each sequence keeps
+        long long io = (long long)b * kept * g;
+        long long so = (long long)b * (kept + (long long)L * reserve);
         for (int l = 0; l < L; ++l) {
             const size_t bl = (size_t)b * L + l;
-            budgets[bl] = (int32_t)bcount[l];
+            const long long bl_tokens = add + bcount[l];
+            budgets[bl] = (int32_t)bl_tokens;
             idx_off[bl] = io;
             seg_off[bl] = so;
-            io += g * bcount[l];
-            so += bcount[l] + reserve;
+            io += g * bl_tokens;
+            so += bl_tokens + reserve;
         }
         if (b == s.B - 1) {
-            idx_off[(size_t)s.B * L] = (long long)s.B * total * g;
-            seg_off[(size_t)s.B * L] = (long long)s.B * (total + (long long)L * reserve);
+            idx_off[(size_t)s.B * L] = (long long)s.B * kept * g;
+            seg_off[(size_t)s.B * L] = (long long)s.B * (kept + (long long)L * reserve);
         }
     }
 }
 
 }  // namespace
 
-hipError_t launch_budget(const Shape& s, const float* tv_mass, int64_t total, int32_t reserve, int32_t n_forced,
-                         int32_t* budgets, int64_t* idx_off, int64_t* seg_off, hipStream_t st) {
+hipError_t launch_budget(const Shape& s, const float* tv_mass, int64_t total, int32_t cap_tokens, int32_t add,
+                         int32_t reserve, int32_t n_floor, int32_t* budgets, int64_t* idx_off, int64_t* seg_off,
+                         hipStream_t st) {
     if (s.B == 0) return hipSuccess;
-    hipLaunchKernelGGL(budget_kernel, dim3(s.B), dim3(kThreads), 0, st, s, tv_mass, (long long)total, reserve,
-                       n_forced, budgets, idx_off, seg_off);
+    hipLaunchKernelGGL(budget_kernel, dim3(s.B), dim3(kThreads), 0, st, s, tv_mass, (long long)total, cap_tokens,
+                       add, reserve, n_floor, budgets, idx_off, seg_off);
     return hipGetLastError();
 }
 

@@ -11,6 +11,7 @@ struct Shape {
     int32_t Ns, Nv, Nq, N, Nt;
     int32_t head_mode, ngroups;
     int32_t n_sink, n_recent;
+    int32_t vision_only;  // every layer keeps all text; budgets count vision tokens
     float sm_scale;
     float scale2;  // sm_scale * log2(e): logits in base-2 units
 };
@@ -65,8 +66,10 @@ hipError_t launch_score_vis_reduce(const Shape& s, const RowPlan& rp, const floa
                                    const int32_t* budgets, int32_t vis_threshold, float* s_vis,
                                    hipStream_t st);
 
-hipError_t launch_budget(const Shape& s, const float* tv_mass, int64_t total, int32_t reserve,
-                         int32_t n_forced, int32_t* budgets, int64_t* idx_off, int64_t* seg_off,
+// Water-fills `total` over the layers with per-layer cap `cap_tokens` and floor
+// n_floor, then writes b_l = add + share (add = N_t in vision-only eviction).
+hipError_t launch_budget(const Shape& s, const float* tv_mass, int64_t total, int32_t cap_tokens, int32_t add,
+                         int32_t reserve, int32_t n_floor, int32_t* budgets, int64_t* idx_off, int64_t* seg_off,
                          hipStream_t st);
 hipError_t launch_select(const Shape& s, const float* s_vis, const float* s_txt, const int32_t* budgets,
                          const int64_t* idx_off, int32_t* idx, hipStream_t st);

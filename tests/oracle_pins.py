@@ -378,11 +378,14 @@ def check_vision_only(O, seed=8):
     assert list(b - nt) == [q + 1] * r + [q] * (L - r)
     # the cap is the vision count, not the sequence length: a dominant layer stops at n_vis
     assert list(O.vision_only_budgets([100.0, 1.0, 1.0, 1.0], 20, 5, 10)) == [15, 9, 8, 8]
-    # forced vision positions (a sink at position 0 with no system text) are the floor
+    # forced vision positions (a sink at position 0 with no system text) are kept like the text;
+    # the budget shares out the other vision tokens
     assert O.forced_vision_count(0, 12, 3, n_sink=4, n_recent=1) == 4
     assert O.forced_vision_count(2, 12, 3, n_sink=4, n_recent=1) == 2
-    b = O.vision_only_budgets([1.0, 0.0, 0.0, 0.0], 20, 3, 12, n_floor=4)
-    assert list(b) == [3 + 8, 3 + 4, 3 + 4, 3 + 4]
+    assert O.forced_vision_count(5, 12, 3, n_sink=4, n_recent=1) == 0
+    b = O.vision_only_budgets([1.0, 0.0, 0.0, 0.0], 20, 3, 12, n_forced_vis=4)
+    assert list(b) == [3 + 4 + 8, 3 + 4 + 4, 3 + 4 + 4, 3 + 4 + 4]
+    assert np.all(O.vision_only_budgets([1.0, 2.0], 0, 3, 12, n_forced_vis=4) == 7)
     # retention: all text, then exactly b_l - N_t vision tokens, the top ones by s^V (brute force)
     for _ in range(100):
         ns, nv, nq = int(rng.integers(0, 4)), int(rng.integers(1, 12)), int(rng.integers(0, 4))

@@ -44,7 +44,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(bd.EXPORTS) <= set(names) and len(names) == len(bd.EXPORTS), names
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.tgvkv_abi_version() == 1
+    assert lib.tgvkv_abi_version() == 2
     for st in (0, -1, -2, -3, -4, -5):
         assert lib.tgvkv_status_string(st)
     assert lib.tgvkv_status_string(7) == b"unknown status"
@@ -81,7 +81,8 @@ def test_validation_before_any_launch(lib):
         assert r == code, (bad.head_dim, r)
     assert lib.tgvkv_score(None, None, 7, fake, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
     # bad options
-    for o in (bd.make_opts(head_mode=2), bd.make_opts(n_sink=-1), bd.make_opts(sm_scale=float("nan"))):
+    for o in (bd.make_opts(head_mode=2), bd.make_opts(n_sink=-1), bd.make_opts(sm_scale=float("nan")),
+              bd.TgvkvOpts(0.0, 0, 0, 0, 2)):
         assert lib.tgvkv_score(ok, ctypes.byref(o), 7, fake, fake, fake, fake, fake, fake, fake, None, fake, big,
                                s) == -1
     # phases, null and misaligned pointers, workspace
@@ -104,6 +105,11 @@ def test_validation_before_any_launch(lib):
     assert lib.tgvkv_budget(ok, None, fake, -1, 0, fake, fake, fake, s) == -1
     assert lib.tgvkv_budget(ok, None, fake, 10, -1, fake, fake, fake, s) == -1
     assert lib.tgvkv_budget(ok, None, None, 10, 0, fake, fake, fake, s) == -1
+    # vision-only eviction: the budget counts vision tokens, at most L * n_vis
+    vo = ctypes.byref(bd.make_opts(vision_only=True))
+    Nv = 40
+    assert lib.tgvkv_budget(ok, vo, fake, L * Nv + 1, 0, fake, fake, fake, s) == -4
+    assert lib.tgvkv_compact(ok, vo, fake, fake, fake, fake, fake, fake, L * Nv + 1, 0, fake, fake, s) == -4
     # select / compact / decode arguments
     assert lib.tgvkv_select(ok, None, fake, fake, None, fake, fake, s) == -1
     assert lib.tgvkv_select(ok, None, None, fake, fake, fake, fake, s) == -1

@@ -17,15 +17,20 @@ pytestmark = pytest.mark.gpu
 
 
 def run_and_check(cfg, rho, head_mode=0, forced=(0, 0), steps=2, seed=0, skip_text_only=True, check_seqs=None,
-                  decode_seqs=None, schedule="auto"):
+                  decode_seqs=None, schedule="auto", vision_only=False):
     import torch
-    log(f"e2e {cfg.name} rho={rho} mode={head_mode} forced={forced} steps={steps}")
+    log(f"e2e {cfg.name} rho={rho} mode={head_mode} forced={forced} steps={steps} vision_only={vision_only}")
     t = make_prefill_tensors(cfg, seed=seed)
     dec = make_decode_tensors(cfg, seed=seed, steps=steps)
     B, L, N = cfg.batch, cfg.layers, cfg.n_tokens
-    tot = total_budget(rho, N, L)
     p = bd.problem_from(cfg)
-    o = bd.make_opts(head_mode=head_mode, n_sink=forced[0], n_recent=forced[1])
+    o = bd.make_opts(head_mode=head_mode, n_sink=forced[0], n_recent=forced[1], vision_only=vision_only)
+    # vision-only eviction (App. B.3): text and forced positions are all kept, rho is the retained
+    # share of the other vision tokens
+    nfv = O.forced_vision_count(cfg.n_sys, cfg.n_vis, cfg.n_qst, *forced)
+    tot = total_budget(rho, cfg.n_vis - nfv if vision_only else N, L)
+    kept = bd.kept_per_sequence(p, o, tot)
+    assert kept == tot + (L * (cfg.n_text + nfv) if vision_only else 0)
     buf = bd.EvictionBuffers(p, o, tot, max(steps, 1))
     q_d, k_d, v_d = dev_bf16(t["q_text"]), dev_bf16(t["k"]), dev_bf16(t["v"])
     sched = buf.evict(q_d, k_d, v_d, schedule=schedule if skip_text_only else "phases")
@@ -46,16 +51,22 @@ def run_and_check(cfg, rho, head_mode=0, forced=(0, 0), steps=2, seed=0, skip_te
     swaps = flips = 0
     tau = 1.0 / np.sqrt(cfg.head_dim)
     D, Hkv = cfg.head_dim, cfg.heads_kv
-    assert np.all(budgets.sum(axis=1) == tot)
+    assert np.all(budgets.sum(axis=1) == kept)
     check_seqs = range(B) if check_seqs is None else check_seqs
     decode_seqs = set(range(B) if decode_seqs is None else decode_seqs)
     for b in check_seqs:
         qf = bf16_bits_to_f32(t["q_text"][b])
         kf = bf16_bits_to_f32(t["k"][b])
         scores, ob, oidx = O.evict_sequence(qf, kf, cfg.n_sys, cfg.n_vis, cfg.n_qst, tot, None, head_mode,
-                                            *forced)
-        assert budgets[b].sum() == tot
-        ok_b = budget_allowed(budgets[b], ob, [s["tv_mass"] for s in scores], tot, N, nf)
+                                            *forced, vision_only=vision_only)
+        assert budgets[b].sum() == kept
+        masses = [s["tv_mass"] for s in scores]
+        if vision_only:
+            base = cfg.n_text + nfv
+            assert np.all(budgets[b] >= base)
+            ok_b = budget_allowed(budgets[b] - base, ob - base, masses, tot, cfg.n_vis - nfv, 0)
+        else:
+            ok_b = budget_allowed(budgets[b], ob, masses, tot, N, nf)
         assert ok_b, (b, budgets[b], ob)
         flips += int(np.abs(budgets[b] - ob).sum()) // 2
         for l in range(L):
@@ -140,3 +151,27 @@ def test_edge_shapes(lib):
     # budget 0 everywhere, then decode over the appended tokens only
     run_and_check(custom_config(name="zero", batch=1, layers=2, heads_q=4, heads_kv=4, n_sys=3, n_vis=40, n_qst=5),
                   0.0, steps=3)
+
+
+# ----------------------------------------------------------------------------- vision-only eviction
+@pytest.mark.parametrize("head_mode", [0, 1])
+@pytest.mark.parametrize("forced", [(0, 0), (4, 1)])
+def test_vision_only_small(lib, head_mode, forced):
+    cfg = custom_config(batch=2, layers=4, heads_q=8, heads_kv=4, head_dim=128, n_sys=6, n_vis=230, n_qst=21)
+    for rho in (0.0, 0.05, 0.3, 1.0):
+        run_and_check(cfg, rho, head_mode, forced, steps=3, seed=5, vision_only=True)
+    # no system text: the sink is a vision token and becomes each layer's floor
+    cfg = custom_config(name="nos", batch=1, layers=3, heads_q=4, heads_kv=4, head_dim=64, n_sys=0, n_vis=90,
+                        n_qst=17)
+    run_and_check(cfg, 0.1, head_mode, forced, steps=2, seed=6, vision_only=True)
+
+
+@pytest.mark.parametrize("rho", [0.05, 0.1, 0.2])
+def test_vision_only_llava15(lib, rho):
+    run_and_check(CONFIGS["llava15"], rho, steps=4, seed=0, vision_only=True)
+
+
+def test_vision_only_gqa_video(lib):
+    cfg = custom_config(name="vid", batch=2, layers=3, heads_q=28, heads_kv=4, head_dim=128, n_sys=16, n_vis=512,
+                        n_qst=48, frames=4)
+    run_and_check(cfg, 0.1, 0, steps=3, seed=2, vision_only=True)

@@ -69,6 +69,37 @@ def test_budget_kernel_exact(lib, L, N, n_sink, n_recent):
             assert np.array_equal(host(so), O.flat_offsets(gb.reshape(-1) + reserve))
 
 
+@pytest.mark.parametrize("L,ns,nv,nq,n_sink,n_recent", [(32, 35, 2880, 64, 0, 0), (28, 16, 8192, 48, 4, 1),
+                                                          (5, 0, 13, 3, 4, 1), (7, 2, 3, 1, 1, 1),
+                                                          (3, 9, 0, 12, 0, 0)])
+def test_budget_kernel_vision_only_exact(lib, L, ns, nv, nq, n_sink, n_recent):
+    """Vision-only eviction (App. B.3): the vision budget is shared out, every layer adds its text."""
+    torch = _torch()
+    rng = np.random.default_rng(L * 100 + nv)
+    cases = list(_mass_cases(rng, L))
+    B = len(cases)
+    masses = np.stack(cases)
+    nt = ns + nq
+    p = bd.make_problem(B, L, 4, 4, 128, ns, nv, nq)
+    o = bd.make_opts(n_sink=n_sink, n_recent=n_recent, vision_only=True)
+    nfv = O.forced_vision_count(ns, nv, nq, n_sink, n_recent)
+    cap = L * (nv - nfv)
+    for total in sorted({v for v in (0, 1, L, cap // 20, cap // 3, cap - 1, cap) if 0 <= v <= cap}):
+        for reserve in (0, 5):
+            tv = torch.from_numpy(masses).cuda()
+            budgets = torch.empty((B, L), dtype=torch.int32, device="cuda")
+            io = torch.empty(B * L + 1, dtype=torch.int64, device="cuda")
+            so = torch.empty(B * L + 1, dtype=torch.int64, device="cuda")
+            bd.tgvkv_budget(p, o, tv, total, reserve, budgets, io, so)
+            torch.cuda.synchronize()
+            gb = host(budgets)
+            for b in range(B):
+                ob = O.vision_only_budgets(masses[b].astype(np.float64), total, nt, nv, nfv)
+                assert np.array_equal(gb[b], ob), (b, total, gb[b], ob)
+            assert np.array_equal(host(io), O.flat_offsets(gb.reshape(-1)))
+            assert np.array_equal(host(so), O.flat_offsets(gb.reshape(-1) + reserve))
+
+
 # ----------------------------------------------------------------------------- selection
 @pytest.mark.parametrize("head_mode", [0, 1])
 @pytest.mark.parametrize("shape", [(3, 40, 5), (0, 30, 4), (8, 144, 16), (35, 576, 40), (2, 0, 9), (16, 1300, 48)])

@@ -126,14 +126,19 @@ def _decode_no_scale(q, Kc, Vc, sm_scale):
     return _orig["decode_attention"](q, Kc, Vc, 1.0)
 
 
-def _vision_only_cap_at_sequence_length(masses, vision_budget, n_text, n_vis, n_floor=0):
+def _vision_only_cap_at_sequence_length(masses, vision_budget, n_text, n_vis, n_forced_vis=0):
     # caps a layer's vision share at N (text + vision) instead of n_vis
-    return int(n_text) + O.layer_budgets(masses, vision_budget, n_vis + n_text, n_floor)
+    return int(n_text) + int(n_forced_vis) + O.layer_budgets(masses, vision_budget, n_vis + n_text, 0)
 
 
-def _vision_only_drops_text(masses, vision_budget, n_text, n_vis, n_floor=0):
+def _vision_only_drops_text(masses, vision_budget, n_text, n_vis, n_forced_vis=0):
     # forgets that every layer also keeps its text tokens
-    return _orig["vision_only_budgets"](masses, vision_budget, 0, n_vis, n_floor)
+    return _orig["vision_only_budgets"](masses, vision_budget, 0, n_vis, n_forced_vis)
+
+
+def _vision_only_forced_inside_budget(masses, vision_budget, n_text, n_vis, n_forced_vis=0):
+    # counts the forced vision tokens inside the vision budget (as a floor) instead of beside it
+    return int(n_text) + O.layer_budgets(masses, vision_budget, n_vis, n_forced_vis)
 
 
 MUTANTS = {
@@ -155,6 +160,7 @@ MUTANTS = {
     "decode_no_scale": ("decode_attention", _decode_no_scale),
     "vision_only_cap_at_sequence_length": ("vision_only_budgets", _vision_only_cap_at_sequence_length),
     "vision_only_drops_text": ("vision_only_budgets", _vision_only_drops_text),
+    "vision_only_forced_inside_budget": ("vision_only_budgets", _vision_only_forced_inside_budget),
 }
 
 
