@@ -44,6 +44,10 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="llavanext")
     ap.add_argument("--rho", type=float, default=None, help="retention ratio (default: the workload's first)")
+    ap.add_argument("--lse-from-prefill", action="store_true",
+                    help="the text rows' normalisers come from the prefill (computed before the timed region "
+                         "by the library's own statistics sweep, standing in for a prefill attention kernel's "
+                         "row log-sum-exp): scoring reads K once")
     ap.add_argument("--vision-only", action="store_true",
                     help="vision-only eviction (every layer keeps all text; rho is the retained share of the "
                          "vision tokens) instead of eviction among all tokens")
@@ -58,7 +62,8 @@ def parse():
                                                             "COPY_WRITE_CSV"),
                     help="turn rocprofv3 --pmc counter files of a bench run and of a --calibrate-copy run into "
                          "profiles/hbm_counters.json (HBM bytes per launch of each kernel)")
-    ap.add_argument("--schedule", default="auto", choices=("auto", "two_step", "phases", "fused", "fused_text"),
+    ap.add_argument("--schedule", default="auto", choices=("auto", "two_step", "phases", "fused", "fused_text",
+                                                           "lse_in"),
                     help="scoring schedule: vision scores after the budgets only for layers that need them "
                          "(auto, two_step), one launch per phase for every layer (phases), or the persistent "
                          "fused kernel (fused, fused_text)")
@@ -264,6 +269,13 @@ def main():
     opts = bd.make_opts(vision_only=args.vision_only)
     buf = bd.EvictionBuffers(p, opts, tot, max(T, 1))
     stream = torch.cuda.current_stream()
+    schedule = args.schedule
+    if args.lse_from_prefill:
+        # what a prefill attention kernel returns for the text rows (their row log-sum-exp),
+        # produced here, outside the timed region, by the library's own statistics sweep
+        buf.score(q_d, k_d, bd.SCORE_STATS | bd.SCORE_TEXT)
+        torch.cuda.synchronize()
+        schedule = "lse_in"
 
     def one_step(events=None):
         names = []
@@ -276,7 +288,7 @@ def main():
                 events.append((name, ev))
 
         mark("start")
-        sched = buf.evict(q_d, k_d, v_d, schedule=args.schedule, marks=mark)
+        sched = buf.evict(q_d, k_d, v_d, schedule=schedule, marks=mark)
         for s_ in range(T):
             mark("decode_gap")  # launch gap before the step: in the step time, not in the kernel's
             buf.decode(s_, dq[s_], dk[s_], dv[s_])
@@ -359,10 +371,13 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{cfg.name}: batch {B}, {L} layers, {H} heads ({Hkv} KV), head_dim {D}, "
                                f"{cfg.n_sys}+{Nv}+{Nq} tokens, retention {rho:g}"
-                               f"{' of vision tokens (all text kept)' if args.vision_only else ''}, {T} decode steps",
+                               f"{' of vision tokens (all text kept)' if args.vision_only else ''}"
+                               f"{', text-row normalisers from the prefill' if args.lse_from_prefill else ''}"
+                               f", {T} decode steps",
                    "batch": B, "layers": L, "heads_q": H, "heads_kv": Hkv, "head_dim": D,
                    "n_sys": cfg.n_sys, "n_vis": Nv, "n_qst": Nq, "retention": rho, "total_budget_per_seq": tot,
                    "vision_only": bool(args.vision_only),
+                   "normalisers_from_prefill": bool(args.lse_from_prefill),
                    "decode_steps": T, "vision_scored_layers": vis_layers, "schedule": sched},
         "evict_ms": round(evict_ms, 4),
         "decode_us_per_step": round(dec_ms * 1e3, 2),

@@ -88,8 +88,13 @@ enum {
     TGVKV_SCORE_TEXT   = 2,  /* text scores s^T, weights w~, per-layer text->vision mass      */
     TGVKV_SCORE_VISION = 4,  /* text-weighted vision scores s^V                               */
     TGVKV_SCORE_ALL    = 7,
-    TGVKV_SCORE_FUSED  = 8   /* with ALL or STATS|TEXT: one persistent launch instead of one
+    TGVKV_SCORE_FUSED  = 8,  /* with ALL or STATS|TEXT: one persistent launch instead of one
                                 per phase (needs budgets_or_null == NULL)                     */
+    TGVKV_SCORE_LSE_IN = 16  /* with exactly TEXT|VISION: lse is an input holding every text
+                                row's normaliser, as a prefill attention kernel returns it;
+                                the statistics sweep is skipped, the vision sweep also gives
+                                each row's vision mass (so tv_mass), and K is read once.
+                                Needs budgets_or_null == NULL (every layer gets s^V).        */
 };
 
 /* Which call a workspace is sized for. */
@@ -109,7 +114,8 @@ enum { TGVKV_CALL_SCORE = 0, TGVKV_CALL_DECODE = 1 };
  *
  * q_text  bf16 [B][L][heads_q][N_t][head_dim]   text-row queries, text order
  * k       bf16 [B][L][heads_kv][N][head_dim]    cached keys (after any positional encoding)
- * lse     f32  [B][L][heads_q][N_t]  out: natural log-sum-exp of each text row's scaled logits
+ * lse     f32  [B][L][heads_q][N_t]  out (in with TGVKV_SCORE_LSE_IN): natural log-sum-exp of each
+ *                                   text row's scaled logits over its visible keys
  * s_txt   f32  [B][L][g][N_t]        out
  * w_txt   f32  [B][L][g][N_t]        out (normalised weights; all 0 if sum(w) == 0)
  * tv_mass f32  [B][L]                out
@@ -117,7 +123,8 @@ enum { TGVKV_CALL_SCORE = 0, TGVKV_CALL_DECODE = 1 };
  * budgets_or_null  int32 [B][L]: if given, the VISION phase skips every layer
  *                  whose budget leaves no room for vision tokens (budget <=
  *                  |forced U T|); s_vis of skipped layers is left untouched.
- * phases  any non-empty OR of STATS, TEXT, VISION, optionally with FUSED.
+ * phases  any non-empty OR of STATS, TEXT, VISION, optionally with FUSED; or
+ *         exactly TEXT|VISION|LSE_IN (see TGVKV_SCORE_LSE_IN).
  *         Phases must run in the order STATS, TEXT, VISION, with the same
  *         workspace and outputs; a later phase reads what the earlier ones left
  *         there.  Pointers of phases not requested may be NULL (lse is needed by

@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libtgvkv.so")
 
 TGVKV_OK, TGVKV_E_INVAL, TGVKV_E_UNSUPPORTED, TGVKV_E_WORKSPACE, TGVKV_E_CAPACITY, TGVKV_E_HIP = 0, -1, -2, -3, -4, -5
 SCORE_STATS, SCORE_TEXT, SCORE_VISION, SCORE_ALL, SCORE_FUSED = 1, 2, 4, 7, 8
+SCORE_LSE_IN = 16  # lse holds the text rows' normalisers from the caller's prefill: K is read once
 CALL_SCORE, CALL_DECODE = 0, 1
 
 EXPORTS = ("tgvkv_score", "tgvkv_budget", "tgvkv_select", "tgvkv_compact", "tgvkv_decode_attn",
@@ -286,9 +287,11 @@ class EvictionBuffers:
         """Score, budget, select and compact.
 
         schedule: 'auto' (= 'two_step'), 'two_step', 'phases' (every scoring phase as its own
-        launch, vision scores for every layer), 'fused' (one persistent scoring launch) or
-        'fused_text' (persistent text pass, then vision scores where needed).  marks(name) is
-        called after each stage (for event timing).
+        launch, vision scores for every layer), 'fused' (one persistent scoring launch),
+        'fused_text' (persistent text pass, then vision scores where needed) or 'lse_in' (self.lse
+        already holds every text row's normaliser from the caller's prefill: text and vision
+        scores and the TV mass in one K pass, then the budgets).  marks(name) is called after
+        each stage (for event timing).
         """
         mark = marks if marks is not None else (lambda name: None)
         sched = self.schedule() if schedule == "auto" else schedule
@@ -311,6 +314,11 @@ class EvictionBuffers:
             mark("budget")
             self.score(q_text, k, SCORE_VISION, budgets=self.budgets, stream=stream)
             mark("score_vision")
+        elif sched == "lse_in":
+            self.score(q_text, k, SCORE_TEXT | SCORE_VISION | SCORE_LSE_IN, stream=stream)
+            mark("score")
+            self.budget(stream)
+            mark("budget")
         elif sched == "phases":
             self.score(q_text, k, SCORE_STATS, stream=stream)
             mark("score_stats")

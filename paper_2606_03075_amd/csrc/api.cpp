@@ -182,10 +182,14 @@ tgvkv_status tgvkv_score(const tgvkv_problem* problem, const tgvkv_opts* opts, i
     tgvkv_status st = make_shape(problem, opts, &s);
     if (st != TGVKV_OK) return st;
     const bool want_fused = (phases & TGVKV_SCORE_FUSED) != 0;
-    phases &= ~TGVKV_SCORE_FUSED;
+    const bool lse_in = (phases & TGVKV_SCORE_LSE_IN) != 0;
+    phases &= ~(TGVKV_SCORE_FUSED | TGVKV_SCORE_LSE_IN);
     if (phases < 1 || phases > TGVKV_SCORE_ALL) return TGVKV_E_INVAL;
-    if (want_fused && (budgets_or_null != nullptr ||
+    if (want_fused && (lse_in || budgets_or_null != nullptr ||
                        (phases != TGVKV_SCORE_ALL && phases != (TGVKV_SCORE_STATS | TGVKV_SCORE_TEXT))))
+        return TGVKV_E_INVAL;
+    // given normalisers: text and vision scores and the TV mass in one pass, for every layer
+    if (lse_in && (phases != (TGVKV_SCORE_TEXT | TGVKV_SCORE_VISION) || budgets_or_null != nullptr))
         return TGVKV_E_INVAL;
     if (s.B == 0) return TGVKV_OK;
     const bool text_rows = s.Nt > 0;
@@ -214,19 +218,28 @@ tgvkv_status tgvkv_score(const tgvkv_problem* problem, const tgvkv_opts* opts, i
     }
 
     hipError_t e = hipSuccess;
+    if (lse_in) {
+        e = tgvkv::launch_score_text(s, q, kk, lse, w.vm, w.colsum, w.vmh, true, stream);
+        if (e == hipSuccess) e = tgvkv::launch_score_fin(s, w.colsum, w.vmh, s_txt, w_txt, tv_mass, false, stream);
+        if (e == hipSuccess)
+            e = tgvkv::launch_score_vision(s, rp, q, kk, lse, w_txt, nullptr, vthr, w.part, w.vm, stream);
+        if (e == hipSuccess) e = tgvkv::launch_score_vis_reduce(s, rp, w.part, nullptr, vthr, s_vis, stream);
+        if (e == hipSuccess) e = tgvkv::launch_score_mass(s, w.vm, w.vmh, tv_mass, stream);
+        return hip_status(e);
+    }
     const bool both = (phases & TGVKV_SCORE_STATS) && (phases & TGVKV_SCORE_TEXT);
     if (both && tgvkv::stats_text_eligible(s, rp)) {
         e = tgvkv::launch_score_stats_text(s, rp, q, kk, lse, w.vm, w.colsum, w.vmh, stream);
-        if (e == hipSuccess) e = tgvkv::launch_score_fin(s, w.colsum, w.vmh, s_txt, w_txt, tv_mass, stream);
+        if (e == hipSuccess) e = tgvkv::launch_score_fin(s, w.colsum, w.vmh, s_txt, w_txt, tv_mass, true, stream);
     } else {
         if (phases & TGVKV_SCORE_STATS) e = tgvkv::launch_score_stats(s, rp, q, kk, lse, w.vm, stream);
         if ((phases & TGVKV_SCORE_TEXT) && e == hipSuccess) {
-            e = tgvkv::launch_score_text(s, q, kk, lse, w.vm, w.colsum, w.vmh, stream);
-            if (e == hipSuccess) e = tgvkv::launch_score_fin(s, w.colsum, w.vmh, s_txt, w_txt, tv_mass, stream);
+            e = tgvkv::launch_score_text(s, q, kk, lse, w.vm, w.colsum, w.vmh, false, stream);
+            if (e == hipSuccess) e = tgvkv::launch_score_fin(s, w.colsum, w.vmh, s_txt, w_txt, tv_mass, true, stream);
         }
     }
     if ((phases & TGVKV_SCORE_VISION) && e == hipSuccess && s.Nv > 0) {
-        e = tgvkv::launch_score_vision(s, rp, q, kk, lse, w_txt, budgets_or_null, vthr, w.part, stream);
+        e = tgvkv::launch_score_vision(s, rp, q, kk, lse, w_txt, budgets_or_null, vthr, w.part, nullptr, stream);
         if (e == hipSuccess) e = tgvkv::launch_score_vis_reduce(s, rp, w.part, budgets_or_null, vthr, s_vis, stream);
     }
     return hip_status(e);

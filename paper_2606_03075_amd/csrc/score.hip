@@ -17,7 +17,11 @@
 //                 text->vision mass (Eq. (5)-(6));
 //   score_vision  sweep 2: question rows x vision keys, p = exp(z - lse),
 //                 column sums weighted by w~ (Eq. (8));
-//   score_vis_reduce  deterministic sum of the per-(KV head, row group) partials.
+//   score_vis_reduce  deterministic sum of the per-(KV head, row group) partials;
+//   score_mass    layer TV mass from per-row vision masses, when the caller gives
+//                 the rows' normalisers (from its prefill) and sweep 1 is skipped:
+//                 the vision sweep then also yields each row's vision mass, so K
+//                 is read once.
 //
 // These kernels serve phase-by-phase calls (and the vision pass restricted to
 // layers whose budget reaches past the text); score_fused.hip runs the same
@@ -132,36 +136,62 @@ __global__ __launch_bounds__(kThreads) void score_text_kernel(Shape s, const uin
                                                               float* __restrict__ lse,
                                                               const float* __restrict__ ws_vm,
                                                               float* __restrict__ ws_colsum,
-                                                              float* __restrict__ ws_vmh) {
+                                                              float* __restrict__ ws_vmh, int lse_given) {
     extern __shared__ float lse2s[];  // [G][N_t] row normalisers, base-2 units
     const int tid = threadIdx.x;
     const int kvh = blockIdx.x % s.Hkv;
     const int bl = blockIdx.x / s.Hkv;
     const size_t head0 = (size_t)bl * s.H + kvh * s.G;
-    for (int x = tid; x < s.G * s.Nq; x += kThreads) {
-        const int g = x / s.Nq, qi = x % s.Nq;
-        lse2s[g * s.Nt + s.Ns + qi] = lse[(head0 + g) * s.Nt + s.Ns + qi] * kLog2e;
-    }
-    if (tid < s.G) {
-        float a = 0.f;
-        for (int qi = 0; qi < s.Nq; ++qi) a += ws_vm[(head0 + tid) * s.Nq + qi];
-        ws_vmh[head0 + tid] = a;
+    if (lse_given) {
+        // every text row's normaliser comes from the caller (a prefill kernel's row log-sum-exp)
+        for (int x = tid; x < s.G * s.Nt; x += kThreads) lse2s[x] = lse[head0 * s.Nt + x] * kLog2e;
+    } else {
+        for (int x = tid; x < s.G * s.Nq; x += kThreads) {
+            const int g = x / s.Nq, qi = x % s.Nq;
+            lse2s[g * s.Nt + s.Ns + qi] = lse[(head0 + g) * s.Nt + s.Ns + qi] * kLog2e;
+        }
+        if (tid < s.G) {
+            float a = 0.f;
+            for (int qi = 0; qi < s.Nq; ++qi) a += ws_vm[(head0 + tid) * s.Nq + qi];
+            ws_vmh[head0 + tid] = a;
+        }
     }
     __syncthreads();
-    text_pass<D>(s, bl, kvh, q_text, k, lse, lse2s, ws_colsum);
+    text_pass<D>(s, bl, kvh, q_text, k, lse, lse2s, ws_colsum, lse_given != 0);
 }
 
 __global__ __launch_bounds__(kThreads) void score_fin_kernel(Shape s, const float* __restrict__ ws_colsum,
                                                              const float* __restrict__ ws_vmh,
                                                              float* __restrict__ s_txt,
                                                              float* __restrict__ w_txt,
-                                                             float* __restrict__ tv_mass) {
+                                                             float* __restrict__ tv_mass, int with_mass) {
     __shared__ float red[kThreads];
     finalize_group(s, (int)(blockIdx.x / s.ngroups), (int)(blockIdx.x % s.ngroups), ws_colsum, ws_vmh, s_txt, w_txt,
-                   tv_mass, red);
+                   tv_mass, red, with_mass != 0);
 }
 
-template <int D, int NSLOT, int KS>
+// Layer TV mass (Eq. (5)-(6)) from per-row vision masses, in the same order as the
+// two-sweep path: per head over question rows, then the mean over heads.
+__global__ __launch_bounds__(kThreads) void score_mass_kernel(Shape s, const float* __restrict__ ws_vm,
+                                                              float* __restrict__ ws_vmh,
+                                                              float* __restrict__ tv_mass) {
+    const int bl = blockIdx.x;
+    for (int h = threadIdx.x; h < s.H; h += kThreads) {
+        float a = 0.f;
+        if (s.Nv > 0)  // with no vision keys the vision sweep does not run and every mass is 0
+            for (int qi = 0; qi < s.Nq; ++qi) a += ws_vm[((size_t)bl * s.H + h) * s.Nq + qi];
+        ws_vmh[(size_t)bl * s.H + h] = a;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float a = 0.f;
+        if (s.Nt > 0)
+            for (int h = 0; h < s.H; ++h) a += ws_vmh[(size_t)bl * s.H + h];
+        tv_mass[bl] = a / (float)s.H;
+    }
+}
+
+template <int D, int NSLOT, int KS, bool MASS>
 __global__ __launch_bounds__(kThreads) void score_vision_kernel(Shape s, int rowgroups,
                                                                 const uint16_t* __restrict__ q_text,
                                                                 const uint16_t* __restrict__ k,
@@ -169,7 +199,8 @@ __global__ __launch_bounds__(kThreads) void score_vision_kernel(Shape s, int row
                                                                 const float* __restrict__ w_txt,
                                                                 const int32_t* __restrict__ budgets,
                                                                 int vis_threshold,
-                                                                float* __restrict__ ws_part) {
+                                                                float* __restrict__ ws_part,
+                                                                float* __restrict__ ws_vm) {
     constexpr int RSETS = 4 / KS;
     __shared__ __attribute__((aligned(16))) char tiles[2][Geo<D>::TILE_BYTES];
     __shared__ float red[2][RSETS][kTile];
@@ -200,7 +231,25 @@ __global__ __launch_bounds__(kThreads) void score_vision_kernel(Shape s, int row
         }
     const uint16_t* kvis = k + (((size_t)bl * s.Hkv + kvh) * (size_t)s.N + s.Ns) * D;
     float* out = ws_part + (((size_t)bl * s.Hkv + kvh) * rowgroups + rg) * (size_t)s.Nv;
-    vision_sweep<D, NSLOT, KS>(s, kvis, 0, s.Nv, qf, lse2, coef, rb0, NB, tiles, red, obuf, out);
+    float rsum[NSLOT][4];
+    vision_sweep<D, NSLOT, KS, MASS>(s, kvis, 0, s.Nv, qf, lse2, coef, rb0, NB, tiles, red, obuf, out, rsum);
+    if (MASS) {
+        // each row's vision mass: the sum of its probabilities over all vision keys
+        const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+        const int rs = wave % RSETS, kp = wave / RSETS;
+        if (kp == 0 && (lane & 15) == 0) {
+#pragma unroll
+            for (int sl = 0; sl < NSLOT; ++sl) {
+                const int rb = rb0 + rs + sl * RSETS;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int qj = (rb % QB) * 16 + (lane >> 4) * 4 + j;
+                    if (rb < NB && qj < s.Nq)
+                        ws_vm[((size_t)bl * s.H + kvh * s.G + rb / QB) * s.Nq + qj] = rsum[sl][j];
+                }
+            }
+        }
+    }
 }
 
 __global__ __launch_bounds__(kThreads) void score_vis_reduce_kernel(Shape s, int rowgroups,
@@ -231,6 +280,17 @@ __global__ __launch_bounds__(kThreads) void score_vis_reduce_kernel(Shape s, int
         else if (rp.nslot == 2) hipLaunchKernelGGL((KERNEL<D, 2, 1>), __VA_ARGS__);               \
         else if (rp.nslot == 4) hipLaunchKernelGGL((KERNEL<D, 4, 1>), __VA_ARGS__);               \
         else hipLaunchKernelGGL((KERNEL<D, 6, 1>), __VA_ARGS__);                                  \
+    } while (0)
+
+#define TGVKV_ROWPLAN_DISPATCH_M(KERNEL, D, M, rp, ...)                                                   \
+    do {                                                                                                  \
+        if (rp.ks == 4) hipLaunchKernelGGL((KERNEL<D, 1, 4, M>), __VA_ARGS__);                            \
+        else if (rp.ks == 2 && rp.nslot == 1) hipLaunchKernelGGL((KERNEL<D, 1, 2, M>), __VA_ARGS__);      \
+        else if (rp.ks == 2) hipLaunchKernelGGL((KERNEL<D, 2, 2, M>), __VA_ARGS__);                       \
+        else if (rp.nslot == 1) hipLaunchKernelGGL((KERNEL<D, 1, 1, M>), __VA_ARGS__);                    \
+        else if (rp.nslot == 2) hipLaunchKernelGGL((KERNEL<D, 2, 1, M>), __VA_ARGS__);                    \
+        else if (rp.nslot == 4) hipLaunchKernelGGL((KERNEL<D, 4, 1, M>), __VA_ARGS__);                    \
+        else hipLaunchKernelGGL((KERNEL<D, 6, 1, M>), __VA_ARGS__);                                       \
     } while (0)
 
 }  // namespace
@@ -285,39 +345,49 @@ hipError_t launch_score_stats_text(const Shape& s, const RowPlan& rp, const uint
 }
 
 hipError_t launch_score_text(const Shape& s, const uint16_t* q_text, const uint16_t* k, float* lse,
-                             const float* ws_vm, float* ws_colsum, float* ws_vmh, hipStream_t st) {
+                             const float* ws_vm, float* ws_colsum, float* ws_vmh, bool lse_given, hipStream_t st) {
     const long long nblk = (long long)s.B * s.L * s.Hkv;
     if (nblk == 0 || s.Nt == 0) return hipSuccess;
     dim3 grid((unsigned)nblk), block(kThreads);
     const size_t lds = sizeof(float) * (size_t)s.G * s.Nt;
     if (s.D == 128)
-        hipLaunchKernelGGL(score_text_kernel<128>, grid, block, lds, st, s, q_text, k, lse, ws_vm, ws_colsum, ws_vmh);
+        hipLaunchKernelGGL(score_text_kernel<128>, grid, block, lds, st, s, q_text, k, lse, ws_vm, ws_colsum, ws_vmh,
+                           (int)lse_given);
     else
-        hipLaunchKernelGGL(score_text_kernel<64>, grid, block, lds, st, s, q_text, k, lse, ws_vm, ws_colsum, ws_vmh);
+        hipLaunchKernelGGL(score_text_kernel<64>, grid, block, lds, st, s, q_text, k, lse, ws_vm, ws_colsum, ws_vmh,
+                           (int)lse_given);
     return hipGetLastError();
 }
 
 hipError_t launch_score_fin(const Shape& s, const float* ws_colsum, const float* ws_vmh, float* s_txt,
-                            float* w_txt, float* tv_mass, hipStream_t st) {
+                            float* w_txt, float* tv_mass, bool with_mass, hipStream_t st) {
     const long long nblk = (long long)s.B * s.L * s.ngroups;
     if (nblk == 0) return hipSuccess;
     hipLaunchKernelGGL(score_fin_kernel, dim3((unsigned)nblk), dim3(kThreads), 0, st, s, ws_colsum, ws_vmh,
-                       s_txt, w_txt, tv_mass);
+                       s_txt, w_txt, tv_mass, (int)with_mass);
     return hipGetLastError();
 }
 
 hipError_t launch_score_vision(const Shape& s, const RowPlan& rp, const uint16_t* q_text, const uint16_t* k,
                                const float* lse, const float* w_txt, const int32_t* budgets,
-                               int32_t vis_threshold, float* ws_part, hipStream_t st) {
+                               int32_t vis_threshold, float* ws_part, float* ws_vm, hipStream_t st) {
     const long long nblk = (long long)s.B * s.L * s.Hkv * rp.rowgroups;
     if (nblk == 0 || s.Nv == 0) return hipSuccess;
     dim3 grid((unsigned)nblk), block(kThreads);
-    if (s.D == 128)
-        TGVKV_ROWPLAN_DISPATCH(score_vision_kernel, 128, rp, grid, block, 0, st, s, rp.rowgroups, q_text, k, lse,
-                               w_txt, budgets, vis_threshold, ws_part);
-    else
-        TGVKV_ROWPLAN_DISPATCH(score_vision_kernel, 64, rp, grid, block, 0, st, s, rp.rowgroups, q_text, k, lse,
-                               w_txt, budgets, vis_threshold, ws_part);
+    if (ws_vm != nullptr) {
+        if (s.D == 128) TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 128, true, rp, grid, block, 0, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm);
+        else TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 64, true, rp, grid, block, 0, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm);
+    } else {
+        if (s.D == 128) TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 128, false, rp, grid, block, 0, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm);
+        else TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 64, false, rp, grid, block, 0, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_score_mass(const Shape& s, const float* ws_vm, float* ws_vmh, float* tv_mass, hipStream_t st) {
+    const long long nblk = (long long)s.B * s.L;
+    if (nblk == 0) return hipSuccess;
+    hipLaunchKernelGGL(score_mass_kernel, dim3((unsigned)nblk), dim3(kThreads), 0, st, s, ws_vm, ws_vmh, tv_mass);
     return hipGetLastError();
 }
 

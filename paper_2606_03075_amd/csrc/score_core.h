@@ -347,18 +347,27 @@ __device__ __forceinline__ void load_row_coefs(const Shape& s, int bl, int kvh, 
 // Vision sweep over vision keys [vbeg, vend) (vbeg a multiple of kTile; kvis
 // points at the first vision key of the unit): out[j] = sum over this
 // workgroup's rows of coef * exp(z - lse), for every key j of the range.
-// obuf: kOutTiles * kTile floats of LDS.
-template <int D, int NSLOT, int KS>
+// obuf: kOutTiles * kTile floats of LDS.  With MASS the sweep also sums each
+// row's probabilities over the range (its vision mass when the range is all
+// vision keys): on return rsum[sl][j] of the key-part-0 waves holds the sum of
+// accumulator row 4*(lane/16) + j of slot sl, in every lane of the 16.
+template <int D, int NSLOT, int KS, bool MASS = false>
 __device__ void vision_sweep(const Shape& s, const uint16_t* kvis, int vbeg, int vend,
                              const bf16x8 (&qf)[NSLOT][Geo<D>::KSTEPS], const float (&lse2)[NSLOT][4],
                              const float (&coef)[NSLOT][4], int rb0, int NB, char (*tiles)[Geo<D>::TILE_BYTES],
-                             float (*red)[4 / KS][kTile], float* obuf, float* out) {
+                             float (*red)[4 / KS][kTile], float* obuf, float* out, float (&rsum)[NSLOT][4]) {
     using GG = Geo<D>;
     constexpr int RSETS = 4 / KS;
     constexpr int KBW = 4 / KS;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int rs = wave % RSETS, kp = wave / RSETS;
     const int ntiles = (vend - vbeg + kTile - 1) / kTile;
+    if (MASS) {
+#pragma unroll
+        for (int sl = 0; sl < NSLOT; ++sl)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) rsum[sl][j] = 0.f;
+    }
     tile_pipeline<D, PipeDepth<NSLOT>::value>(
         kvis, vbeg, vend, tiles,
         [&](const char* buf, int key0, int t) {
@@ -367,6 +376,7 @@ __device__ void vision_sweep(const Shape& s, const uint16_t* kvis, int vbeg, int
                 const int kb = kp + kbi * KS;
                 bf16x8 kf[GG::KSTEPS];
                 load_kfrag<D>(kf, buf, kb, lane);
+                const int kcol = key0 + kb * 16 + (lane & 15);  // this lane's key (accumulator column)
                 float col = 0.f;
 #pragma unroll
                 for (int sl = 0; sl < NSLOT; ++sl) {
@@ -375,7 +385,12 @@ __device__ void vision_sweep(const Shape& s, const uint16_t* kvis, int vbeg, int
 #pragma unroll
                     for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(qf[sl][ks], kf[ks], acc);
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) col += coef[sl][j] * fast_exp2(acc[j] * s.scale2 - lse2[sl][j]);
+                    for (int j = 0; j < 4; ++j) {
+                        const float p = fast_exp2(acc[j] * s.scale2 - lse2[sl][j]);
+                        col += coef[sl][j] * p;
+                        // the last tile repeats the last key past vend (clamped loads): not a key
+                        if (MASS && kcol < vend) rsum[sl][j] += p;
+                    }
                 }
                 col += shfl_xor(col, 16);
                 col += shfl_xor(col, 32);
@@ -403,6 +418,35 @@ __device__ void vision_sweep(const Shape& s, const uint16_t* kvis, int vbeg, int
             }
         });
     __syncthreads();
+    if (MASS) {
+        // a row's keys are spread over the 16 lanes of its quarter, then over the key parts
+#pragma unroll
+        for (int sl = 0; sl < NSLOT; ++sl)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int off = 1; off < 16; off <<= 1) rsum[sl][j] += shfl_xor(rsum[sl][j], off);
+        if (KS > 1) {
+            float* buf = reinterpret_cast<float*>(tiles[0]);  // [wave][NSLOT][16]
+            if (kp > 0 && (lane & 15) == 0) {
+#pragma unroll
+                for (int sl = 0; sl < NSLOT; ++sl)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) buf[(wave * NSLOT + sl) * 16 + (lane >> 4) * 4 + j] = rsum[sl][j];
+            }
+            __syncthreads();
+            if (kp == 0) {
+                for (int p2 = 1; p2 < KS; ++p2) {
+                    const int w2 = p2 * RSETS + rs;
+#pragma unroll
+                    for (int sl = 0; sl < NSLOT; ++sl)
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) rsum[sl][j] += buf[(w2 * NSLOT + sl) * 16 + (lane >> 4) * 4 + j];
+                }
+            }
+            __syncthreads();
+        }
+    }
 }
 
 // Text x text pass of one unit.  lse2s [G][N_t] (LDS, base-2 units) must hold the
@@ -412,10 +456,12 @@ __device__ void vision_sweep(const Shape& s, const uint16_t* kvis, int vbeg, int
 // The work is small and latency-bound: each wave walks its items with the next
 // block's 16-byte fragments fetched while the current block is used (two
 // register sets, loads clamped into the unit so that every one is issued).
+// With lse_given every text row's normaliser is already in lse2s (taken from the
+// caller), the system rows are not recomputed and lse is not written.
 template <int D>
 __device__ void text_pass(const Shape& s, int bl, int kvh, const uint16_t* __restrict__ q_text,
                           const uint16_t* __restrict__ k, float* __restrict__ lse, float* lse2s,
-                          float* __restrict__ ws_colsum) {
+                          float* __restrict__ ws_colsum, bool lse_given = false) {
     using GG = Geo<D>;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const size_t head0 = (size_t)bl * s.H + kvh * s.G;
@@ -427,7 +473,7 @@ __device__ void text_pass(const Shape& s, int bl, int kvh, const uint16_t* __res
     };
 
     // system rows x system keys: row normalisers (C[key][row]: a lane owns row i)
-    const int SB = (s.Ns + 15) >> 4;
+    const int SB = lse_given ? 0 : (s.Ns + 15) >> 4;
     for (int item = wave; item < s.G * SB; item += 4) {
         const int g = item / SB, rb = item % SB;
         const int i = rb * 16 + (lane & 15);
@@ -516,7 +562,7 @@ __device__ void text_pass(const Shape& s, int bl, int kvh, const uint16_t* __res
 // Head means of one (sequence, layer, group): s^T (Eq. (9)), w and w~ (Eq. (7)),
 // and for group 0 the layer's text->vision mass (Eq. (5)-(6)).  red: 256 floats of LDS.
 __device__ inline void finalize_group(const Shape& s, int bl, int gi, const float* ws_colsum, const float* ws_vmh,
-                                      float* s_txt, float* w_txt, float* tv_mass, float* red) {
+                                      float* s_txt, float* w_txt, float* tv_mass, float* red, bool with_mass = true) {
     const int tid = threadIdx.x;
     const int h0 = s.head_mode == 0 ? 0 : gi * s.G;
     const int hn = s.head_mode == 0 ? s.H : s.G;
@@ -542,7 +588,7 @@ __device__ inline void finalize_group(const Shape& s, int bl, int gi, const floa
         const float w = s_txt[obase + j] / (float)(s.Nt - j);
         w_txt[obase + j] = W > 0.f ? w / W : 0.f;
     }
-    if (gi == 0 && tid == 0) {
+    if (with_mass && gi == 0 && tid == 0) {
         float a = 0.f;
         if (s.Nt > 0)
             for (int h = 0; h < s.H; ++h) a += ws_vmh[(size_t)bl * s.H + h];

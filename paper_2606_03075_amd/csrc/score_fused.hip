@@ -216,7 +216,9 @@ __global__ __launch_bounds__(kThreads) void score_fused_kernel(
                     const uint16_t* kvis = k + ((size_t)u * s.N + s.Ns) * D;
                     const int vb = sp * fp.cv, ve = min(s.Nv, vb + fp.cv);
                     float* out = s.head_mode == 0 ? ws_part + (size_t)u * s.Nv : s_vis + (size_t)u * s.Nv;
-                    vision_sweep<D, NSLOT, KS>(s, kvis, vb, ve, qf, lse2, coef, 0, NB, tiles, red, obuf, out);
+                    float rsum_unused[NSLOT][4];
+                    vision_sweep<D, NSLOT, KS>(s, kvis, vb, ve, qf, lse2, coef, 0, NB, tiles, red, obuf, out,
+                                               rsum_unused);
                 }
                 if (s.head_mode == 0) {
                     if (tid == 0) {

@@ -55,13 +55,14 @@ bool stats_text_eligible(const Shape& s, const RowPlan& rp);
 hipError_t launch_score_stats_text(const Shape& s, const RowPlan& rp, const uint16_t* q_text, const uint16_t* k,
                                    float* lse, float* ws_vm, float* ws_colsum, float* ws_vmh, hipStream_t st);
 hipError_t launch_score_text(const Shape& s, const uint16_t* q_text, const uint16_t* k, float* lse,
-                             const float* ws_vm, float* ws_colsum, float* ws_vmh, hipStream_t st);
+                             const float* ws_vm, float* ws_colsum, float* ws_vmh, bool lse_given, hipStream_t st);
 hipError_t launch_score_fin(const Shape& s, const float* ws_colsum, const float* ws_vmh, float* s_txt,
-                            float* w_txt, float* tv_mass, hipStream_t st);
+                            float* w_txt, float* tv_mass, bool with_mass, hipStream_t st);
 hipError_t launch_score_vision(const Shape& s, const RowPlan& rp, const uint16_t* q_text,
                                const uint16_t* k, const float* lse, const float* w_txt,
-                               const int32_t* budgets, int32_t vis_threshold, float* ws_part,
+                               const int32_t* budgets, int32_t vis_threshold, float* ws_part, float* ws_vm,
                                hipStream_t st);
+hipError_t launch_score_mass(const Shape& s, const float* ws_vm, float* ws_vmh, float* tv_mass, hipStream_t st);
 hipError_t launch_score_vis_reduce(const Shape& s, const RowPlan& rp, const float* ws_part,
                                    const int32_t* budgets, int32_t vis_threshold, float* s_vis,
                                    hipStream_t st);

@@ -92,7 +92,13 @@ def test_validation_before_any_launch(lib):
     assert lib.tgvkv_score(ok, None, 8 | 4, fake, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
     assert lib.tgvkv_score(ok, None, 8 | 1, fake, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
     assert lib.tgvkv_score(ok, None, 8 | 7, fake, fake, fake, fake, fake, fake, fake, fake, fake, big, s) == -1
+    # normalisers from the caller: only with exactly TEXT|VISION, no budgets, not fused
     assert lib.tgvkv_score(ok, None, 16, fake, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
+    assert lib.tgvkv_score(ok, None, 16 | 7, fake, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
+    assert lib.tgvkv_score(ok, None, 16 | 2, fake, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
+    assert lib.tgvkv_score(ok, None, 16 | 6, fake, fake, fake, fake, fake, fake, fake, fake, fake, big, s) == -1
+    assert lib.tgvkv_score(ok, None, 16 | 8 | 6, fake, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
+    assert lib.tgvkv_score(ok, None, 32, fake, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
     assert lib.tgvkv_score(ok, None, 7, None, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
     assert lib.tgvkv_score(ok, None, 7, odd, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
     assert lib.tgvkv_score(ok, None, 2, fake, fake, fake, None, fake, fake, fake, None, fake, big, s) == -1

@@ -33,6 +33,19 @@ def run_and_check(cfg, rho, head_mode=0, forced=(0, 0), steps=2, seed=0, skip_te
     assert kept == tot + (L * (cfg.n_text + nfv) if vision_only else 0)
     buf = bd.EvictionBuffers(p, o, tot, max(steps, 1))
     q_d, k_d, v_d = dev_bf16(t["q_text"]), dev_bf16(t["k"]), dev_bf16(t["v"])
+    check_seqs = range(B) if check_seqs is None else check_seqs
+    orc = {}
+
+    def oracle_seq(b):
+        if b not in orc:
+            orc[b] = O.evict_sequence(bf16_bits_to_f32(t["q_text"][b]), bf16_bits_to_f32(t["k"][b]), cfg.n_sys,
+                                      cfg.n_vis, cfg.n_qst, tot, None, head_mode, *forced, vision_only=vision_only)
+        return orc[b]
+
+    if schedule == "lse_in":
+        # the rows' normalisers a prefill kernel would return: here the fp64 oracle's, rounded to fp32
+        lse = np.stack([np.stack([sc["lse"] for sc in oracle_seq(b)[0]]) for b in range(B)]).astype(np.float32)
+        buf.lse.copy_(torch.from_numpy(lse))
     sched = buf.evict(q_d, k_d, v_d, schedule=schedule if skip_text_only else "phases")
     log(f"  schedule {sched}")
     outs = []
@@ -52,13 +65,9 @@ def run_and_check(cfg, rho, head_mode=0, forced=(0, 0), steps=2, seed=0, skip_te
     tau = 1.0 / np.sqrt(cfg.head_dim)
     D, Hkv = cfg.head_dim, cfg.heads_kv
     assert np.all(budgets.sum(axis=1) == kept)
-    check_seqs = range(B) if check_seqs is None else check_seqs
     decode_seqs = set(range(B) if decode_seqs is None else decode_seqs)
     for b in check_seqs:
-        qf = bf16_bits_to_f32(t["q_text"][b])
-        kf = bf16_bits_to_f32(t["k"][b])
-        scores, ob, oidx = O.evict_sequence(qf, kf, cfg.n_sys, cfg.n_vis, cfg.n_qst, tot, None, head_mode,
-                                            *forced, vision_only=vision_only)
+        scores, ob, oidx = oracle_seq(b)
         assert budgets[b].sum() == kept
         masses = [s["tv_mass"] for s in scores]
         if vision_only:
@@ -75,7 +84,7 @@ def run_and_check(cfg, rho, head_mode=0, forced=(0, 0), steps=2, seed=0, skip_te
             assert_close_rel("s_txt", host(buf.s_txt[b, l]), sc["s_txt"])
             assert_close_rel("w_txt", host(buf.w_txt[b, l]), sc["w_txt"])
             needs_vis = budgets[b, l] > buf.forced_or_text()
-            if needs_vis or sched in ("fused", "phases"):
+            if needs_vis or sched in ("fused", "phases", "lse_in"):
                 assert_close_rel("s_vis", host(buf.s_vis[b, l]), sc["s_vis"])
             if budgets[b, l] != ob[l]:
                 continue  # a rounding-cut trade: this layer's set is legitimately different
@@ -175,3 +184,30 @@ def test_vision_only_gqa_video(lib):
     cfg = custom_config(name="vid", batch=2, layers=3, heads_q=28, heads_kv=4, head_dim=128, n_sys=16, n_vis=512,
                         n_qst=48, frames=4)
     run_and_check(cfg, 0.1, 0, steps=3, seed=2, vision_only=True)
+
+
+# ----------------------------------------------------------------------------- normalisers from the prefill
+@pytest.mark.parametrize("head_mode", [0, 1])
+@pytest.mark.parametrize("forced", [(0, 0), (4, 1)])
+def test_lse_in_small(lib, head_mode, forced):
+    cfg = custom_config(batch=2, layers=4, heads_q=8, heads_kv=4, head_dim=128, n_sys=6, n_vis=230, n_qst=21)
+    for rho in (0.05, 0.3, 1.0):
+        run_and_check(cfg, rho, head_mode, forced, steps=2, seed=7, schedule="lse_in")
+    run_and_check(cfg, 0.1, head_mode, forced, steps=2, seed=8, schedule="lse_in", vision_only=True)
+
+
+def test_lse_in_shapes(lib):
+    # GQA video, d64 tiny, no question text, no vision, no system text
+    run_and_check(custom_config(name="vid", batch=2, layers=3, heads_q=28, heads_kv=4, head_dim=128, n_sys=16,
+                                n_vis=512, n_qst=48, frames=4), 0.1, steps=2, seed=2, schedule="lse_in")
+    run_and_check(CONFIGS["tiny"], 0.5, steps=1, seed=0, schedule="lse_in")
+    run_and_check(custom_config(name="noq", batch=1, layers=3, heads_q=4, heads_kv=2, n_sys=9, n_vis=70, n_qst=0),
+                  0.3, steps=2, schedule="lse_in")
+    run_and_check(custom_config(name="nov", batch=1, layers=3, heads_q=4, heads_kv=2, n_sys=9, n_vis=0, n_qst=12),
+                  0.5, steps=2, schedule="lse_in")
+    run_and_check(custom_config(name="nos", batch=1, layers=3, heads_q=4, heads_kv=4, head_dim=64, n_sys=0,
+                                n_vis=90, n_qst=17), 0.25, steps=2, schedule="lse_in")
+
+
+def test_lse_in_llava15(lib):
+    run_and_check(CONFIGS["llava15"], 0.1, steps=4, seed=0, schedule="lse_in")
