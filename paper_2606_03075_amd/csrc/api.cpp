@@ -191,6 +191,7 @@ tgvkv_status tgvkv_score(const tgvkv_problem* problem, const tgvkv_opts* opts, i
     // given normalisers: text and vision scores and the TV mass in one pass, for every layer
     if (lse_in && (phases != (TGVKV_SCORE_TEXT | TGVKV_SCORE_VISION) || budgets_or_null != nullptr))
         return TGVKV_E_INVAL;
+    if (lse_in && (int64_t)s.B * s.L * s.H * ((s.Nt + 15) / 16) > kMaxBlocks) return TGVKV_E_UNSUPPORTED;
     if (s.B == 0) return TGVKV_OK;
     const bool text_rows = s.Nt > 0;
     if (q_text == nullptr && text_rows) return TGVKV_E_INVAL;

@@ -119,8 +119,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(Shape s, uint16_t* __r
                 float d = 0.f;
 #pragma unroll
                 for (int e = 0; e < 8; ++e) d += qv[h][e] * kf[e];
-#pragma unroll
-                for (int o = 1; o < LPR; o <<= 1) d += shfl_xor(d, o);
+                d = group_sum<LPR>(d);
                 z[u] = ok[u] ? d : kNegInf;
                 mx = fmaxf(mx, z[u]);
             }

@@ -160,6 +160,24 @@ __global__ __launch_bounds__(kThreads) void score_text_kernel(Shape s, const uin
     text_pass<D>(s, bl, kvh, q_text, k, lse, lse2s, ws_colsum, lse_given != 0);
 }
 
+// One wave per (unit, query head, 16-key block) of the text->text column sums, when
+// every text row's normaliser is given.
+template <int D>
+__global__ __launch_bounds__(64) void score_text_cols_kernel(Shape s, const uint16_t* __restrict__ q_text,
+                                                             const uint16_t* __restrict__ k,
+                                                             const float* __restrict__ lse,
+                                                             float* __restrict__ ws_colsum) {
+    const int TB = (s.Nt + 15) >> 4;
+    long long item = blockIdx.x;
+    const int kb = (int)(item % TB);
+    item /= TB;
+    const int g = (int)(item % s.G);
+    item /= s.G;
+    const int kvh = (int)(item % s.Hkv);
+    const int bl = (int)(item / s.Hkv);
+    text_cols_item<D>(s, bl, kvh, g, kb, q_text, k, lse, ws_colsum);
+}
+
 __global__ __launch_bounds__(kThreads) void score_fin_kernel(Shape s, const float* __restrict__ ws_colsum,
                                                              const float* __restrict__ ws_vmh,
                                                              float* __restrict__ s_txt,
@@ -348,6 +366,16 @@ hipError_t launch_score_text(const Shape& s, const uint16_t* q_text, const uint1
                              const float* ws_vm, float* ws_colsum, float* ws_vmh, bool lse_given, hipStream_t st) {
     const long long nblk = (long long)s.B * s.L * s.Hkv;
     if (nblk == 0 || s.Nt == 0) return hipSuccess;
+    if (lse_given) {
+        const long long items = nblk * s.G * ((s.Nt + 15) / 16);
+        if (s.D == 128)
+            hipLaunchKernelGGL(score_text_cols_kernel<128>, dim3((unsigned)items), dim3(64), 0, st, s, q_text, k, lse,
+                               ws_colsum);
+        else
+            hipLaunchKernelGGL(score_text_cols_kernel<64>, dim3((unsigned)items), dim3(64), 0, st, s, q_text, k, lse,
+                               ws_colsum);
+        return hipGetLastError();
+    }
     dim3 grid((unsigned)nblk), block(kThreads);
     const size_t lds = sizeof(float) * (size_t)s.G * s.Nt;
     if (s.D == 128)

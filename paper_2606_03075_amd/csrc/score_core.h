@@ -392,8 +392,7 @@ __device__ void vision_sweep(const Shape& s, const uint16_t* kvis, int vbeg, int
                         if (MASS && kcol < vend) rsum[sl][j] += p;
                     }
                 }
-                col += shfl_xor(col, 16);
-                col += shfl_xor(col, 32);
+                col = sum_xor32(sum_xor16(col));
                 if (lane < 16) red[t & 1][rs][kb * 16 + lane] = col;
             }
         },
@@ -424,8 +423,7 @@ __device__ void vision_sweep(const Shape& s, const uint16_t* kvis, int vbeg, int
         for (int sl = 0; sl < NSLOT; ++sl)
 #pragma unroll
             for (int j = 0; j < 4; ++j)
-#pragma unroll
-                for (int off = 1; off < 16; off <<= 1) rsum[sl][j] += shfl_xor(rsum[sl][j], off);
+                rsum[sl][j] = group_sum<16>(rsum[sl][j]);
         if (KS > 1) {
             float* buf = reinterpret_cast<float*>(tiles[0]);  // [wave][NSLOT][16]
             if (kp > 0 && (lane & 15) == 0) {
@@ -552,11 +550,68 @@ __device__ void text_pass(const Shape& s, int bl, int kvh, const uint16_t* __res
             load_frag(qa, qrow(rb + 2));
             step(qb, rb + 1);
         }
-        col += shfl_xor(col, 16);
-        col += shfl_xor(col, 32);
+        col = sum_xor32(sum_xor16(col));
         if (lane < 16 && j < s.Nt) ws_colsum[(head0 + g) * s.Nt + j] = col;
     }
     __syncthreads();
+}
+
+// Column sums of the text->text probabilities for one 16-key block kb of query
+// head g of a unit, by one wave, with every text row's normaliser given (natural
+// log, lse [.., N_t] of the head): the items of a unit are independent, so each
+// is its own wave and their latencies overlap.  C[row][key]: a lane owns key
+// j = 16*kb + lane%16; the row fragments and the rows' normalisers of the next
+// 16-row block are fetched while the current block is used.
+template <int D>
+__device__ void text_cols_item(const Shape& s, int bl, int kvh, int g, int kb, const uint16_t* __restrict__ q_text,
+                               const uint16_t* __restrict__ k, const float* __restrict__ lse,
+                               float* __restrict__ ws_colsum) {
+    using GG = Geo<D>;
+    const int lane = threadIdx.x & 63;
+    const size_t head = (size_t)bl * s.H + kvh * s.G + g;
+    const uint16_t* kbase = k + ((size_t)bl * s.Hkv + kvh) * (size_t)s.N * D;
+    const int koff = (lane >> 4) * 8;
+    const int TB = (s.Nt + 15) >> 4;
+    const int j = kb * 16 + (lane & 15);
+    const int jc = min(j, s.Nt - 1);
+    const int pos = jc < s.Ns ? jc : jc + s.Nv;
+    auto load_frag = [&](bf16x8 (&f)[GG::KSTEPS], const uint16_t* row) {
+#pragma unroll
+        for (int ks = 0; ks < GG::KSTEPS; ++ks) f[ks] = as_bf16x8(load16(row + koff + ks * 32));
+    };
+    auto qrow = [&](int rb) { return q_text + (head * s.Nt + min(rb * 16 + (lane & 15), s.Nt - 1)) * D; };
+    // the normalisers of this lane's accumulator rows 16*rb + 4*(lane/16) + jj (clamped into the head)
+    auto load_lse = [&](float (&l2)[4], int rb) {
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) l2[jj] = lse[head * s.Nt + min(rb * 16 + (lane >> 4) * 4 + jj, s.Nt - 1)];
+    };
+    bf16x8 kf[GG::KSTEPS], qa[GG::KSTEPS], qb[GG::KSTEPS];
+    float la[4], lb[4];
+    load_frag(kf, kbase + (size_t)pos * D);
+    load_frag(qa, qrow(kb));
+    load_lse(la, kb);
+    float col = 0.f;
+    auto step = [&](const bf16x8 (&qf)[GG::KSTEPS], const float (&l2)[4], int rb) {
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(qf[ks], kf[ks], acc);
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+            const int ii = rb * 16 + (lane >> 4) * 4 + jj;
+            if (ii < s.Nt && j <= ii) col += fast_exp2(acc[jj] * s.scale2 - l2[jj] * kLog2e);
+        }
+    };
+    // row blocks kb..TB-1; a block past the last is masked out by ii < N_t
+    for (int rb = kb; rb < TB; rb += 2) {
+        load_frag(qb, qrow(rb + 1));
+        load_lse(lb, rb + 1);
+        step(qa, la, rb);
+        load_frag(qa, qrow(rb + 2));
+        load_lse(la, rb + 2);
+        step(qb, lb, rb + 1);
+    }
+    col = sum_xor32(sum_xor16(col));
+    if (lane < 16 && j < s.Nt) ws_colsum[head * s.Nt + j] = col;
 }
 
 // Head means of one (sequence, layer, group): s^T (Eq. (9)), w and w~ (Eq. (7)),

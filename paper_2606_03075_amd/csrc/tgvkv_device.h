@@ -71,6 +71,39 @@ __device__ __forceinline__ T shfl_xor(T v, int mask) {
     return __shfl_xor(v, mask, 64);
 }
 
+// Cross-lane sums on the VALU (no LDS crossbar traffic, unlike ds_bpermute).
+// DPP row controls: quad_perm [1,0,3,2] (lane ^ 1), quad_perm [2,3,0,1] (lane ^ 2),
+// row_half_mirror (7 - i within 8 lanes), row_mirror (15 - i within 16 lanes).
+template <int CTRL>
+__device__ __forceinline__ float dpp_read(float x) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, true));
+}
+
+// Sum over each aligned group of W lanes (W = 8 or 16), left in every lane of the group.
+// Each step adds the value of a partner lane that holds the same partial set, so the
+// two lanes of a pair compute the same sum.
+template <int W>
+__device__ __forceinline__ float group_sum(float x) {
+    static_assert(W == 8 || W == 16, "group width");
+    x += dpp_read<0xB1>(x);   // lane ^ 1
+    x += dpp_read<0x4E>(x);   // lane ^ 2
+    x += dpp_read<0x141>(x);  // the other quad of the 8
+    if (W == 16) x += dpp_read<0x140>(x);  // the other 8 of the 16
+    return x;
+}
+
+// x + x of lane (l ^ 16), and x + x of lane (l ^ 32): v_permlane16_swap / v_permlane32_swap
+// exchange rows between two registers; passing x twice yields both partners, in the same
+// order in both lanes of a pair.
+__device__ __forceinline__ float sum_xor16(float x) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float sum_xor32(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // Combine two online-softmax partials (max m in log2 units, sum l, extra sum v
 // that shares the normaliser).
 __device__ __forceinline__ void merge_stats(float& m, float& l, float& v, float m2, float l2, float v2) {
