@@ -16,12 +16,59 @@ from workloads.configs import CONFIGS, custom_config
 pytestmark = pytest.mark.gpu
 
 
+class _Tiled:
+    """Host view of a batch whose sequence b holds generated sequence src[b] (index axis `axis`)."""
+
+    def __init__(self, arr, src, axis):
+        self.arr, self.src, self.axis = arr, src, axis
+
+    def __getitem__(self, key):
+        key = list(key) if isinstance(key, tuple) else [key]
+        key[self.axis] = self.src[key[self.axis]]
+        return self.arr[tuple(key)]
+
+
+def _inputs(cfg, seed, steps, gen_seqs):
+    """Host inputs (indexable by sequence) and their device copies for the whole batch.
+
+    With gen_seqs, only those sequences are generated; sequence b of the batch then
+    holds generated sequence gen_seqs[b % len(gen_seqs)] (each listed sequence holds its own
+    data), so the device runs the full-size batch while the oracle checks real sequences.
+    """
+    if gen_seqs is None:
+        t = make_prefill_tensors(cfg, seed=seed)
+        dec = make_decode_tensors(cfg, seed=seed, steps=steps)
+        dev_t = {n: dev_bf16(a) for n, a in t.items()}
+        dev_dec = [{n: dev_bf16(dec[n][st]) for n in dec} for st in range(steps)]
+        return t, dec, dev_t, dev_dec
+    import torch
+    gen_seqs = list(gen_seqs)
+    src = [b % len(gen_seqs) for b in range(cfg.batch)]
+    assert all(src[b] == i for i, b in enumerate(gen_seqs)), "each generated sequence must map to itself"
+    tg = make_prefill_tensors(cfg, seed=seed, seqs=gen_seqs)
+    dg = make_decode_tensors(cfg, seed=seed, steps=steps, seqs=gen_seqs)
+    dev_t = {}
+    for n, a in tg.items():
+        part = dev_bf16(a)
+        dev_t[n] = torch.stack([part[src[b]] for b in range(cfg.batch)])
+        del part
+    dev_dec = []
+    for st in range(steps):
+        d = {}
+        for n, a in dg.items():
+            part = dev_bf16(a[st])
+            d[n] = torch.stack([part[src[b]] for b in range(cfg.batch)])
+        dev_dec.append(d)
+    t = {n: _Tiled(a, src, 0) for n, a in tg.items()}
+    dec = {n: _Tiled(a, src, 1) for n, a in dg.items()}
+    return t, dec, dev_t, dev_dec
+
+
 def run_and_check(cfg, rho, head_mode=0, forced=(0, 0), steps=2, seed=0, skip_text_only=True, check_seqs=None,
-                  decode_seqs=None, schedule="auto", vision_only=False):
+                  decode_seqs=None, schedule="auto", vision_only=False, gen_seqs=None):
     import torch
     log(f"e2e {cfg.name} rho={rho} mode={head_mode} forced={forced} steps={steps} vision_only={vision_only}")
-    t = make_prefill_tensors(cfg, seed=seed)
-    dec = make_decode_tensors(cfg, seed=seed, steps=steps)
+    t, dec, dev_t, dev_dec = _inputs(cfg, seed, steps, gen_seqs)
     B, L, N = cfg.batch, cfg.layers, cfg.n_tokens
     p = bd.problem_from(cfg)
     o = bd.make_opts(head_mode=head_mode, n_sink=forced[0], n_recent=forced[1], vision_only=vision_only)
@@ -32,7 +79,7 @@ def run_and_check(cfg, rho, head_mode=0, forced=(0, 0), steps=2, seed=0, skip_te
     kept = bd.kept_per_sequence(p, o, tot)
     assert kept == tot + (L * (cfg.n_text + nfv) if vision_only else 0)
     buf = bd.EvictionBuffers(p, o, tot, max(steps, 1))
-    q_d, k_d, v_d = dev_bf16(t["q_text"]), dev_bf16(t["k"]), dev_bf16(t["v"])
+    q_d, k_d, v_d = dev_t["q_text"], dev_t["k"], dev_t["v"]
     check_seqs = range(B) if check_seqs is None else check_seqs
     orc = {}
 
@@ -44,13 +91,14 @@ def run_and_check(cfg, rho, head_mode=0, forced=(0, 0), steps=2, seed=0, skip_te
 
     if schedule == "lse_in":
         # the rows' normalisers a prefill kernel would return: here the fp64 oracle's, rounded to fp32
+        assert gen_seqs is None
         lse = np.stack([np.stack([sc["lse"] for sc in oracle_seq(b)[0]]) for b in range(B)]).astype(np.float32)
         buf.lse.copy_(torch.from_numpy(lse))
     sched = buf.evict(q_d, k_d, v_d, schedule=schedule if skip_text_only else "phases")
     log(f"  schedule {sched}")
     outs = []
     for st in range(steps):
-        buf.decode(st, dev_bf16(dec["q"][st]), dev_bf16(dec["k_new"][st]), dev_bf16(dec["v_new"][st]))
+        buf.decode(st, dev_dec[st]["q"], dev_dec[st]["k_new"], dev_dec[st]["v_new"])
         outs.append(host(buf.out).copy())
     torch.cuda.synchronize()
 

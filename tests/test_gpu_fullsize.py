@@ -50,3 +50,28 @@ def test_qwen2vl_video_full(lib, rho):
     cfg = CONFIGS["qwen2vl_video"]
     buf = run_and_check(cfg, rho, steps=cfg.decode_steps, seed=0, check_seqs=[0, 7], decode_seqs=[0])
     _properties(buf, cfg)
+
+
+def test_stress13b_full(lib):
+    """batch 16 x 40 layers x 40 heads, 35 + 2880 + 256 tokens, 5 % retention, 256 decode steps.
+
+    Sequences 0 and 15 are generated and checked against the oracle (every layer); the other
+    sequences of the batch repeat them (even ones sequence 0, odd ones sequence 15), so the
+    device runs the full-size batch, and sequences holding the same data must agree exactly.
+    """
+    cfg = CONFIGS["stress13b"]
+    buf = run_and_check(cfg, cfg.rhos[0], steps=cfg.decode_steps, seed=0, check_seqs=[0, 15], decode_seqs=[0],
+                        gen_seqs=[0, 15])
+    _properties(buf, cfg)
+    budgets = buf.budgets.cpu().numpy()
+    io = buf.idx_offsets.cpu().numpy()
+    idx = buf.idx.cpu().numpy()
+    L = cfg.layers
+    for b in range(2, cfg.batch):
+        ref = 0 if b % 2 == 0 else 15
+        assert np.array_equal(budgets[b], budgets[ref]), b
+        for l in range(L):
+            got = idx[io[b * L + l]: io[b * L + l + 1]]
+            want = idx[io[ref * L + l]: io[ref * L + l + 1]]
+            assert np.array_equal(got, want), (b, l)
+    log(f"  stress13b budgets seq0: {buf.budgets[0].tolist()}")

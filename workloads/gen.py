@@ -23,7 +23,7 @@ from __future__ import annotations
 
 import concurrent.futures as _fut
 import os
-from typing import Dict, Optional
+from typing import Dict, Optional, Sequence
 
 import numpy as np
 
@@ -120,12 +120,16 @@ def _threads(threads: Optional[int]) -> int:
 
 
 def make_prefill_tensors(cfg: WorkloadConfig, seed: int = 0, threads: Optional[int] = None,
-                         names=("q_text", "k", "v")) -> Dict[str, np.ndarray]:
+                         names=("q_text", "k", "v"), seqs: Optional[Sequence[int]] = None) -> Dict[str, np.ndarray]:
     """Whole-batch prefill inputs as bf16 bit patterns (uint16), in the library's layouts.
 
-    q_text [B][L][H][N_t][d], k and v [B][L][H_kv][N][d].
+    q_text [B][L][H][N_t][d], k and v [B][L][H_kv][N][d].  With seqs, only those
+    sequences of the batch are generated (leading dimension len(seqs), in that
+    order); each is identical to its slice of the whole batch.
     """
-    B, L = cfg.batch, cfg.layers
+    L = cfg.layers
+    bs = list(range(cfg.batch)) if seqs is None else [int(b) for b in seqs]
+    B = len(bs)
     shapes = {
         "q_text": (B, L, cfg.heads_q, cfg.n_text, cfg.head_dim),
         "k": (B, L, cfg.heads_kv, cfg.n_tokens, cfg.head_dim),
@@ -135,31 +139,36 @@ def make_prefill_tensors(cfg: WorkloadConfig, seed: int = 0, threads: Optional[i
     out = {n: np.empty(shapes[n], dtype=np.uint16) for n in names}
 
     def work(item):
-        n, b, l = item
-        out[n][b, l] = f32_to_bf16_bits(fns[n](cfg, seed, b, l))
+        n, i, l = item
+        out[n][i, l] = f32_to_bf16_bits(fns[n](cfg, seed, bs[i], l))
 
-    items = [(n, b, l) for n in names for b in range(B) for l in range(L)]
+    items = [(n, i, l) for n in names for i in range(B) for l in range(L)]
     with _fut.ThreadPoolExecutor(_threads(threads)) as ex:
         list(ex.map(work, items))
     return out
 
 
 def make_decode_tensors(cfg: WorkloadConfig, seed: int = 0, steps: Optional[int] = None,
-                        threads: Optional[int] = None) -> Dict[str, np.ndarray]:
-    """Decode inputs as bf16 bits: q [T][B][L][H][d], k_new and v_new [T][B][L][H_kv][d]."""
+                        threads: Optional[int] = None, seqs: Optional[Sequence[int]] = None) -> Dict[str, np.ndarray]:
+    """Decode inputs as bf16 bits: q [T][B][L][H][d], k_new and v_new [T][B][L][H_kv][d].
+
+    With seqs, only those sequences (second dimension len(seqs), in that order).
+    """
     T = cfg.decode_steps if steps is None else steps
-    B, L = cfg.batch, cfg.layers
+    L = cfg.layers
+    bs = list(range(cfg.batch)) if seqs is None else [int(b) for b in seqs]
+    B = len(bs)
     q = np.empty((T, B, L, cfg.heads_q, cfg.head_dim), np.uint16)
     kn = np.empty((T, B, L, cfg.heads_kv, cfg.head_dim), np.uint16)
     vn = np.empty_like(kn)
 
     def work(item):
-        b, l = item
-        a, c, e = gen_decode_slice(cfg, seed, b, l, T)
-        q[:, b, l] = f32_to_bf16_bits(a)
-        kn[:, b, l] = f32_to_bf16_bits(c)
-        vn[:, b, l] = f32_to_bf16_bits(e)
+        i, l = item
+        a, c, e = gen_decode_slice(cfg, seed, bs[i], l, T)
+        q[:, i, l] = f32_to_bf16_bits(a)
+        kn[:, i, l] = f32_to_bf16_bits(c)
+        vn[:, i, l] = f32_to_bf16_bits(e)
 
     with _fut.ThreadPoolExecutor(_threads(threads)) as ex:
-        list(ex.map(work, [(b, l) for b in range(B) for l in range(L)]))
+        list(ex.map(work, [(i, l) for i in range(B) for l in range(L)]))
     return {"q": q, "k_new": kn, "v_new": vn}
