@@ -140,21 +140,50 @@ def vision_scores(Abar: np.ndarray, w_tilde: np.ndarray, n_sys: int, n_vis: int)
     return np.einsum("gi,gij->gj", w_tilde, TV)
 
 
-def score_slice(q_text, k, n_sys, n_vis, n_qst, sm_scale=None, head_mode=0) -> Dict[str, np.ndarray]:
-    """All scores of one (sequence, layer): lse, s_txt, w_txt (= w~), tv_mass, s_vis."""
+def score_slice(q_text, k, n_sys, n_vis, n_qst, sm_scale=None, head_mode=0,
+                vision_rank: int = 0) -> Dict[str, np.ndarray]:
+    """All scores of one (sequence, layer): lse, s_txt, w_txt (= w~), tv_mass, s_vis.
+
+    vision_rank 1 is the ablation's plain attention sum in place of TWR (Table 5):
+    every text row weighs 1, so s^V_j = sum_i A^TV_ij, and w_txt is all ones.
+    """
     H_kv, _, d = np.shape(k)
     if sm_scale is None:
         sm_scale = default_scale(d)
     P, lse = text_row_softmax(q_text, k, n_sys, n_vis, n_qst, sm_scale)
     Abar = head_average(P, H_kv, head_mode)
     s_txt = text_scores(Abar, n_sys, n_vis, n_qst)
-    w_til = text_weights(s_txt)
+    w_til = text_weights(s_txt) if vision_rank == 0 else np.ones_like(s_txt)
     s_vis = vision_scores(Abar, w_til, n_sys, n_vis)
     return {"lse": lse, "s_txt": s_txt, "w_txt": w_til, "tv_mass": tv_mass(P, n_sys, n_vis),
             "s_vis": s_vis, "P": P}
 
 
 # --------------------------------------------------------------------------- budgets
+def budget_masses(tv_masses: Sequence[float], rule: int, n_text: int) -> List[float]:
+    """Per-layer masses that share out the budget (Table 1(a), Eq. (5) over other slices).
+
+    rule 0: the text->vision mass (TVB); 1: uniform (every layer 1); 2: the
+    text->text mass.  Every text row's probabilities over its visible keys sum
+    to 1, and its visible keys are text and vision tokens, so the head-averaged
+    text->text mass of a layer is N_t minus its text->vision mass.  Non-finite
+    or negative masses count as 0 first (as in layer_budgets).
+    """
+    out = []
+    for x in tv_masses:
+        x = float(x)
+        x = x if (math.isfinite(x) and x > 0.0) else 0.0
+        if rule == 0:
+            out.append(x)
+        elif rule == 1:
+            out.append(1.0)
+        elif rule == 2:
+            out.append(max(float(n_text) - x, 0.0))
+        else:
+            raise ValueError("unknown budget rule")
+    return out
+
+
 def layer_budgets(masses: Sequence[float], total_budget: int, n_tokens: int, n_floor: int = 0,
                   return_detail: bool = False):
     """Integer per-layer budgets of one sequence (TVB, Eq. (5)-(6)).
@@ -232,19 +261,22 @@ def forced_vision_count(n_sys: int, n_vis: int, n_qst: int, n_sink: int = 0, n_r
 
 
 def vision_only_budgets(masses: Sequence[float], vision_budget: int, n_text: int, n_vis: int,
-                        n_floor: int = 0) -> np.ndarray:
+                        n_forced_vis: int = 0) -> np.ndarray:
     """Per-layer kept-token counts of vision-only eviction (App. B.3).
 
     In this mode every layer keeps all of its N_t text tokens and the retention
-    ratio counts vision tokens only.  The per-sequence vision budget V_tot is
-    shared out over the layers by TVB exactly as the full budget is in
-    layer_budgets (Eq. (5)-(6)), with the per-layer cap n_vis and, as floor, the
-    forced positions that are vision tokens; layer l keeps b_l = N_t + v_l tokens.
-    Retention then always falls in the first case of Eq. (10).  Returns int64 [L].
+    ratio counts vision tokens only.  Forced positions that are vision tokens
+    (App. A.2) are kept like the text, so the per-sequence vision budget V_tot
+    counts the other n_vis - n_forced_vis vision tokens.  It is shared out over the
+    layers by TVB exactly as the full budget is in layer_budgets (Eq. (5)-(6)),
+    with that count as the per-layer cap, and layer l keeps
+    b_l = N_t + n_forced_vis + v_l tokens.  Retention then always falls in the
+    first case of Eq. (10).  Returns int64 [L].
     """
-    if vision_budget < 0 or vision_budget > len(masses) * n_vis:
-        raise ValueError("vision budget outside [0, L*n_vis]")
-    return int(n_text) + layer_budgets(masses, vision_budget, n_vis, n_floor)
+    cap = n_vis - n_forced_vis
+    if vision_budget < 0 or vision_budget > len(masses) * cap:
+        raise ValueError("vision budget outside [0, L*(n_vis - forced vision)]")
+    return int(n_text) + int(n_forced_vis) + layer_budgets(masses, vision_budget, cap, 0)
 
 
 # --------------------------------------------------------------------------- retention
@@ -278,6 +310,34 @@ def tpr_select(s_vis: np.ndarray, s_txt: np.ndarray, budget: int, n_sys: int, n_
     else:
         order = np.lexsort((v_cand, -v_sc))
         chosen = np.concatenate([t_cand, v_cand[order[:rest - len(t_cand)]]])
+    return np.sort(np.concatenate([forced, chosen])).astype(np.int64)
+
+
+def joint_select(s_vis: np.ndarray, s_txt: np.ndarray, budget: int, n_sys: int, n_vis: int,
+                 n_qst: int, n_sink: int = 0, n_recent: int = 0, vis_scale: float = 1.0) -> np.ndarray:
+    """Retention without TPR (the ablation's TPR-off rows, Table 5), ascending.
+
+    Forced tokens first, as in tpr_select; then the top (budget - |forced|) of all
+    other positions ranked together: text token j by s^T_j, vision token j by
+    vis_scale * s^V_j.  Under TWR (weights summing to 1) vis_scale = N_t puts s^V
+    on the column-sum scale of s^T; under the plain attention sum it is 1.
+    Ties go to the lower position.
+    """
+    N = n_sys + n_vis + n_qst
+    tpos = text_positions(n_sys, n_vis, n_qst)
+    vpos = vision_positions(n_sys, n_vis, n_qst)
+    forced = forced_positions(N, n_sink, n_recent)
+    if budget < 0 or budget > N:
+        raise ValueError("budget outside [0, N]")
+    if budget <= len(forced):
+        return forced[:budget].copy()
+    fset = set(forced.tolist())
+    pos = np.concatenate([tpos, vpos])
+    sc = np.concatenate([np.asarray(s_txt, np.float64), vis_scale * np.asarray(s_vis, np.float64)])
+    keep = np.array([p not in fset for p in pos], dtype=bool)
+    pos, sc = pos[keep], sc[keep]
+    order = np.lexsort((pos, -sc))
+    chosen = pos[order[:budget - len(forced)]]
     return np.sort(np.concatenate([forced, chosen])).astype(np.int64)
 
 
@@ -319,25 +379,29 @@ def decode_attention(q: np.ndarray, Kc: Sequence[np.ndarray], Vc: Sequence[np.nd
 # --------------------------------------------------------------------------- whole slices
 def evict_sequence(q_text_seq, k_seq, n_sys, n_vis, n_qst, total_budget_per_seq, sm_scale=None,
                    head_mode=0, n_sink=0, n_recent=0, layers: Optional[Sequence[int]] = None,
-                   keep_P: bool = False, vision_only: bool = False):
+                   keep_P: bool = False, vision_only: bool = False, budget_rule: int = 0,
+                   vision_rank: int = 0, joint_rank: bool = False):
     """Score, budget and select every layer of one sequence.
 
     q_text_seq [L][H][N_t][d], k_seq [L][H_kv][N][d] (any float dtype; used in float64).
     total_budget_per_seq is B_tot, or the vision budget V_tot with vision_only
-    (App. B.3; see vision_only_budgets).  Returns per-layer score dicts, the
-    budgets [L] (tokens kept per layer) and the retained positions per layer and
-    group.
+    (App. B.3; see vision_only_budgets).  budget_rule / vision_rank / joint_rank
+    select the paper's variants (budget_masses, score_slice, joint_select); all
+    0 / False is TGV-KV.  Returns per-layer score dicts, the budgets [L] (tokens
+    kept per layer) and the retained positions per layer and group.
     """
+    if vision_only and joint_rank:
+        raise ValueError("vision-only eviction keeps all text: no joint ranking")
     L = len(k_seq)
     H_kv, N, d = np.shape(k_seq[0])
     scale = default_scale(d) if sm_scale is None else sm_scale
     scores = []
     for l in range(L):
-        sc = score_slice(q_text_seq[l], k_seq[l], n_sys, n_vis, n_qst, scale, head_mode)
+        sc = score_slice(q_text_seq[l], k_seq[l], n_sys, n_vis, n_qst, scale, head_mode, vision_rank)
         if not keep_P:
             sc.pop("P")
         scores.append(sc)
-    masses = [s["tv_mass"] for s in scores]
+    masses = budget_masses([s["tv_mass"] for s in scores], budget_rule, n_sys + n_qst)
     if vision_only:
         nfv = forced_vision_count(n_sys, n_vis, n_qst, n_sink, n_recent)
         budgets = vision_only_budgets(masses, total_budget_per_seq, n_sys + n_qst, n_vis, nfv)
@@ -347,8 +411,13 @@ def evict_sequence(q_text_seq, k_seq, n_sys, n_vis, n_qst, total_budget_per_seq,
     idx = []
     for l in range(L):
         g = scores[l]["s_vis"].shape[0]
-        idx.append([tpr_select(scores[l]["s_vis"][gi], scores[l]["s_txt"][gi], int(budgets[l]),
-                               n_sys, n_vis, n_qst, n_sink, n_recent) for gi in range(g)])
+        if joint_rank:
+            vis_scale = float(n_sys + n_qst) if vision_rank == 0 else 1.0
+            idx.append([joint_select(scores[l]["s_vis"][gi], scores[l]["s_txt"][gi], int(budgets[l]),
+                                     n_sys, n_vis, n_qst, n_sink, n_recent, vis_scale) for gi in range(g)])
+        else:
+            idx.append([tpr_select(scores[l]["s_vis"][gi], scores[l]["s_txt"][gi], int(budgets[l]),
+                                   n_sys, n_vis, n_qst, n_sink, n_recent) for gi in range(g)])
     return scores, budgets, idx
 
 

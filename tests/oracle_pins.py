@@ -413,6 +413,66 @@ def check_vision_only(O, seed=8):
         assert text <= set(idx[l][0].tolist()) and len(idx[l][0]) == b[l]
 
 
+def check_variants(O, seed=9):
+    """Budget rules, the plain attention sum and ranking without TPR (Table 1(a), Table 5)."""
+    rng = np.random.default_rng(seed)
+    # uniform budgets ignore the masses: the closed form of an equal split
+    for L, N, tot in [(32, 2979, 4766), (5, 100, 13), (7, 40, 0)]:
+        m = rng.random(L) * 10
+        b = O.layer_budgets(O.budget_masses(m, 1, 99), tot, N)
+        q, r = divmod(tot, L)
+        assert list(b) == [q + 1] * r + [q] * (L - r)
+    # the text->text rule: N_t minus the text->vision mass, clamped at 0, non-finite masses as 0
+    tt = O.budget_masses([0.25, 0.875, 0.5, 3.0, float("nan")], 2, 1)
+    assert tt == [0.75, 0.125, 0.5, 0.0, 1.0]
+    assert list(O.layer_budgets(tt[:3], 11, 100)) == [6, 1, 4]  # shares 0.75 : 0.125 : 0.5 of 11
+    # ... and the identity behind it, from the oracle's own softmax: the head-averaged mass of
+    # the text x text block plus the text->vision mass is N_t
+    for head_mode in (0, 1):
+        q, k = _tiny_inputs(rng, n_sys=3, n_vis=7, n_qst=5)
+        P, _ = O.text_row_softmax(q, k, 3, 7, 5, 0.4)
+        tpos = _positions(3, 7, 5)
+        tt_direct = P[:, :, tpos].sum(axis=(1, 2)).mean()
+        assert abs(tt_direct + O.tv_mass(P, 3, 7) - 8) < 1e-9
+    # plain attention sum: unit weights, and the vision scores add up to the layer's TV mass
+    for head_mode in (0, 1):
+        q, k = _tiny_inputs(rng, n_sys=2, n_vis=9, n_qst=4)
+        sc = O.score_slice(q, k, 2, 9, 4, 0.5, head_mode, vision_rank=1)
+        assert np.all(sc["w_txt"] == 1.0)
+        if head_mode == 0:
+            assert abs(sc["s_vis"].sum() - sc["tv_mass"]) < 1e-9
+        tw = O.score_slice(q, k, 2, 9, 4, 0.5, head_mode)
+        assert np.allclose(tw["s_txt"], sc["s_txt"]) and not np.allclose(tw["s_vis"], sc["s_vis"])
+    # ranking without TPR: forced first, then every other token on one scale (pairwise dominance)
+    for _ in range(200):
+        ns, nv, nq = int(rng.integers(0, 4)), int(rng.integers(0, 10)), int(rng.integers(0, 4))
+        n = ns + nv + nq
+        if n == 0:
+            continue
+        fs, fr = int(rng.integers(0, 3)), int(rng.integers(0, 2))
+        sv = np.round(rng.random(nv), 1)
+        st = np.round(rng.random(ns + nq) * 3, 1)
+        scale = float(rng.choice([1.0, ns + nq if ns + nq else 1.0]))
+        b = int(rng.integers(0, n + 1))
+        keep = O.joint_select(sv, st, b, ns, nv, nq, fs, fr, scale)
+        assert len(keep) == b and np.all(np.diff(keep) > 0)
+        forced = set(O.forced_positions(n, fs, fr).tolist())
+        score = {}
+        for i, p_ in enumerate(_positions(ns, nv, nq)):
+            score[p_] = st[i]
+        for j in range(nv):
+            score[ns + j] = scale * sv[j]
+        kept = set(keep.tolist())
+        if b >= len(forced):
+            assert forced <= kept
+            for p_ in kept - forced:
+                for q_ in set(range(n)) - kept - forced:
+                    assert score[p_] > score[q_] or (score[p_] == score[q_] and p_ < q_), (p_, q_)
+    # a dominant vision token beats the text without TPR, and never with it
+    assert list(O.joint_select([5.0, 0.0], [1.0, 1.0], 1, 1, 2, 1)) == [1]
+    assert list(O.tpr_select([5.0, 0.0], [1.0, 1.0], 1, 1, 2, 1)) == [0]
+
+
 ALL_CHECKS = [
     check_softmax_rows,
     check_mass_split,
@@ -424,4 +484,5 @@ ALL_CHECKS = [
     check_tpr,
     check_compact_and_decode,
     check_vision_only,
+    check_variants,
 ]

@@ -14,7 +14,8 @@ from tests import oracle_pins as pins
 
 _orig = {name: getattr(O, name) for name in
          ("text_row_softmax", "text_scores", "text_weights", "vision_scores", "tv_mass",
-          "head_average", "layer_budgets", "tpr_select", "decode_attention", "vision_only_budgets")}
+          "head_average", "layer_budgets", "tpr_select", "decode_attention", "vision_only_budgets",
+          "budget_masses", "score_slice", "joint_select")}
 
 
 def _softmax_mask_off_by_one(q_text, k, n_sys, n_vis, n_qst, sm_scale):
@@ -141,6 +142,29 @@ def _vision_only_forced_inside_budget(masses, vision_budget, n_text, n_vis, n_fo
     return int(n_text) + O.layer_budgets(masses, vision_budget, n_vis, n_forced_vis)
 
 
+def _tt_mass_not_flipped(tv_masses, rule, n_text):
+    # uses the text->vision mass for the text->text rule
+    return _orig["budget_masses"](tv_masses, 0 if rule == 2 else rule, n_text)
+
+
+def _attention_sum_still_weighted(q_text, k, n_sys, n_vis, n_qst, sm_scale=None, head_mode=0, vision_rank=0):
+    # ignores the plain-attention-sum switch
+    return _orig["score_slice"](q_text, k, n_sys, n_vis, n_qst, sm_scale, head_mode, 0)
+
+
+def _joint_ties_to_higher_position(s_vis, s_txt, budget, n_sys, n_vis, n_qst, n_sink=0, n_recent=0,
+                                   vis_scale=1.0):
+    N = n_sys + n_vis + n_qst
+    I = _orig["joint_select"](np.asarray(s_vis, float)[::-1].copy(), np.asarray(s_txt, float)[::-1].copy(),
+                              budget, n_qst, n_vis, n_sys, n_recent, n_sink, vis_scale)
+    return np.sort(N - 1 - I)
+
+
+def _joint_without_scale(s_vis, s_txt, budget, n_sys, n_vis, n_qst, n_sink=0, n_recent=0, vis_scale=1.0):
+    # ranks the vision scores unscaled
+    return _orig["joint_select"](s_vis, s_txt, budget, n_sys, n_vis, n_qst, n_sink, n_recent, 1.0)
+
+
 MUTANTS = {
     "softmax_mask_off_by_one": ("text_row_softmax", _softmax_mask_off_by_one),
     "softmax_wrong_kv_head": ("text_row_softmax", _softmax_wrong_kv_head),
@@ -161,6 +185,10 @@ MUTANTS = {
     "vision_only_cap_at_sequence_length": ("vision_only_budgets", _vision_only_cap_at_sequence_length),
     "vision_only_drops_text": ("vision_only_budgets", _vision_only_drops_text),
     "vision_only_forced_inside_budget": ("vision_only_budgets", _vision_only_forced_inside_budget),
+    "tt_mass_not_flipped": ("budget_masses", _tt_mass_not_flipped),
+    "attention_sum_still_weighted": ("score_slice", _attention_sum_still_weighted),
+    "joint_ties_to_higher_position": ("joint_select", _joint_ties_to_higher_position),
+    "joint_without_scale": ("joint_select", _joint_without_scale),
 }
 
 
