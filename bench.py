@@ -48,6 +48,11 @@ def parse():
                     help="the text rows' normalisers come from the prefill (computed before the timed region "
                          "by the library's own statistics sweep, standing in for a prefill attention kernel's "
                          "row log-sum-exp): scoring reads K once")
+    ap.add_argument("--budget-rule", default="tv", choices=("tv", "uniform", "tt"),
+                    help="layer budgets by text->vision mass (TVB), equally, or by text->text mass")
+    ap.add_argument("--vision-rank", default="twr", choices=("twr", "attention_sum"),
+                    help="vision importance: text-weighted ranking or the plain text-row attention sum")
+    ap.add_argument("--no-tpr", action="store_true", help="rank text and vision tokens together (no TPR)")
     ap.add_argument("--vision-only", action="store_true",
                     help="vision-only eviction (every layer keeps all text; rho is the retained share of the "
                          "vision tokens) instead of eviction among all tokens")
@@ -107,7 +112,7 @@ def traffic_for(kernel, workload, decode_steps=None):
     return rec.get("bytes_per_launch")
 
 
-def cpu_baseline(cfg, t, dec, tot, budget_s, vision_only=False):
+def cpu_baseline(cfg, t, dec, tot, budget_s, vision_only=False, opts=None):
     """The fp64 oracle, as it stands, on whole sequences of the same inputs until ~budget_s seconds."""
     import numpy as np
     import oracle.tgvkv_oracle as O
@@ -123,7 +128,10 @@ def cpu_baseline(cfg, t, dec, tot, budget_s, vision_only=False):
     for b in range(cfg.batch):
         q = bf16_bits_to_f32(t["q_text"][b])
         k = bf16_bits_to_f32(t["k"][b])
-        _, budgets, idx = O.evict_sequence(q, k, cfg.n_sys, cfg.n_vis, cfg.n_qst, tot, vision_only=vision_only)
+        _, budgets, idx = O.evict_sequence(q, k, cfg.n_sys, cfg.n_vis, cfg.n_qst, tot, vision_only=vision_only,
+                                           budget_rule=opts.budget_rule if opts else 0,
+                                           vision_rank=opts.vision_rank if opts else 0,
+                                           joint_rank=bool(opts.joint_rank) if opts else False)
         for l in range(cfg.layers):
             O.compact_slice(t["k"][b, l], t["v"][b, l], idx[l], 0)
         if idx0 is None:
@@ -266,7 +274,11 @@ def main():
     q_d, k_d, v_d = dev(t["q_text"]), dev(t["k"]), dev(t["v"])
     dq, dk, dv = dev(dec["q"]), dev(dec["k_new"]), dev(dec["v_new"])
     p = bd.problem_from(cfg)
-    opts = bd.make_opts(vision_only=args.vision_only)
+    opts = bd.make_opts(vision_only=args.vision_only,
+                        budget_rule={"tv": bd.BUDGET_TV, "uniform": bd.BUDGET_UNIFORM, "tt": bd.BUDGET_TT}[
+                            args.budget_rule],
+                        vision_rank={"twr": bd.RANK_TWR, "attention_sum": bd.RANK_ATTENTION_SUM}[args.vision_rank],
+                        joint_rank=args.no_tpr)
     buf = bd.EvictionBuffers(p, opts, tot, max(T, 1))
     stream = torch.cuda.current_stream()
     schedule = args.schedule
@@ -378,6 +390,7 @@ def main():
                    "n_sys": cfg.n_sys, "n_vis": Nv, "n_qst": Nq, "retention": rho, "total_budget_per_seq": tot,
                    "vision_only": bool(args.vision_only),
                    "normalisers_from_prefill": bool(args.lse_from_prefill),
+                   "budget_rule": args.budget_rule, "vision_rank": args.vision_rank, "tpr": not args.no_tpr,
                    "decode_steps": T, "vision_scored_layers": vis_layers, "schedule": sched},
         "evict_ms": round(evict_ms, 4),
         "decode_us_per_step": round(dec_ms * 1e3, 2),
@@ -390,7 +403,7 @@ def main():
         "wall_ms_per_step": round(wall / args.steps * 1e3, 3),
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(cfg, t, dec, tot, args.cpu_seconds, args.vision_only)
+        line["cpu_baseline"] = cpu_baseline(cfg, t, dec, tot, args.cpu_seconds, args.vision_only, opts)
     print(json.dumps(line), flush=True)
 
 

@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define TGVKV_ABI_VERSION 2
+#define TGVKV_ABI_VERSION 3
 
 typedef enum tgvkv_status {
     TGVKV_OK = 0,
@@ -71,7 +71,7 @@ typedef struct tgvkv_problem {
     int32_t n_qst;
 } tgvkv_problem;
 
-/* Options.  Passing NULL selects the defaults {0, 0, 0, 0, 0}. */
+/* Options.  Passing NULL selects the defaults (all 0: the paper's TGV-KV). */
 typedef struct tgvkv_opts {
     float   sm_scale;    /* logit scale; <= 0 selects 1/sqrt(head_dim)                       */
     int32_t head_mode;   /* 0: per-layer retained set (paper); 1: per-KV-head retained sets  */
@@ -80,6 +80,14 @@ typedef struct tgvkv_opts {
     int32_t vision_only; /* 0: evict among all tokens (TPR, Eq. (10)); 1: vision-only eviction
                             of App. B.3: every layer keeps all text, and the budget given to
                             tgvkv_budget counts vision tokens only (see there)                */
+    /* The paper's variants (Table 1(a), Table 5), for ablations:                            */
+    int32_t budget_rule; /* layer budgets in proportion to 0: the text->vision mass (TVB);
+                            1: nothing (uniform); 2: the text->text mass, N_t - tv_mass      */
+    int32_t vision_rank; /* vision importance 0: TWR, Eq. (8); 1: the plain text-row attention
+                            sum s_vis[j] = sum_i Abar[i, n_sys + j] (w_txt is then all ones) */
+    int32_t joint_rank;  /* 0: TPR, Eq. (10); 1: no TPR: forced tokens, then all others ranked
+                            together, text by s_txt and vision by s_vis (times N_t under TWR,
+                            whose weights sum to 1).  Not with vision_only.                  */
 } tgvkv_opts;
 
 /* Score phases (bit mask for tgvkv_score). */

@@ -34,7 +34,8 @@ class TgvkvProblem(ctypes.Structure):
 
 class TgvkvOpts(ctypes.Structure):
     _fields_ = [("sm_scale", ctypes.c_float), ("head_mode", ctypes.c_int32), ("n_sink", ctypes.c_int32),
-                ("n_recent", ctypes.c_int32), ("vision_only", ctypes.c_int32)]
+                ("n_recent", ctypes.c_int32), ("vision_only", ctypes.c_int32), ("budget_rule", ctypes.c_int32),
+                ("vision_rank", ctypes.c_int32), ("joint_rank", ctypes.c_int32)]
 
 
 class TgvkvError(RuntimeError):
@@ -86,9 +87,16 @@ def problem_from(cfg) -> TgvkvProblem:
                         cfg.n_qst)
 
 
+BUDGET_TV, BUDGET_UNIFORM, BUDGET_TT = 0, 1, 2        # layer budgets by TV mass, equally, by TT mass
+RANK_TWR, RANK_ATTENTION_SUM = 0, 1                     # vision importance
+
+
 def make_opts(sm_scale: float = 0.0, head_mode: int = 0, n_sink: int = 0, n_recent: int = 0,
-              vision_only: bool = False) -> TgvkvOpts:
-    return TgvkvOpts(sm_scale, head_mode, n_sink, n_recent, int(bool(vision_only)))
+              vision_only: bool = False, budget_rule: int = BUDGET_TV, vision_rank: int = RANK_TWR,
+              joint_rank: bool = False) -> TgvkvOpts:
+    """Options; the defaults are the paper's TGV-KV (TVB, TWR, TPR over all tokens)."""
+    return TgvkvOpts(sm_scale, head_mode, n_sink, n_recent, int(bool(vision_only)), int(budget_rule),
+                     int(vision_rank), int(bool(joint_rank)))
 
 
 def forced_or_text_count(problem, opts) -> int:
@@ -102,6 +110,16 @@ def forced_or_text_count(problem, opts) -> int:
     v0, v1 = p.n_sys, p.n_sys + p.n_vis
     fv = max(0, min(fs, v1) - v0) + max(0, v1 - max(fr, v0))
     return p.n_sys + p.n_qst + fv
+
+
+def forced_count(problem, opts) -> int:
+    """|forced|: the first n_sink and the last n_recent positions."""
+    N = problem.n_sys + problem.n_vis + problem.n_qst
+    n_sink = opts.n_sink if opts is not None else 0
+    n_recent = opts.n_recent if opts is not None else 0
+    fs = min(n_sink, N)
+    fr = max(N - n_recent, fs)
+    return fs + (N - fr)
 
 
 def kept_per_sequence(problem, opts, total_budget: int) -> int:
@@ -275,7 +293,10 @@ class EvictionBuffers:
                       self.total_budget, self.decode_reserve, self.kc, self.vc, stream)
 
     def forced_or_text(self) -> int:
-        """|forced U T|: a layer needs vision scores only when its budget exceeds this."""
+        """A layer needs vision scores only when its budget exceeds this: |forced U T| with TPR,
+        |forced| when text and vision are ranked jointly."""
+        if self.opts is not None and self.opts.joint_rank:
+            return forced_count(self.problem, self.opts)
         return forced_or_text_count(self.problem, self.opts)
 
     def schedule(self) -> str:

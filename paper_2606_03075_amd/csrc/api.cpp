@@ -39,6 +39,9 @@ tgvkv_status make_shape(const tgvkv_problem* p, const tgvkv_opts* o, Shape* s) {
     if (d.head_mode != 0 && d.head_mode != 1) return TGVKV_E_INVAL;
     if (d.n_sink < 0 || d.n_recent < 0) return TGVKV_E_INVAL;
     if (d.vision_only != 0 && d.vision_only != 1) return TGVKV_E_INVAL;
+    if (d.budget_rule < 0 || d.budget_rule > 2 || d.vision_rank < 0 || d.vision_rank > 1 || d.joint_rank < 0 ||
+        d.joint_rank > 1 || (d.vision_only && d.joint_rank))
+        return TGVKV_E_INVAL;
     if (!std::isfinite(d.sm_scale)) return TGVKV_E_INVAL;
     if (p->head_dim != 64 && p->head_dim != 128) return TGVKV_E_UNSUPPORTED;
     if (p->layers > kMaxLayers || N > kMaxTokens) return TGVKV_E_UNSUPPORTED;
@@ -63,6 +66,9 @@ tgvkv_status make_shape(const tgvkv_problem* p, const tgvkv_opts* o, Shape* s) {
     s->n_sink = d.n_sink;
     s->n_recent = d.n_recent;
     s->vision_only = d.vision_only;
+    s->budget_rule = d.budget_rule;
+    s->vision_rank = d.vision_rank;
+    s->joint_rank = d.joint_rank;
     s->sm_scale = d.sm_scale > 0.f ? d.sm_scale : 1.0f / std::sqrt((float)p->head_dim);
     s->scale2 = s->sm_scale * 1.4426950408889634f;
     return TGVKV_OK;
@@ -86,8 +92,12 @@ int32_t forced_vision_count(const Shape& s) {
     return (int32_t)fv;
 }
 
-// |forced U T|: a layer needs vision scores only when its budget exceeds this.
+// |forced U T|.
 int32_t forced_or_text_count(const Shape& s) { return s.Nt + forced_vision_count(s); }
+
+// A layer needs vision scores only when its budget exceeds this: |forced U T| with TPR
+// (vision tokens compete only once all text is kept), |forced| when ranked jointly.
+int32_t vision_threshold(const Shape& s) { return s.joint_rank ? forced_count(s) : forced_or_text_count(s); }
 
 // Vision-only eviction (App. B.3): every layer keeps its text and its forced vision
 // positions; the budget shares out the other vision tokens.
@@ -208,7 +218,7 @@ tgvkv_status tgvkv_score(const tgvkv_problem* problem, const tgvkv_opts* opts, i
     const ScoreWs w = score_workspace(s, rp, workspace);
     const uint16_t* q = static_cast<const uint16_t*>(q_text);
     const uint16_t* kk = static_cast<const uint16_t*>(k);
-    const int32_t vthr = forced_or_text_count(s);
+    const int32_t vthr = vision_threshold(s);
 
     // One persistent kernel when asked for and the shape allows it (one row group per unit).
     if (want_fused && w.sync != nullptr) {

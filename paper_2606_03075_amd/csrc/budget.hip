@@ -49,7 +49,11 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(Shape s, const float* 
 
     for (int l = tid; l < L; l += kThreads) {
         const float mv = tv_mass[(size_t)b * L + l];
-        x[l] = (isfinite(mv) && mv > 0.f) ? (double)mv : 0.0;  // masses, for now
+        double m = (isfinite(mv) && mv > 0.f) ? (double)mv : 0.0;
+        // the variants of Table 1(a): uniform, or the text->text mass N_t - m
+        if (s.budget_rule == 1) m = 1.0;
+        else if (s.budget_rule == 2) m = fmax((double)s.Nt - m, 0.0);
+        x[l] = m;  // masses, for now
         active[l] = 1;
     }
     __syncthreads();

@@ -641,7 +641,8 @@ __device__ inline void finalize_group(const Shape& s, int bl, int gi, const floa
     const float W = red[0];
     for (int j = tid; j < s.Nt; j += kThreads) {
         const float w = s_txt[obase + j] / (float)(s.Nt - j);
-        w_txt[obase + j] = W > 0.f ? w / W : 0.f;
+        // the plain attention sum (Table 5) weighs every text row 1
+        w_txt[obase + j] = s.vision_rank == 1 ? 1.f : (W > 0.f ? w / W : 0.f);
     }
     if (with_mass && gi == 0 && tid == 0) {
         float a = 0.f;

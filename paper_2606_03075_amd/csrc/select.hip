@@ -8,7 +8,9 @@
 // k-th key is found by a wave-wide scan of the histogram), which yields the k-th
 // largest key and how many of its ties to take; ties go to the lower position.
 // A single ordered scan over all N positions then emits the retained positions
-// already in ascending order, with no sort.  Candidate keys are read from global
+// already in ascending order, with no sort.  Without TPR (an ablation of Table 5)
+// all non-forced positions compete on one scale: text by s^T, vision by s^V times
+// a factor (N_t under TWR, whose weights sum to 1).  Candidate keys are read from global
 // memory once and kept in LDS when the row fits (N <= kLdsKeys).
 #include "tgvkv_device.h"
 #include "tgvkv_shape.h"
@@ -18,12 +20,13 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kLdsKeys = 12288;  // 48 KB of LDS keys per workgroup
-enum { MODE_FORCED = 0, MODE_TEXT = 1, MODE_VIS = 2 };
+enum { MODE_FORCED = 0, MODE_TEXT = 1, MODE_VIS = 2, MODE_JOINT = 3 };
 constexpr uint32_t kNotCand = 0u;  // keys of real candidates have the top bit or are >= 1
 
 struct RowCtx {
     int N, Ns, Nv, Nt, fs, fr;  // forced = [0, fs) U [fr, N)
     int mode;
+    float vscale;               // factor on s^V in the joint ranking
     const float* sv;            // s_vis row (n_vis)
     const float* st;            // s_txt row (N_t)
     __device__ bool forced(int p) const { return p < fs || p >= fr; }
@@ -31,12 +34,14 @@ struct RowCtx {
     __device__ bool cand(int p) const {
         if (mode == MODE_FORCED) return forced(p);
         if (forced(p)) return false;
+        if (mode == MODE_JOINT) return true;
         return mode == MODE_VIS ? is_vis(p) : !is_vis(p);
     }
     // key of a candidate (only called when cand(p))
     __device__ uint32_t key(int p) const {
         if (mode == MODE_FORCED) return 0u;
         if (mode == MODE_VIS) return ordered_key(sv[p - Ns]);
+        if (mode == MODE_JOINT && is_vis(p)) return ordered_key(sv[p - Ns] * vscale);
         return ordered_key(st[p < Ns ? p : p - Nv]);
     }
     // kept without competing (forced in the text/vision modes, all text in the vision mode)
@@ -128,6 +133,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(Shape s, const float* 
     c.Nt = s.Nt;
     c.fs = min(s.n_sink, s.N);
     c.fr = max(s.N - s.n_recent, c.fs);
+    c.vscale = s.vision_rank == 0 ? (float)s.Nt : 1.f;
     c.sv = s_vis + ((size_t)bl * s.ngroups + gi) * s.Nv;
     c.st = s_txt + ((size_t)bl * s.ngroups + gi) * s.Nt;
 
@@ -141,9 +147,13 @@ __global__ __launch_bounds__(kThreads) void select_kernel(Shape s, const float* 
 
     int k;
     if (bgt <= nf) { c.mode = MODE_FORCED; k = bgt; }
+    else if (s.joint_rank) { c.mode = MODE_JOINT; k = bgt - nf; }
     else if (bgt - nf <= ntf) { c.mode = MODE_TEXT; k = bgt - nf; }
     else { c.mode = MODE_VIS; k = bgt - nf - ntf; }
-    const int nc = c.mode == MODE_FORCED ? nf : (c.mode == MODE_TEXT ? ntf : s.N - nf - ntf);
+    const int nc = c.mode == MODE_FORCED ? nf
+                 : c.mode == MODE_JOINT  ? s.N - nf
+                 : c.mode == MODE_TEXT   ? ntf
+                                         : s.N - nf - ntf;
 
     // key lookup: from LDS when the row fits, else re-read
     auto key_at = [&](int p) -> uint32_t { return LDS_KEYS ? keys[p] : c.key(p); };

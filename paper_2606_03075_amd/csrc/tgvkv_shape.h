@@ -12,6 +12,9 @@ struct Shape {
     int32_t head_mode, ngroups;
     int32_t n_sink, n_recent;
     int32_t vision_only;  // every layer keeps all text; budgets count vision tokens
+    int32_t budget_rule;  // 0: TV mass, 1: uniform, 2: TT mass
+    int32_t vision_rank;  // 0: TWR, 1: plain attention sum
+    int32_t joint_rank;   // 1: no TPR (text and vision ranked together)
     float sm_scale;
     float scale2;  // sm_scale * log2(e): logits in base-2 units
 };

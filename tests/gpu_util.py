@@ -86,8 +86,11 @@ def budget_allowed(gpu_b, orc_b, masses, total, N, n_floor, tol=SCORE_RTOL):
     return bool(span <= 2 * tol * max(1.0, float(np.max(x[diff]))))
 
 
-def candidate_scores(s_vis, s_txt, budget, cfg, n_sink=0, n_recent=0):
-    """Oracle view of one selection row: per-position score of the competing candidates and the k-th score."""
+def candidate_scores(s_vis, s_txt, budget, cfg, n_sink=0, n_recent=0, vis_scale=None):
+    """Oracle view of one selection row: per-position score of the competing candidates and the k-th score.
+
+    vis_scale: None for TPR (text first); a factor for the joint ranking without TPR.
+    """
     N = cfg.n_tokens
     forced = set(O.forced_positions(N, n_sink, n_recent).tolist())
     tpos = O.text_positions(cfg.n_sys, cfg.n_vis, cfg.n_qst)
@@ -97,7 +100,15 @@ def candidate_scores(s_vis, s_txt, budget, cfg, n_sink=0, n_recent=0):
     sc = {}
     if rest <= 0:
         return sc, None
-    if rest <= n_tf:
+    if vis_scale is not None:
+        for i, p in enumerate(tpos):
+            if p not in forced:
+                sc[int(p)] = float(s_txt[i])
+        for j, p in enumerate(vpos):
+            if p not in forced:
+                sc[int(p)] = float(vis_scale * s_vis[j])
+        k = rest
+    elif rest <= n_tf:
         for i, p in enumerate(tpos):
             if p not in forced:
                 sc[int(p)] = float(s_txt[i])
@@ -113,7 +124,8 @@ def candidate_scores(s_vis, s_txt, budget, cfg, n_sink=0, n_recent=0):
     return sc, kth
 
 
-def idx_allowed(gpu_idx, orc_idx, s_vis, s_txt, budget, cfg, n_sink=0, n_recent=0, tol=SCORE_RTOL):
+def idx_allowed(gpu_idx, orc_idx, s_vis, s_txt, budget, cfg, n_sink=0, n_recent=0, tol=SCORE_RTOL,
+                vis_scale=None):
     """Number of boundary swaps; raises AssertionError if a difference is not a boundary tie."""
     g = set(int(x) for x in gpu_idx)
     o = set(int(x) for x in orc_idx)
@@ -121,7 +133,7 @@ def idx_allowed(gpu_idx, orc_idx, s_vis, s_txt, budget, cfg, n_sink=0, n_recent=
     assert list(gpu_idx) == sorted(gpu_idx), "retained positions not ascending"
     if g == o:
         return 0
-    sc, kth = candidate_scores(s_vis, s_txt, budget, cfg, n_sink, n_recent)
+    sc, kth = candidate_scores(s_vis, s_txt, budget, cfg, n_sink, n_recent, vis_scale)
     assert kth is not None, "sets differ but no top-k boundary exists"
     for p in g ^ o:
         assert p in sc, f"position {p} differs but is not a top-k candidate"

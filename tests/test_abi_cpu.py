@@ -44,7 +44,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(bd.EXPORTS) <= set(names) and len(names) == len(bd.EXPORTS), names
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.tgvkv_abi_version() == 2
+    assert lib.tgvkv_abi_version() == 3
     for st in (0, -1, -2, -3, -4, -5):
         assert lib.tgvkv_status_string(st)
     assert lib.tgvkv_status_string(7) == b"unknown status"
@@ -82,7 +82,8 @@ def test_validation_before_any_launch(lib):
     assert lib.tgvkv_score(None, None, 7, fake, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
     # bad options
     for o in (bd.make_opts(head_mode=2), bd.make_opts(n_sink=-1), bd.make_opts(sm_scale=float("nan")),
-              bd.TgvkvOpts(0.0, 0, 0, 0, 2)):
+              bd.TgvkvOpts(0.0, 0, 0, 0, 2), bd.make_opts(budget_rule=3), bd.make_opts(vision_rank=2),
+              bd.TgvkvOpts(0.0, 0, 0, 0, 0, 0, 0, 2), bd.make_opts(vision_only=True, joint_rank=True)):
         assert lib.tgvkv_score(ok, ctypes.byref(o), 7, fake, fake, fake, fake, fake, fake, fake, None, fake, big,
                                s) == -1
     # phases, null and misaligned pointers, workspace

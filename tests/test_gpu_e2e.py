@@ -65,13 +65,16 @@ def _inputs(cfg, seed, steps, gen_seqs):
 
 
 def run_and_check(cfg, rho, head_mode=0, forced=(0, 0), steps=2, seed=0, skip_text_only=True, check_seqs=None,
-                  decode_seqs=None, schedule="auto", vision_only=False, gen_seqs=None):
+                  decode_seqs=None, schedule="auto", vision_only=False, gen_seqs=None, budget_rule=0, vision_rank=0,
+                  joint_rank=False):
     import torch
-    log(f"e2e {cfg.name} rho={rho} mode={head_mode} forced={forced} steps={steps} vision_only={vision_only}")
+    log(f"e2e {cfg.name} rho={rho} mode={head_mode} forced={forced} steps={steps} vision_only={vision_only} "
+        f"budget_rule={budget_rule} vision_rank={vision_rank} joint_rank={joint_rank}")
     t, dec, dev_t, dev_dec = _inputs(cfg, seed, steps, gen_seqs)
     B, L, N = cfg.batch, cfg.layers, cfg.n_tokens
     p = bd.problem_from(cfg)
-    o = bd.make_opts(head_mode=head_mode, n_sink=forced[0], n_recent=forced[1], vision_only=vision_only)
+    o = bd.make_opts(head_mode=head_mode, n_sink=forced[0], n_recent=forced[1], vision_only=vision_only,
+                     budget_rule=budget_rule, vision_rank=vision_rank, joint_rank=joint_rank)
     # vision-only eviction (App. B.3): text and forced positions are all kept, rho is the retained
     # share of the other vision tokens
     nfv = O.forced_vision_count(cfg.n_sys, cfg.n_vis, cfg.n_qst, *forced)
@@ -86,7 +89,8 @@ def run_and_check(cfg, rho, head_mode=0, forced=(0, 0), steps=2, seed=0, skip_te
     def oracle_seq(b):
         if b not in orc:
             orc[b] = O.evict_sequence(bf16_bits_to_f32(t["q_text"][b]), bf16_bits_to_f32(t["k"][b]), cfg.n_sys,
-                                      cfg.n_vis, cfg.n_qst, tot, None, head_mode, *forced, vision_only=vision_only)
+                                      cfg.n_vis, cfg.n_qst, tot, None, head_mode, *forced, vision_only=vision_only,
+                                      budget_rule=budget_rule, vision_rank=vision_rank, joint_rank=joint_rank)
         return orc[b]
 
     if schedule == "lse_in":
@@ -117,7 +121,7 @@ def run_and_check(cfg, rho, head_mode=0, forced=(0, 0), steps=2, seed=0, skip_te
     for b in check_seqs:
         scores, ob, oidx = oracle_seq(b)
         assert budgets[b].sum() == kept
-        masses = [s["tv_mass"] for s in scores]
+        masses = O.budget_masses([s["tv_mass"] for s in scores], budget_rule, cfg.n_text)
         if vision_only:
             base = cfg.n_text + nfv
             assert np.all(budgets[b] >= base)
@@ -141,7 +145,9 @@ def run_and_check(cfg, rho, head_mode=0, forced=(0, 0), steps=2, seed=0, skip_te
             agree = True
             for gg in range(g):
                 gidx = idx[io[bl] + gg * bsz: io[bl] + (gg + 1) * bsz]
-                s_ = idx_allowed(gidx, oidx[l][gg], sc["s_vis"][gg], sc["s_txt"][gg], bsz, cfg, *forced)
+                vscale = (cfg.n_text if vision_rank == 0 else 1.0) if joint_rank else None
+                s_ = idx_allowed(gidx, oidx[l][gg], sc["s_vis"][gg], sc["s_txt"][gg], bsz, cfg, *forced,
+                                 vis_scale=vscale)
                 swaps += s_
                 agree = agree and s_ == 0
             if not agree:
@@ -259,3 +265,25 @@ def test_lse_in_shapes(lib):
 
 def test_lse_in_llava15(lib):
     run_and_check(CONFIGS["llava15"], 0.1, steps=4, seed=0, schedule="lse_in")
+
+
+# ----------------------------------------------------------------------------- the paper's variants
+@pytest.mark.parametrize("budget_rule", [0, 1, 2])
+@pytest.mark.parametrize("vision_rank", [0, 1])
+@pytest.mark.parametrize("joint_rank", [False, True])
+def test_variants_small(lib, budget_rule, vision_rank, joint_rank):
+    """Layer budgets by TV mass / equally / by TT mass; TWR or the plain attention sum; with or without TPR."""
+    cfg = custom_config(batch=2, layers=4, heads_q=8, heads_kv=4, head_dim=128, n_sys=6, n_vis=230, n_qst=21)
+    for rho in (0.05, 0.3):
+        for forced in [(0, 0), (4, 1)]:
+            run_and_check(cfg, rho, 0, forced, steps=2, seed=9, budget_rule=budget_rule, vision_rank=vision_rank,
+                          joint_rank=joint_rank)
+    run_and_check(cfg, 0.1, 1, (0, 0), steps=2, seed=10, budget_rule=budget_rule, vision_rank=vision_rank,
+                  joint_rank=joint_rank, schedule="lse_in")
+
+
+def test_variants_llava15(lib):
+    cfg = CONFIGS["llava15"]
+    run_and_check(cfg, 0.05, steps=2, seed=0, budget_rule=2, vision_rank=1, joint_rank=True)
+    run_and_check(cfg, 0.2, steps=2, seed=0, budget_rule=1, vision_rank=0, joint_rank=True)
+    run_and_check(cfg, 0.1, steps=2, seed=0, budget_rule=1, vision_rank=1, vision_only=True)

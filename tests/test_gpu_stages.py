@@ -42,16 +42,18 @@ def _mass_cases(rng, L):
     yield (rng.integers(1, 4, L) / 4).astype(np.float32)   # many equal fractions
 
 
+@pytest.mark.parametrize("budget_rule", [0, 1, 2])
 @pytest.mark.parametrize("L,N,n_sink,n_recent", [(32, 2979, 0, 0), (28, 8256, 4, 1), (5, 13, 0, 0),
                                                  (1, 168, 0, 0), (40, 3171, 4, 1), (7, 3, 1, 1)])
-def test_budget_kernel_exact(lib, L, N, n_sink, n_recent):
+def test_budget_kernel_exact(lib, L, N, n_sink, n_recent, budget_rule):
     torch = _torch()
     rng = np.random.default_rng(L * 1000 + N)
     cases = list(_mass_cases(rng, L))
     B = len(cases)
     masses = np.stack(cases)
     p = bd.make_problem(B, L, 4, 4, 128, 1, N - 2, 1)
-    o = bd.make_opts(n_sink=n_sink, n_recent=n_recent)
+    o = bd.make_opts(n_sink=n_sink, n_recent=n_recent, budget_rule=budget_rule)
+    nt = 2
     nf = len(O.forced_positions(N, n_sink, n_recent))
     for total in sorted({0, 1, L, (L * N) // 20, (L * N) // 3, L * N - 1, L * N}):
         for reserve in (0, 7):
@@ -63,7 +65,7 @@ def test_budget_kernel_exact(lib, L, N, n_sink, n_recent):
             torch.cuda.synchronize()
             gb = host(budgets)
             for b in range(B):
-                ob = O.layer_budgets(masses[b].astype(np.float64), total, N, nf)
+                ob = O.layer_budgets(O.budget_masses(masses[b].astype(np.float64), budget_rule, nt), total, N, nf)
                 assert np.array_equal(gb[b], ob), (b, total, gb[b], ob)
             assert np.array_equal(host(io), O.flat_offsets(gb.reshape(-1)))
             assert np.array_equal(host(so), O.flat_offsets(gb.reshape(-1) + reserve))
@@ -101,10 +103,11 @@ def test_budget_kernel_vision_only_exact(lib, L, ns, nv, nq, n_sink, n_recent):
 
 
 # ----------------------------------------------------------------------------- selection
+@pytest.mark.parametrize("rank", ["tpr", "joint_twr", "joint_sum"])
 @pytest.mark.parametrize("head_mode", [0, 1])
 @pytest.mark.parametrize("shape", [(3, 40, 5), (0, 30, 4), (8, 144, 16), (35, 576, 40), (2, 0, 9), (16, 1300, 48)])
 @pytest.mark.parametrize("forced", [(0, 0), (4, 1)])
-def test_select_kernel_exact(lib, head_mode, shape, forced):
+def test_select_kernel_exact(lib, head_mode, shape, forced, rank):
     torch = _torch()
     ns, nv, nq = shape
     N, nt = ns + nv + nq, ns + nq
@@ -123,7 +126,10 @@ def test_select_kernel_exact(lib, head_mode, shape, forced):
             bud[b, l] = choices[(b * L + l) % len(choices)]
     io = O.flat_offsets((bud * g).reshape(-1))
     p = bd.make_problem(B, L, 4, Hkv, 128, ns, nv, nq)
-    o = bd.make_opts(head_mode=head_mode, n_sink=forced[0], n_recent=forced[1])
+    joint = rank != "tpr"
+    vrank = 1 if rank == "joint_sum" else 0
+    o = bd.make_opts(head_mode=head_mode, n_sink=forced[0], n_recent=forced[1], vision_rank=vrank, joint_rank=joint)
+    vscale = float(nt) if vrank == 0 else 1.0   # scores on a grid of 1/8: the scaled values are exact in fp32
     d_sv = torch.from_numpy(sv).cuda() if nv else torch.zeros(1, device="cuda")
     d_st = torch.from_numpy(st).cuda() if nt else torch.zeros(1, device="cuda")
     d_b = torch.from_numpy(bud.astype(np.int32)).cuda()
@@ -136,8 +142,12 @@ def test_select_kernel_exact(lib, head_mode, shape, forced):
         for l in range(L):
             bl = b * L + l
             for gg in range(g):
-                want = O.tpr_select(sv[b, l, gg].astype(np.float64), st[b, l, gg].astype(np.float64),
-                                    int(bud[b, l]), ns, nv, nq, *forced)
+                if joint:
+                    want = O.joint_select(sv[b, l, gg].astype(np.float64), st[b, l, gg].astype(np.float64),
+                                          int(bud[b, l]), ns, nv, nq, *forced, vis_scale=vscale)
+                else:
+                    want = O.tpr_select(sv[b, l, gg].astype(np.float64), st[b, l, gg].astype(np.float64),
+                                        int(bud[b, l]), ns, nv, nq, *forced)
                 got = gi[io[bl] + gg * bud[b, l]: io[bl] + (gg + 1) * bud[b, l]]
                 assert np.array_equal(got, want), (b, l, gg, bud[b, l], got[:12], want[:12])
 
