@@ -12,6 +12,9 @@
  *   tgvkv_compact gather of the retained K/V rows into a ragged cache;
  * then every decode step appends one key/value and attends (Eq. (3)-(4)):
  *   tgvkv_decode_attn.
+ * The same cache can instead live in fixed-size pages of a shared pool, for
+ * serving with continuous batching: tgvkv_page_plan, tgvkv_page_table,
+ * tgvkv_compact_paged, tgvkv_decode_attn_paged.
  *
  * Conventions shared by every call
  *  - Token layout of each sequence: n_sys system-text tokens, then n_vis vision
@@ -43,7 +46,7 @@
 extern "C" {
 #endif
 
-#define TGVKV_ABI_VERSION 3
+#define TGVKV_ABI_VERSION 4
 
 typedef enum tgvkv_status {
     TGVKV_OK = 0,
@@ -237,8 +240,85 @@ tgvkv_status tgvkv_decode_attn(const tgvkv_problem* problem, const tgvkv_opts* o
                                const void* q, const void* k_new, const void* v_new, float* out,
                                void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * Paged cache, for serving with continuous batching.
+ *
+ * The retained rows of Eq. (10) and the rows decode appends (Eq. (3)-(4)) may
+ * instead live in fixed-size pages of one pool shared by every sequence in
+ * service, so a serving loop admits a newly evicted batch and retires finished
+ * sequences without moving anyone else's cache.  A page holds page_size rows of
+ * every KV head:
+ *   k_pool, v_pool  bf16 [n_pages][heads_kv][page_size][head_dim]
+ * and row n of (sequence b, layer l) is row n % page_size of page
+ *   block_table[(b*L + l) * max_pages + n / page_size].
+ * page_size is a power of two in [1, 4096] (TGVKV_E_INVAL otherwise); max_pages
+ * is in [1, 4096] (TGVKV_E_UNSUPPORTED above); 1 <= n_pages <= 2^31 - 1.  A page
+ * id outside [0, n_pages) (such as an unused entry's -1) is clamped into the
+ * pool, so a wrong table gives wrong values but never addresses outside it.
+ * Rows are bit-identical to tgvkv_compact's, and tgvkv_decode_attn_paged does
+ * the same arithmetic as tgvkv_decode_attn, so the layouts give equal results.
+ */
+
+/* tgvkv_page_plan -- host-only sizes of a paged batch (no HIP call).
+ * With the total_budget / decode_reserve given to tgvkv_budget:
+ *   *max_pages_out  = ceil((b_max + decode_reserve) / page_size), the table width
+ *                     every segment fits in, b_max the largest budget one layer can
+ *                     get (min(N, B_tot); N_t + F_v + min(n_vis - F_v, V_tot) with
+ *                     vision_only), at least 1;
+ *   *pool_pages_out = floor((B*K + B*L*(decode_reserve + page_size - 1)) / page_size),
+ *                     an upper bound on the pages tgvkv_page_table takes (K as in
+ *                     tgvkv_budget).
+ * TGVKV_E_UNSUPPORTED if the width exceeds 4096. */
+tgvkv_status tgvkv_page_plan(const tgvkv_problem* problem, const tgvkv_opts* opts, int64_t total_budget,
+                             int32_t decode_reserve, int32_t page_size, int32_t* max_pages_out,
+                             int64_t* pool_pages_out);
+
+/* tgvkv_page_table -- give every (sequence, layer) of a batch its pages.
+ * Segment i = b*L + l needs n_i = ceil((budgets[i] + decode_reserve) / page_size)
+ * pages; they are the next entries of free_pages in order of i:
+ *   block_table[i * max_pages + j] = free_pages[P_i + j] for j < n_i, P_i = sum_{i'<i} n_i',
+ *   block_table[i * max_pages + j] = -1 for n_i <= j < max_pages,
+ * and *pages_used = sum_i n_i (the caller drops that many ids from its free list).
+ * budgets      int32 [B][L] from tgvkv_budget (same total_budget, decode_reserve)
+ * free_pages   int32 [n_free] device, distinct page ids; n_free must be at least
+ *              tgvkv_page_plan's pool bound and max_pages at least its width
+ *              (TGVKV_E_CAPACITY otherwise)
+ * block_table  int32 [B*L][max_pages] out;  pages_used  int64 device scalar out
+ * With batch == 0 nothing is launched and *pages_used is not written. */
+tgvkv_status tgvkv_page_table(const tgvkv_problem* problem, const tgvkv_opts* opts, const int32_t* budgets,
+                              int64_t total_budget, int32_t decode_reserve, int32_t page_size,
+                              const int32_t* free_pages, int64_t n_free, int32_t* block_table, int32_t max_pages,
+                              int64_t* pages_used, hipStream_t stream);
+
+/* tgvkv_compact_paged -- tgvkv_compact into the pages of block_table: row n < b_l
+ * of (b, l), KV head h goes to k_pool[page][h][n % page_size][:] with page the
+ * table entry n / page_size.  Rows b_l .. are left for tgvkv_decode_attn_paged.
+ * TGVKV_E_CAPACITY if max_pages is below ceil(b_max / page_size). */
+tgvkv_status tgvkv_compact_paged(const tgvkv_problem* problem, const tgvkv_opts* opts, const void* k, const void* v,
+                                 const int32_t* idx, const int32_t* budgets, const int64_t* idx_offsets,
+                                 int64_t total_budget, const int32_t* block_table, int32_t max_pages,
+                                 int32_t page_size, void* k_pool, void* v_pool, int64_t n_pages,
+                                 hipStream_t stream);
+
+/* tgvkv_decode_attn_paged -- one decode step of a continuous batch over the paged cache.
+ * Each sequence b is at its own step steps[b] (int32 [B], device): for every layer
+ * it writes k_new / v_new at row budgets[b*L+l] + steps[b] of its pages and
+ * attends over rows n < budgets[b*L+l] + steps[b] + 1, as tgvkv_decode_attn does.
+ * A sequence whose step is outside [0, decode_reserve) (finished, or an empty slot)
+ * is skipped: its pages and its rows of out are not touched.  The batch may mix
+ * sequences from different prefill batches: only batch, layers, heads and
+ * head_dim of `problem` are used, and budgets / block_table rows are the
+ * callers' concatenation.  A segment's table row must cover its
+ * ceil((b_l + steps[b] + 1) / page_size) pages (tgvkv_page_table's do).
+ * Workspace: tgvkv_workspace_size(p, o, TGVKV_CALL_DECODE). */
+tgvkv_status tgvkv_decode_attn_paged(const tgvkv_problem* problem, const tgvkv_opts* opts, void* k_pool,
+                                     void* v_pool, int64_t n_pages, int32_t page_size, const int32_t* block_table,
+                                     int32_t max_pages, const int32_t* budgets, int32_t decode_reserve,
+                                     const int32_t* steps, const void* q, const void* k_new, const void* v_new,
+                                     float* out, void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Workspace bytes needed by tgvkv_score (which = TGVKV_CALL_SCORE) or
- * tgvkv_decode_attn (TGVKV_CALL_DECODE); 0 for an invalid problem. */
+ * tgvkv_decode_attn / tgvkv_decode_attn_paged (TGVKV_CALL_DECODE); 0 for an invalid problem. */
 size_t tgvkv_workspace_size(const tgvkv_problem* problem, const tgvkv_opts* opts, int32_t which);
 
 /* Static, NUL-terminated description of a status code. */

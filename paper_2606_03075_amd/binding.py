@@ -23,6 +23,7 @@ SCORE_LSE_IN = 16  # lse holds the text rows' normalisers from the caller's pref
 CALL_SCORE, CALL_DECODE = 0, 1
 
 EXPORTS = ("tgvkv_score", "tgvkv_budget", "tgvkv_select", "tgvkv_compact", "tgvkv_decode_attn",
+           "tgvkv_page_plan", "tgvkv_page_table", "tgvkv_compact_paged", "tgvkv_decode_attn_paged",
            "tgvkv_workspace_size", "tgvkv_status_string", "tgvkv_abi_version")
 
 
@@ -64,12 +65,18 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.tgvkv_select.argtypes = [P, O, vp, vp, vp, vp, vp, vp]
     lib.tgvkv_compact.argtypes = [P, O, vp, vp, vp, vp, vp, vp, i64, i32, vp, vp, vp]
     lib.tgvkv_decode_attn.argtypes = [P, O, vp, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, sz, vp]
+    lib.tgvkv_page_plan.argtypes = [P, O, i64, i32, i32, vp, vp]
+    lib.tgvkv_page_table.argtypes = [P, O, vp, i64, i32, i32, vp, i64, vp, i32, vp, vp]
+    lib.tgvkv_compact_paged.argtypes = [P, O, vp, vp, vp, vp, vp, i64, vp, i32, i32, vp, vp, i64, vp]
+    lib.tgvkv_decode_attn_paged.argtypes = [P, O, vp, vp, i64, i32, vp, i32, vp, i32, vp, vp, vp, vp, vp, vp, sz,
+                                            vp]
     lib.tgvkv_workspace_size.argtypes = [P, O, i32]
     lib.tgvkv_workspace_size.restype = sz
     lib.tgvkv_status_string.argtypes = [ctypes.c_int]
     lib.tgvkv_status_string.restype = ctypes.c_char_p
     lib.tgvkv_abi_version.argtypes = []
     for name in ("tgvkv_score", "tgvkv_budget", "tgvkv_select", "tgvkv_compact", "tgvkv_decode_attn",
+                 "tgvkv_page_plan", "tgvkv_page_table", "tgvkv_compact_paged", "tgvkv_decode_attn_paged",
                  "tgvkv_abi_version"):
         getattr(lib, name).restype = ctypes.c_int32
     if path is None:
@@ -240,6 +247,77 @@ def tgvkv_decode_attn(problem, opts, kc, vc, budgets, seg_offsets, decode_reserv
     _check("tgvkv_decode_attn", st)
 
 
+# --------------------------------------------------------------------------- paged cache
+def page_plan(problem, opts, total_budget, decode_reserve, page_size):
+    """(max_pages, pool_pages): table width and pool-page bound of a batch (host only)."""
+    mp, pool = ctypes.c_int32(0), ctypes.c_int64(0)
+    st = load_library().tgvkv_page_plan(ctypes.byref(problem), _opts_ref(opts), int(total_budget),
+                                        int(decode_reserve), int(page_size), ctypes.byref(mp), ctypes.byref(pool))
+    _check("tgvkv_page_plan", st)
+    return int(mp.value), int(pool.value)
+
+
+def _table_width(block_table, problem) -> int:
+    if block_table is None or block_table.dim() != 2 or block_table.shape[0] != problem.batch * problem.layers:
+        raise ValueError("block_table must be a [batch * layers, max_pages] tensor")
+    return int(block_table.shape[1])
+
+
+def _pool_pages(k_pool, v_pool, problem, page_size) -> int:
+    """n_pages of a pool, after checking both pools are [n_pages, heads_kv, page_size, head_dim]."""
+    if k_pool is None or v_pool is None or k_pool.shape != v_pool.shape or k_pool.dim() != 4 or \
+            tuple(k_pool.shape[1:]) != (problem.heads_kv, int(page_size), problem.head_dim):
+        raise ValueError("k_pool and v_pool must both be [n_pages, heads_kv, page_size, head_dim]")
+    return int(k_pool.shape[0])
+
+
+def tgvkv_page_table(problem, opts, budgets, total_budget, decode_reserve, page_size, free_pages, block_table,
+                     pages_used, stream=None):
+    import torch
+    st = load_library().tgvkv_page_table(ctypes.byref(problem), _opts_ref(opts),
+                                         _ptr(budgets, (torch.int32,), "budgets"), int(total_budget),
+                                         int(decode_reserve), int(page_size),
+                                         _ptr(free_pages, (torch.int32,), "free_pages"), int(free_pages.numel()),
+                                         _ptr(block_table, (torch.int32,), "block_table"),
+                                         _table_width(block_table, problem),
+                                         _ptr(pages_used, (torch.int64,), "pages_used"),
+                                         _stream(stream))
+    _check("tgvkv_page_table", st)
+
+
+def tgvkv_compact_paged(problem, opts, k, v, idx, budgets, idx_offsets, total_budget, block_table, page_size,
+                        k_pool, v_pool, stream=None):
+    import torch
+    n_pages = _pool_pages(k_pool, v_pool, problem, page_size)
+    st = load_library().tgvkv_compact_paged(ctypes.byref(problem), _opts_ref(opts), _ptr(k, _bf16(), "k"),
+                                            _ptr(v, _bf16(), "v"), _ptr(idx, (torch.int32,), "idx"),
+                                            _ptr(budgets, (torch.int32,), "budgets"),
+                                            _ptr(idx_offsets, (torch.int64,), "idx_offsets"), int(total_budget),
+                                            _ptr(block_table, (torch.int32,), "block_table"),
+                                            _table_width(block_table, problem), int(page_size),
+                                            _ptr(k_pool, _bf16(), "k_pool"), _ptr(v_pool, _bf16(), "v_pool"),
+                                            n_pages, _stream(stream))
+    _check("tgvkv_compact_paged", st)
+
+
+def tgvkv_decode_attn_paged(problem, opts, k_pool, v_pool, page_size, block_table, budgets, decode_reserve, steps,
+                            q, k_new, v_new, out, workspace=None, stream=None):
+    import torch
+    n_pages = _pool_pages(k_pool, v_pool, problem, page_size)
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    st = load_library().tgvkv_decode_attn_paged(ctypes.byref(problem), _opts_ref(opts),
+                                                _ptr(k_pool, _bf16(), "k_pool"), _ptr(v_pool, _bf16(), "v_pool"),
+                                                n_pages, int(page_size),
+                                                _ptr(block_table, (torch.int32,), "block_table"),
+                                                _table_width(block_table, problem),
+                                                _ptr(budgets, (torch.int32,), "budgets"),
+                                                int(decode_reserve), _ptr(steps, (torch.int32,), "steps"),
+                                                _ptr(q, _bf16(), "q"), _ptr(k_new, _bf16(), "k_new"),
+                                                _ptr(v_new, _bf16(), "v_new"), _ptr(out, _f32(), "out"),
+                                                _ptr(workspace, None, "workspace"), ws_bytes, _stream(stream))
+    _check("tgvkv_decode_attn_paged", st)
+
+
 # --------------------------------------------------------------------------- whole-pass helpers
 class EvictionBuffers:
     """Device buffers of one eviction pass plus decode, allocated once for a problem.
@@ -361,3 +439,52 @@ class EvictionBuffers:
         tgvkv_decode_attn(self.problem, self.opts, self.kc, self.vc, self.budgets, self.seg_offsets,
                           self.decode_reserve, step, q, k_new, v_new, self.out, self.ws_decode, stream)
         return self.out
+
+
+class PagedPool:
+    """A pool of cache pages shared by the sequences in service (continuous batching).
+
+    Owns k_pool / v_pool [n_pages][heads_kv][page_size][head_dim] and the list of free
+    page ids.  admit() places a batch evicted into EvictionBuffers in the pool (page
+    table, then paged compaction); release() returns a finished sequence's pages.
+    Page assignment and every copy run in the library; this class only keeps the
+    free list, which needs the number of pages a batch took (one device read).
+    """
+
+    def __init__(self, heads_kv: int, head_dim: int, page_size: int, n_pages: int, device="cuda"):
+        import torch
+        self.page_size, self.n_pages = int(page_size), int(n_pages)
+        self.k_pool = torch.empty((n_pages, heads_kv, page_size, head_dim), dtype=torch.bfloat16, device=device)
+        self.v_pool = torch.empty_like(self.k_pool)
+        self.free = list(range(n_pages))
+        self.device = device
+
+    def admit(self, buf: "EvictionBuffers", k, v, stream=None):
+        """Page table [B*L, max_pages] of an evicted batch, with its rows compacted into the pool."""
+        import torch
+        p, o = buf.problem, buf.opts
+        width, pool = page_plan(p, o, buf.total_budget, buf.decode_reserve, self.page_size)
+        if pool > len(self.free):
+            raise MemoryError(f"pool has {len(self.free)} free pages, the batch may need {pool}")
+        ids = torch.tensor(self.free[:pool], dtype=torch.int32, device=self.device)
+        table = torch.empty((p.batch * p.layers, width), dtype=torch.int32, device=self.device)
+        used = torch.zeros((1,), dtype=torch.int64, device=self.device)
+        tgvkv_page_table(p, o, buf.budgets, buf.total_budget, buf.decode_reserve, self.page_size, ids, table, used,
+                         stream)
+        tgvkv_compact_paged(p, o, k, v, buf.idx, buf.budgets, buf.idx_offsets, buf.total_budget, table,
+                            self.page_size, self.k_pool, self.v_pool, stream)
+        n = int(used.item()) if p.batch > 0 else 0
+        del self.free[:n]
+        return table
+
+    def release(self, table_rows):
+        """Return the pages of finished sequences' table rows to the free list."""
+        ids = table_rows.reshape(-1).cpu().tolist()
+        self.free.extend(int(i) for i in ids if i >= 0)
+
+    def decode(self, problem, opts, table, budgets, decode_reserve, steps, q, k_new, v_new, out, workspace,
+               stream=None):
+        """One decode step of a continuous batch whose sequence b is at step steps[b]."""
+        tgvkv_decode_attn_paged(problem, opts, self.k_pool, self.v_pool, self.page_size, table, budgets,
+                                decode_reserve, steps, q, k_new, v_new, out, workspace, stream)
+        return out

@@ -3,6 +3,7 @@
 // Every entry point checks its arguments before touching the HIP runtime, so an
 // invalid call returns a negative status and enqueues nothing.
 #include <algorithm>
+#include <climits>
 #include <cmath>
 #include <cstdint>
 #include <cstdlib>
@@ -152,6 +153,33 @@ size_t decode_workspace_bytes(const Shape& s) {
     const int ns = tgvkv::decode_splits(s);
     if (ns <= 1) return 0;
     return align_up(sizeof(float) * (size_t)s.B * s.L * s.H * ns * (s.D + 2));
+}
+
+// Paged cache limits: page_size and max_pages bound the LDS copy of a segment's page ids.
+constexpr int32_t kMaxPageSize = 4096;
+constexpr int32_t kMaxTablePages = 4096;
+
+// log2(page_size), or -1 unless page_size is a power of two in [1, kMaxPageSize].
+int32_t page_shift(int32_t page_size) {
+    if (page_size < 1 || page_size > kMaxPageSize || (page_size & (page_size - 1)) != 0) return -1;
+    int32_t sh = 0;
+    while ((1 << sh) < page_size) ++sh;
+    return sh;
+}
+
+// Largest b_l a layer can get for this total_budget (every b_l <= N and sum_l b_l = total).
+int64_t max_layer_budget(const Shape& s, int64_t total_budget) {
+    if (s.vision_only) return always_kept(s) + std::min<int64_t>(s.Nv - forced_vision_count(s), total_budget);
+    return std::min<int64_t>(s.N, total_budget);
+}
+
+// Table width and pool pages (upper bound) of a batch: sum_i ceil((b_i + R) / P) <=
+// (sum_i b_i + B*L*(R + P - 1)) / P.
+void page_plan(const Shape& s, int64_t total_budget, int32_t reserve, int32_t page_size, int64_t* width,
+               int64_t* pool) {
+    *width = (max_layer_budget(s, total_budget) + reserve + page_size - 1) / page_size;
+    *pool = ((int64_t)s.B * kept_per_sequence(s, total_budget) + (int64_t)s.B * s.L * (reserve + page_size - 1)) /
+            page_size;
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -336,4 +364,94 @@ tgvkv_status tgvkv_decode_attn(const tgvkv_problem* problem, const tgvkv_opts* o
                                            out, static_cast<float*>(workspace), stream));
 }
 
-}  // extern "C"
+tgvkv_status tgvkv_page_plan(const tgvkv_problem* problem, const tgvkv_opts* opts, int64_t total_budget,
+                             int32_t decode_reserve, int32_t page_size, int32_t* max_pages_out,
+                             int64_t* pool_pages_out) {
+    Shape s;
+    tgvkv_status st = make_shape(problem, opts, &s);
+    if (st != TGVKV_OK) return st;
+    if (max_pages_out == nullptr || pool_pages_out == nullptr) return TGVKV_E_INVAL;
+    if (decode_reserve < 0 || total_budget < 0 || page_shift(page_size) < 0) return TGVKV_E_INVAL;
+    if (total_budget > budget_capacity(s)) return TGVKV_E_CAPACITY;
+    int64_t width, pool;
+    page_plan(s, total_budget, decode_reserve, page_size, &width, &pool);
+    if (width > kMaxTablePages) return TGVKV_E_UNSUPPORTED;
+    *max_pages_out = (int32_t)std::max<int64_t>(width, 1);
+    *pool_pages_out = pool;
+    return TGVKV_OK;
+}
+
+tgvkv_status tgvkv_page_table(const tgvkv_problem* problem, const tgvkv_opts* opts, const int32_t* budgets,
+                              int64_t total_budget, int32_t decode_reserve, int32_t page_size,
+                              const int32_t* free_pages, int64_t n_free, int32_t* block_table, int32_t max_pages,
+                              int64_t* pages_used, hipStream_t stream) {
+    Shape s;
+    tgvkv_status st = make_shape(problem, opts, &s);
+    if (st != TGVKV_OK) return st;
+    const int32_t sh = page_shift(page_size);
+    if (decode_reserve < 0 || total_budget < 0 || sh < 0 || n_free < 0 || max_pages < 1) return TGVKV_E_INVAL;
+    if (max_pages > kMaxTablePages) return TGVKV_E_UNSUPPORTED;
+    if (total_budget > budget_capacity(s)) return TGVKV_E_CAPACITY;
+    if (pages_used == nullptr) return TGVKV_E_INVAL;
+    if (s.B > 0 && (budgets == nullptr || block_table == nullptr || (n_free > 0 && free_pages == nullptr)))
+        return TGVKV_E_INVAL;
+    int64_t width, pool;
+    page_plan(s, total_budget, decode_reserve, page_size, &width, &pool);
+    if (width > max_pages || pool > n_free) return TGVKV_E_CAPACITY;
+    if (s.B == 0) return TGVKV_OK;
+    return hip_status(tgvkv::launch_page_table(s, budgets, decode_reserve, sh, free_pages, n_free, block_table,
+                                               max_pages, pages_used, stream));
+}
+
+tgvkv_status tgvkv_compact_paged(const tgvkv_problem* problem, const tgvkv_opts* opts, const void* k, const void* v,
+                                 const int32_t* idx, const int32_t* budgets, const int64_t* idx_offsets,
+                                 int64_t total_budget, const int32_t* block_table, int32_t max_pages,
+                                 int32_t page_size, void* k_pool, void* v_pool, int64_t n_pages,
+                                 hipStream_t stream) {
+    Shape s;
+    tgvkv_status st = make_shape(problem, opts, &s);
+    if (st != TGVKV_OK) return st;
+    const int32_t sh = page_shift(page_size);
+    if (total_budget < 0 || sh < 0 || max_pages < 1 || n_pages < 1) return TGVKV_E_INVAL;
+    if (max_pages > kMaxTablePages || n_pages > INT32_MAX) return TGVKV_E_UNSUPPORTED;
+    if (total_budget > budget_capacity(s)) return TGVKV_E_CAPACITY;
+    if ((max_layer_budget(s, total_budget) + page_size - 1) / page_size > max_pages) return TGVKV_E_CAPACITY;
+    const int64_t kept = kept_per_sequence(s, total_budget);
+    if (s.B == 0 || kept == 0) return TGVKV_OK;
+    if (k == nullptr || v == nullptr || idx == nullptr || budgets == nullptr || idx_offsets == nullptr ||
+        block_table == nullptr || k_pool == nullptr || v_pool == nullptr)
+        return TGVKV_E_INVAL;
+    if (!aligned16(k) || !aligned16(v) || !aligned16(k_pool) || !aligned16(v_pool)) return TGVKV_E_INVAL;
+    if ((int64_t)s.B * s.L * 16 > kMaxBlocks || s.Hkv > 65535) return TGVKV_E_UNSUPPORTED;
+    return hip_status(tgvkv::launch_compact_paged(
+        s, static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), idx, budgets, idx_offsets,
+        (int64_t)s.B * kept, block_table, max_pages, sh, n_pages, static_cast<uint16_t*>(k_pool),
+        static_cast<uint16_t*>(v_pool), stream));
+}
+
+tgvkv_status tgvkv_decode_attn_paged(const tgvkv_problem* problem, const tgvkv_opts* opts, void* k_pool,
+                                     void* v_pool, int64_t n_pages, int32_t page_size, const int32_t* block_table,
+                                     int32_t max_pages, const int32_t* budgets, int32_t decode_reserve,
+                                     const int32_t* steps, const void* q, const void* k_new, const void* v_new,
+                                     float* out, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    Shape s;
+    tgvkv_status st = make_shape(problem, opts, &s);
+    if (st != TGVKV_OK) return st;
+    const int32_t sh = page_shift(page_size);
+    if (decode_reserve < 0 || sh < 0 || max_pages < 1 || n_pages < 1) return TGVKV_E_INVAL;
+    if (max_pages > kMaxTablePages || n_pages > INT32_MAX) return TGVKV_E_UNSUPPORTED;
+    if (s.B == 0) return TGVKV_OK;
+    if (k_pool == nullptr || v_pool == nullptr || block_table == nullptr || budgets == nullptr || steps == nullptr ||
+        q == nullptr || k_new == nullptr || v_new == nullptr || out == nullptr)
+        return TGVKV_E_INVAL;
+    if (!aligned16(k_pool) || !aligned16(v_pool) || !aligned16(q) || !aligned16(k_new) || !aligned16(v_new))
+        return TGVKV_E_INVAL;
+    const size_t need = decode_workspace_bytes(s);
+    if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return TGVKV_E_WORKSPACE;
+    return hip_status(tgvkv::launch_decode_paged(
+        s, static_cast<uint16_t*>(k_pool), static_cast<uint16_t*>(v_pool), n_pages, block_table, max_pages, sh,
+        budgets, decode_reserve, steps, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_new),
+        static_cast<const uint16_t*>(v_new), out, static_cast<float*>(workspace), stream));
+}
+
+}  // extern "C\"

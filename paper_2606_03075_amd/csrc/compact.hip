@@ -9,9 +9,13 @@
 // no search.  A row of head_dim bf16 is moved by head_dim/8 lanes with 16-byte
 // accesses (non-temporal loads); each thread keeps kPasses rows in flight, and
 // the positions of the next rows are fetched while the current ones are moved.
+// The destination is either a contiguous segment per (sequence, layer) or the
+// pages that a block table names (paged cache); only the row addressing differs.
 #include <algorithm>
+#include <climits>
 
 #include "tgvkv_device.h"
+#include "tgvkv_rows.h"
 #include "tgvkv_shape.h"
 
 namespace tgvkv {
@@ -20,15 +24,14 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kPasses = 8;
 
-template <int D>
-__global__ __launch_bounds__(kThreads) void compact_kernel(Shape s, const uint16_t* __restrict__ k,
+template <int D, class Rows>
+__global__ __launch_bounds__(kThreads) void compact_kernel(Shape s, Rows rows, const uint16_t* __restrict__ k,
                                                            const uint16_t* __restrict__ v,
                                                            const int32_t* __restrict__ idx,
                                                            const int32_t* __restrict__ budgets,
-                                                           const int64_t* __restrict__ idx_off,
-                                                           const int64_t* __restrict__ seg_off, int reserve,
-                                                           int nsplit, uint16_t* __restrict__ kc,
-                                                           uint16_t* __restrict__ vc) {
+                                                           const int64_t* __restrict__ idx_off, int nsplit,
+                                                           uint16_t* __restrict__ kc, uint16_t* __restrict__ vc) {
+    extern __shared__ int lds_pages[];  // paged layout: the unit's page ids
     constexpr int CPR = D / 8;             // lanes per row
     constexpr int RPP = kThreads / CPR;    // rows per pass
     constexpr int ROWS = RPP * kPasses;    // rows per iteration
@@ -37,12 +40,12 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(Shape s, const uint16
     const int bl = blockIdx.x / nsplit;
     const int bsz = budgets[bl];
     const long long ioff = idx_off[bl] + (s.head_mode == 0 ? 0 : (long long)kvh * bsz);
-    const long long soff = seg_off[bl];
     const int per = (bsz + nsplit - 1) / nsplit;
     const int r_beg = min(split * per, bsz), r_end = min(r_beg + per, bsz);
     const int cc = threadIdx.x % CPR, rl = threadIdx.x / CPR;
     const size_t src0 = ((size_t)bl * s.Hkv + kvh) * (size_t)s.N * D + cc * 8;
-    const size_t dst0 = ((size_t)soff * s.Hkv + (size_t)kvh * (bsz + reserve)) * D + cc * 8;
+    rows.init(s, bl, kvh, bsz, bsz, lds_pages);
+    __syncthreads();
 
     // positions come from tgvkv_select; clamp so a corrupt index can never read outside the slice
     int pos[kPasses];
@@ -70,7 +73,7 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(Shape s, const uint16
 #pragma unroll
         for (int i = 0; i < kPasses; ++i) {
             if (cur[i] >= 0) {
-                const size_t dst = dst0 + (size_t)(r0 + i * RPP + rl) * D;
+                const size_t dst = rows.row(r0 + i * RPP + rl) + cc * 8;
                 store16(kc + dst, kr[i]);
                 store16(vc + dst, vr[i]);
             }
@@ -88,21 +91,42 @@ int compact_splits(const Shape& s, int64_t rows_total) {
     return (int)std::max<long long>(1, std::min<long long>(n, 16));
 }
 
+template <int D, class Rows>
+hipError_t launch_compact_d(const Shape& s, const Rows& rows, size_t lds, const uint16_t* k, const uint16_t* v,
+                            const int32_t* idx, const int32_t* budgets, const int64_t* idx_off, int64_t rows_total,
+                            uint16_t* kc, uint16_t* vc, hipStream_t st) {
+    const int nsplit = compact_splits(s, rows_total);
+    dim3 grid((unsigned)((long long)s.B * s.L * nsplit), (unsigned)s.Hkv);
+    hipLaunchKernelGGL((compact_kernel<D, Rows>), grid, dim3(kThreads), lds, st, s, rows, k, v, idx, budgets, idx_off,
+                       nsplit, kc, vc);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_compact(const Shape& s, const uint16_t* k, const uint16_t* v, const int32_t* idx,
                           const int32_t* budgets, const int64_t* idx_off, const int64_t* seg_off, int32_t reserve,
                           int64_t rows_total, uint16_t* kc, uint16_t* vc, hipStream_t st) {
     if (rows_total <= 0 || s.B * s.L == 0) return hipSuccess;
-    const int nsplit = compact_splits(s, rows_total);
-    dim3 grid((unsigned)((long long)s.B * s.L * nsplit), (unsigned)s.Hkv);
     if (s.D == 128)
-        hipLaunchKernelGGL(compact_kernel<128>, grid, dim3(kThreads), 0, st, s, k, v, idx, budgets, idx_off, seg_off,
-                           reserve, nsplit, kc, vc);
-    else
-        hipLaunchKernelGGL(compact_kernel<64>, grid, dim3(kThreads), 0, st, s, k, v, idx, budgets, idx_off, seg_off,
-                           reserve, nsplit, kc, vc);
-    return hipGetLastError();
+        return launch_compact_d<128>(s, ContigRows<128>{seg_off, reserve, 0}, 0, k, v, idx, budgets, idx_off,
+                                     rows_total, kc, vc, st);
+    return launch_compact_d<64>(s, ContigRows<64>{seg_off, reserve, 0}, 0, k, v, idx, budgets, idx_off, rows_total,
+                                kc, vc, st);
+}
+
+hipError_t launch_compact_paged(const Shape& s, const uint16_t* k, const uint16_t* v, const int32_t* idx,
+                                const int32_t* budgets, const int64_t* idx_off, int64_t rows_total,
+                                const int32_t* block_table, int32_t max_pages, int32_t page_shift, int64_t n_pages,
+                                uint16_t* k_pool, uint16_t* v_pool, hipStream_t st) {
+    if (rows_total <= 0 || s.B * s.L == 0) return hipSuccess;
+    const int np = (int)std::min<int64_t>(n_pages, INT32_MAX);
+    const size_t lds = PagedRows<128>::lds_bytes(max_pages);
+    if (s.D == 128)
+        return launch_compact_d<128>(s, PagedRows<128>{block_table, max_pages, page_shift, np, 0, 0, nullptr}, lds, k,
+                                     v, idx, budgets, idx_off, rows_total, k_pool, v_pool, st);
+    return launch_compact_d<64>(s, PagedRows<64>{block_table, max_pages, page_shift, np, 0, 0, nullptr}, lds, k, v,
+                                idx, budgets, idx_off, rows_total, k_pool, v_pool, st);
 }
 
 }  // namespace tgvkv

@@ -15,8 +15,15 @@
 //     too small to fill the GPU the token range is split and a second kernel
 //     combines the partial (max, sum, weighted sum) triples.
 // The step's new token is read from the k_new / v_new inputs (the cache slot it
-// is written to is not re-read in the same launch).
+// is written to is not re-read in the same launch).  The cache is either one
+// contiguous segment per (sequence, layer) or fixed-size pages found through a
+// block table (staged in LDS); with per-sequence steps (continuous batching) a
+// sequence whose step is outside [0, reserve) is skipped.
+#include <algorithm>
+#include <climits>
+
 #include "tgvkv_device.h"
+#include "tgvkv_rows.h"
 #include "tgvkv_shape.h"
 
 namespace tgvkv {
@@ -32,10 +39,11 @@ __device__ __forceinline__ void unpack8(u32x4 r, float (&f)[8]) {
     }
 }
 
-template <int D, int GMAX>
-__global__ __launch_bounds__(kThreads) void decode_kernel(Shape s, uint16_t* __restrict__ kc, uint16_t* __restrict__ vc,
-                                                          const int32_t* __restrict__ budgets,
-                                                          const int64_t* __restrict__ seg_off, int reserve, int step,
+template <int D, int GMAX, class Rows>
+__global__ __launch_bounds__(kThreads) void decode_kernel(Shape s, Rows rows, uint16_t* __restrict__ kc,
+                                                          uint16_t* __restrict__ vc,
+                                                          const int32_t* __restrict__ budgets, int reserve, int step,
+                                                          const int32_t* __restrict__ steps,
                                                           const uint16_t* __restrict__ q,
                                                           const uint16_t* __restrict__ k_new,
                                                           const uint16_t* __restrict__ v_new, float* __restrict__ out,
@@ -46,6 +54,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(Shape s, uint16_t* __r
     constexpr int kUnroll = GMAX <= 2 ? 8 : 4;  // tokens in flight per lane group
     __shared__ float wm[4][GMAX], wl[4][GMAX];
     __shared__ float wacc[4][GMAX][D];
+    extern __shared__ int lds_pages[];  // paged layout: the unit's page ids
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int sub = lane % LPR;
@@ -57,16 +66,20 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(Shape s, uint16_t* __r
     const int bl = bid / s.Hkv;
     const int G = s.G;
 
+    // continuous batching: each sequence at its own step, outside [0, reserve) = not decoding
+    const int st = steps != nullptr ? steps[bl / s.L] : step;
+    if (st < 0 || st >= reserve) return;  // uniform over the workgroup, before any barrier
     const int bsz = budgets[bl];
-    const int cap = bsz + reserve;
-    const int len = bsz + step + 1;
-    const size_t seg = ((size_t)seg_off[bl] * s.Hkv + (size_t)kvh * cap) * D;
+    const int len = bsz + st + 1;
+    rows.init(s, bl, kvh, bsz, len, lds_pages);
+    __syncthreads();
     const uint16_t* knew = k_new + ((size_t)bl * s.Hkv + kvh) * D;
     const uint16_t* vnew = v_new + ((size_t)bl * s.Hkv + kvh) * D;
 
     if (split == 0 && tid < LPR) {
-        store16(kc + seg + (size_t)(bsz + step) * D + tid * 8, load16(knew + tid * 8));
-        store16(vc + seg + (size_t)(bsz + step) * D + tid * 8, load16(vnew + tid * 8));
+        const size_t r = rows.row(bsz + st);
+        store16(kc + r + tid * 8, load16(knew + tid * 8));
+        store16(vc + r + tid * 8, load16(vnew + tid * 8));
     }
 
     float qv[GMAX][8];
@@ -102,8 +115,9 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(Shape s, uint16_t* __r
             const int n = n0 + u * NGRP;
             ok[u] = n < t1;
             const bool fresh = n >= len - 1 || !ok[u];
-            const uint16_t* kp = fresh ? knew : kc + seg + (size_t)n * D;
-            const uint16_t* vp = fresh ? vnew : vc + seg + (size_t)n * D;
+            const size_t r = fresh ? 0 : rows.row(n);
+            const uint16_t* kp = fresh ? knew : kc + r;
+            const uint16_t* vp = fresh ? vnew : vc + r;
             kr[u] = load16_stream(kp + sub * 8);
             vr[u] = load16_stream(vp + sub * 8);
         }
@@ -202,8 +216,13 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(Shape s, uint16_t* __r
 
 template <int D>
 __global__ __launch_bounds__(D) void decode_combine_kernel(Shape s, const float* __restrict__ ws_part, int nsplit,
-                                                           float* __restrict__ out) {
+                                                           float* __restrict__ out, const int32_t* __restrict__ steps,
+                                                           int reserve) {
     const size_t bh = blockIdx.x;
+    if (steps != nullptr) {
+        const int st = steps[(int)(bh / ((size_t)s.L * s.H))];
+        if (st < 0 || st >= reserve) return;  // this sequence is not decoding
+    }
     const int dd = threadIdx.x;
     const float* p = ws_part + bh * nsplit * (size_t)(D + 2);
     float M = kNegInf;
@@ -217,14 +236,15 @@ __global__ __launch_bounds__(D) void decode_combine_kernel(Shape s, const float*
     out[bh * D + dd] = num / den;
 }
 
-template <int D>
-hipError_t launch_decode_d(const Shape& s, uint16_t* kc, uint16_t* vc, const int32_t* budgets, const int64_t* seg_off,
-                           int32_t reserve, int32_t step, const uint16_t* q, const uint16_t* k_new,
-                           const uint16_t* v_new, float* out, float* ws_part, int nsplit, hipStream_t st) {
+template <int D, class Rows>
+hipError_t launch_decode_d(const Shape& s, const Rows& rows, size_t lds_bytes, uint16_t* kc, uint16_t* vc,
+                           const int32_t* budgets, int32_t reserve, int32_t step, const int32_t* steps,
+                           const uint16_t* q, const uint16_t* k_new, const uint16_t* v_new, float* out, float* ws_part,
+                           int nsplit, hipStream_t st) {
     dim3 grid((unsigned)((long long)s.B * s.L * s.Hkv * nsplit)), block(kThreads);
-#define TGVKV_DECODE_LAUNCH(GM)                                                                                     \
-    hipLaunchKernelGGL((decode_kernel<D, GM>), grid, block, 0, st, s, kc, vc, budgets, seg_off, reserve, step, q, \
-                       k_new, v_new, out, ws_part, nsplit)
+#define TGVKV_DECODE_LAUNCH(GM)                                                                                   \
+    hipLaunchKernelGGL((decode_kernel<D, GM, Rows>), grid, block, lds_bytes, st, s, rows, kc, vc, budgets, reserve, \
+                       step, steps, q, k_new, v_new, out, ws_part, nsplit)
     if (s.G <= 1) TGVKV_DECODE_LAUNCH(1);
     else if (s.G <= 2) TGVKV_DECODE_LAUNCH(2);
     else if (s.G <= 4) TGVKV_DECODE_LAUNCH(4);
@@ -234,7 +254,7 @@ hipError_t launch_decode_d(const Shape& s, uint16_t* kc, uint16_t* vc, const int
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || nsplit == 1) return e;
     hipLaunchKernelGGL(decode_combine_kernel<D>, dim3((unsigned)((long long)s.B * s.L * s.H)), dim3(D), 0, st, s,
-                       ws_part, nsplit, out);
+                       ws_part, nsplit, out, steps, reserve);
     return hipGetLastError();
 }
 
@@ -254,10 +274,33 @@ hipError_t launch_decode(const Shape& s, uint16_t* kc, uint16_t* vc, const int32
                          float* out, float* ws_part, hipStream_t st) {
     if ((long long)s.B * s.L == 0) return hipSuccess;
     const int nsplit = decode_splits(s);
-    if (s.D == 128)
-        return launch_decode_d<128>(s, kc, vc, budgets, seg_off, reserve, step, q, k_new, v_new, out, ws_part, nsplit,
-                                    st);
-    return launch_decode_d<64>(s, kc, vc, budgets, seg_off, reserve, step, q, k_new, v_new, out, ws_part, nsplit, st);
+    if (s.D == 128) {
+        ContigRows<128> rows{seg_off, reserve, 0};
+        return launch_decode_d<128>(s, rows, 0, kc, vc, budgets, reserve, step, nullptr, q, k_new, v_new, out,
+                                    ws_part, nsplit, st);
+    }
+    ContigRows<64> rows{seg_off, reserve, 0};
+    return launch_decode_d<64>(s, rows, 0, kc, vc, budgets, reserve, step, nullptr, q, k_new, v_new, out, ws_part,
+                               nsplit, st);
+}
+
+hipError_t launch_decode_paged(const Shape& s, uint16_t* k_pool, uint16_t* v_pool, int64_t n_pages,
+                               const int32_t* block_table, int32_t max_pages, int32_t page_shift,
+                               const int32_t* budgets, int32_t reserve, const int32_t* steps, const uint16_t* q,
+                               const uint16_t* k_new, const uint16_t* v_new, float* out, float* ws_part,
+                               hipStream_t st) {
+    if ((long long)s.B * s.L == 0) return hipSuccess;
+    const int nsplit = decode_splits(s);
+    const size_t lds = PagedRows<128>::lds_bytes(max_pages);
+    const int np = (int)std::min<int64_t>(n_pages, INT32_MAX);
+    if (s.D == 128) {
+        PagedRows<128> rows{block_table, max_pages, page_shift, np, 0, 0, nullptr};
+        return launch_decode_d<128>(s, rows, lds, k_pool, v_pool, budgets, reserve, 0, steps, q, k_new, v_new, out,
+                                    ws_part, nsplit, st);
+    }
+    PagedRows<64> rows{block_table, max_pages, page_shift, np, 0, 0, nullptr};
+    return launch_decode_d<64>(s, rows, lds, k_pool, v_pool, budgets, reserve, 0, steps, q, k_new, v_new, out,
+                               ws_part, nsplit, st);
 }
 
 }  // namespace tgvkv

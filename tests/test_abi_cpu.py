@@ -44,7 +44,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(bd.EXPORTS) <= set(names) and len(names) == len(bd.EXPORTS), names
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.tgvkv_abi_version() == 3
+    assert lib.tgvkv_abi_version() == 4
     for st in (0, -1, -2, -3, -4, -5):
         assert lib.tgvkv_status_string(st)
     assert lib.tgvkv_status_string(7) == b"unknown status"
@@ -129,6 +129,93 @@ def test_validation_before_any_launch(lib):
     assert lib.tgvkv_decode_attn(ok, None, fake, fake, fake, fake, 4, 0, fake, fake, fake, fake, None, 0, s) == -3
 
 
+def _plan(problem, opts, total, reserve, page):
+    return bd.page_plan(problem, opts, total, reserve, page)
+
+
+def _splits(total, layers, cap):
+    """Every way of writing total as layers parts in [0, cap] (tiny cases only)."""
+    if layers == 1:
+        if 0 <= total <= cap:
+            yield (total,)
+        return
+    for b in range(0, min(cap, total) + 1):
+        for rest in _splits(total - b, layers - 1, cap):
+            yield (b,) + rest
+
+
+@pytest.mark.parametrize("total,reserve,page", [(0, 0, 1), (10, 4, 8), (37, 3, 4), (96, 0, 16), (50, 9, 2),
+                                                (96, 5, 64)])
+def test_page_plan_bounds_every_budget_split(lib, total, reserve, page):
+    """The plan's width is the largest segment's page count over every budget split the
+    budget call can produce, and the pool bound covers the worst split's total."""
+    prob = P(layers=2, n_sys=3, n_vis=40, n_qst=5)  # N = 48
+    width, pool = _plan(prob, None, total, reserve, page)
+    need = lambda b: -(-(b + reserve) // page)
+    splits = list(_splits(total, 2, 48))
+    assert width == max(1, max(max(need(b) for b in sp) for sp in splits))
+    assert pool >= max(sum(need(b) for b in sp) for sp in splits)
+    assert pool <= (total + 2 * (reserve + page - 1)) // page
+
+
+def test_page_plan_vision_only(lib):
+    """Vision-only eviction keeps N_t text tokens per layer beside the vision budget."""
+    prob = P(layers=2, n_sys=3, n_vis=40, n_qst=5)
+    vo = bd.make_opts(vision_only=True)
+    width, pool = _plan(prob, vo, 10, 4, 8)
+    assert width == -(-(8 + 10 + 4) // 8)            # b_max = N_t + min(n_vis, V_tot)
+    assert pool == (2 * 8 + 10 + 2 * (4 + 7)) // 8   # K = L*N_t + V_tot
+
+
+def test_page_plan_rejects_bad_arguments(lib):
+    out_w, out_p = ctypes.c_int32(), ctypes.c_int64()
+    ok = ctypes.byref(P())
+    for page in (0, 3, 6, 8192, -4):
+        assert lib.tgvkv_page_plan(ok, None, 10, 4, page, ctypes.byref(out_w), ctypes.byref(out_p)) == -1
+    assert lib.tgvkv_page_plan(ok, None, 2 * 48 + 1, 4, 8, ctypes.byref(out_w), ctypes.byref(out_p)) == -4
+    assert lib.tgvkv_page_plan(ok, None, 10, -1, 8, ctypes.byref(out_w), ctypes.byref(out_p)) == -1
+    assert lib.tgvkv_page_plan(ok, None, 10, 4, 8, None, ctypes.byref(out_p)) == -1
+    # a segment wider than 4096 pages is beyond the LDS copy of its page ids
+    assert lib.tgvkv_page_plan(ok, None, 48, 5000, 1, ctypes.byref(out_w), ctypes.byref(out_p)) == -2
+
+
+@pytest.mark.skipif(_gpu(), reason="fake pointers are used only where no GPU exists")
+def test_paged_validation_before_any_launch(lib):
+    fake = ctypes.c_void_p(0x10000)
+    odd = ctypes.c_void_p(0x10008)
+    big = ctypes.c_size_t(1 << 40)
+    s = ctypes.c_void_p(0)
+    ok = ctypes.byref(P())
+    width, pool = _plan(P(), None, 10, 4, 8)
+    # page table: width and pool bound, page size, pointers
+    assert lib.tgvkv_page_table(ok, None, fake, 10, 4, 8, fake, pool, fake, width - 1, fake, s) == -4
+    assert lib.tgvkv_page_table(ok, None, fake, 10, 4, 8, fake, pool - 1, fake, width, fake, s) == -4
+    assert lib.tgvkv_page_table(ok, None, fake, 10, 4, 6, fake, pool, fake, width, fake, s) == -1
+    assert lib.tgvkv_page_table(ok, None, fake, 10, 4, 8, fake, pool, fake, 5000, fake, s) == -2
+    assert lib.tgvkv_page_table(ok, None, None, 10, 4, 8, fake, pool, fake, width, fake, s) == -1
+    assert lib.tgvkv_page_table(ok, None, fake, 10, 4, 8, fake, pool, fake, width, None, s) == -1
+    assert lib.tgvkv_page_table(ok, None, fake, 2 * 48 + 1, 4, 8, fake, 999, fake, 64, fake, s) == -4
+    # paged compaction: the table must hold b_max rows
+    assert lib.tgvkv_compact_paged(ok, None, fake, fake, fake, fake, fake, 10, fake, 1, 8, fake, fake, 64, s) == -4
+    assert lib.tgvkv_compact_paged(ok, None, fake, fake, fake, fake, fake, 10, fake, 2, 8, fake, fake, 0, s) == -1
+    assert lib.tgvkv_compact_paged(ok, None, fake, fake, fake, fake, fake, 10, fake, 2, 8, fake, odd, 64, s) == -1
+    assert lib.tgvkv_compact_paged(ok, None, fake, fake, fake, fake, fake, 10, None, 2, 8, fake, fake, 64, s) == -1
+    assert lib.tgvkv_compact_paged(ok, None, fake, fake, fake, fake, fake, 10, fake, 2, 5, fake, fake, 64, s) == -1
+    assert lib.tgvkv_compact_paged(ok, None, fake, fake, fake, fake, fake, 10, fake, 2, 8, fake, fake, 1 << 31,
+                                   s) == -2
+    # paged decode: steps are required, workspace as for contiguous decode
+    assert lib.tgvkv_decode_attn_paged(ok, None, fake, fake, 64, 8, fake, 2, fake, 4, None, fake, fake, fake, fake,
+                                       fake, big, s) == -1
+    assert lib.tgvkv_decode_attn_paged(ok, None, fake, fake, 64, 8, fake, 2, fake, 4, fake, fake, fake, fake, fake,
+                                       None, 0, s) == -3
+    assert lib.tgvkv_decode_attn_paged(ok, None, fake, fake, 64, 12, fake, 2, fake, 4, fake, fake, fake, fake, fake,
+                                       fake, big, s) == -1
+    assert lib.tgvkv_decode_attn_paged(ok, None, odd, fake, 64, 8, fake, 2, fake, 4, fake, fake, fake, fake, fake,
+                                       fake, big, s) == -1
+    assert lib.tgvkv_decode_attn_paged(ok, None, fake, fake, 64, 8, fake, 0, fake, 4, fake, fake, fake, fake, fake,
+                                       fake, big, s) == -1
+
+
 def test_empty_batch_is_a_no_op(lib):
     z = ctypes.byref(P(batch=0))
     s = ctypes.c_void_p(0)
@@ -138,6 +225,11 @@ def test_empty_batch_is_a_no_op(lib):
     assert lib.tgvkv_select(z, None, None, None, None, None, None, s) == 0
     assert lib.tgvkv_compact(z, None, None, None, None, None, None, None, 5, 0, None, None, s) == 0
     assert lib.tgvkv_decode_attn(z, None, None, None, None, None, 2, 0, None, None, None, None, None, 0, s) == 0
+    used = ctypes.c_void_p(0x10000)
+    assert lib.tgvkv_page_table(z, None, None, 5, 2, 4, None, 0, None, 8, used, s) == 0
+    assert lib.tgvkv_compact_paged(z, None, None, None, None, None, None, 5, None, 8, 4, None, None, 1, s) == 0
+    assert lib.tgvkv_decode_attn_paged(z, None, None, None, 1, 4, None, 8, None, 2, None, None, None, None, None,
+                                       None, 0, s) == 0
 
 
 def test_binding_fails_loudly_without_library(tmp_path):
