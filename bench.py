@@ -56,6 +56,10 @@ def parse():
     ap.add_argument("--vision-only", action="store_true",
                     help="vision-only eviction (every layer keeps all text; rho is the retained share of the "
                          "vision tokens) instead of eviction among all tokens")
+    ap.add_argument("--cache", default="contiguous", choices=("contiguous", "paged"),
+                    help="compacted cache layout: one segment per (sequence, layer), or pages of a pool "
+                         "assigned by the page-table kernel (decode then takes a per-sequence step)")
+    ap.add_argument("--page-size", type=int, default=16, help="rows per page of the paged cache")
     ap.add_argument("--decode-steps", type=int, default=None)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -87,14 +91,15 @@ KERNEL_SOURCES = {
     "score_text": ["score.hip", "score_core.h", "tgvkv_device.h"],
     "score_stats": ["score.hip", "score_core.h", "tgvkv_device.h"],
     "score_vision": ["score.hip", "score_core.h", "tgvkv_device.h"],
-    "compact": ["compact.hip", "tgvkv_device.h"],
-    "decode": ["decode.hip", "tgvkv_device.h"],
+    "compact": ["compact.hip", "tgvkv_rows.h", "tgvkv_device.h"],
+    "decode": ["decode.hip", "tgvkv_rows.h", "tgvkv_device.h"],
 }
 
 
-def counter_key(workload, vision_only=False):
-    """Key of a workload's counters in profiles/hbm_counters.json (the eviction mode changes the bytes)."""
-    return workload + (":vision_only" if vision_only else "")
+def counter_key(workload, vision_only=False, cache="contiguous"):
+    """Key of a workload's counters in profiles/hbm_counters.json (the eviction mode and the cache
+    layout change the bytes)."""
+    return workload + (":vision_only" if vision_only else "") + (":paged" if cache == "paged" else "")
 
 
 def traffic_for(kernel, workload, decode_steps=None):
@@ -235,7 +240,8 @@ def main():
     if args.ingest_counters:
         from workloads import CONFIGS
         T = CONFIGS[args.workload].decode_steps if args.decode_steps is None else args.decode_steps
-        ingest_counters(*args.ingest_counters, workload=counter_key(args.workload, args.vision_only), decode_steps=T)
+        ingest_counters(*args.ingest_counters, workload=counter_key(args.workload, args.vision_only, args.cache),
+                        decode_steps=T)
         return
     if args.calibrate_copy:
         calibrate_copy()
@@ -289,6 +295,17 @@ def main():
         torch.cuda.synchronize()
         schedule = "lse_in"
 
+    paged = args.cache == "paged"
+    if paged:
+        # the pool, its free list and the per-step step vectors are set up outside the timed region
+        width, n_pages = bd.page_plan(p, opts, tot, max(T, 1), args.page_size)
+        pool = bd.PagedPool(cfg.heads_kv, cfg.head_dim, args.page_size, n_pages)
+        free_ids = torch.arange(n_pages, dtype=torch.int32, device="cuda")
+        table = torch.empty((B * L, width), dtype=torch.int32, device="cuda")
+        used = torch.zeros((1,), dtype=torch.int64, device="cuda")
+        steps_d = torch.arange(max(T, 1), dtype=torch.int32, device="cuda")[:, None].repeat(1, B).contiguous()
+        log(f"[bench] paged cache: {n_pages} pages of {args.page_size} rows, table width {width}")
+
     def one_step(events=None):
         names = []
 
@@ -300,10 +317,20 @@ def main():
                 events.append((name, ev))
 
         mark("start")
-        sched = buf.evict(q_d, k_d, v_d, schedule=schedule, marks=mark)
+        sched = buf.evict(q_d, k_d, v_d, schedule=schedule, marks=mark, compact=not paged)
+        if paged:
+            bd.tgvkv_page_table(p, opts, buf.budgets, tot, max(T, 1), args.page_size, free_ids, table, used)
+            mark("pages")
+            bd.tgvkv_compact_paged(p, opts, k_d, v_d, buf.idx, buf.budgets, buf.idx_offsets, tot, table,
+                                   args.page_size, pool.k_pool, pool.v_pool)
+            mark("compact")
         for s_ in range(T):
             mark("decode_gap")  # launch gap before the step: in the step time, not in the kernel's
-            buf.decode(s_, dq[s_], dk[s_], dv[s_])
+            if paged:
+                pool.decode(p, opts, table, buf.budgets, max(T, 1), steps_d[s_], dq[s_], dk[s_], dv[s_], buf.out,
+                            buf.ws_decode)
+            else:
+                buf.decode(s_, dq[s_], dk[s_], dv[s_])
             mark("decode")
         return sched
 
@@ -360,7 +387,7 @@ def main():
         gbs = alg[kname] / (ms * 1e-3) / 1e9
         roofs[kname] = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                         "frac": round(gbs / HBM_PEAK_GBS, 4),
-                        "traffic": traffic_for(kname, counter_key(cfg.name, args.vision_only), T),
+                        "traffic": traffic_for(kname, counter_key(cfg.name, args.vision_only, args.cache), T),
                         "kernel": kname, "alg_bytes_per_launch": int(alg[kname]), "avg_launch_ms": round(ms, 4),
                         "ms_per_step": round(ms * (T if kname == "decode" else 1), 4)}
     dominant = max(roofs, key=lambda k: roofs[k]["ms_per_step"])
@@ -385,13 +412,15 @@ def main():
                                f"{cfg.n_sys}+{Nv}+{Nq} tokens, retention {rho:g}"
                                f"{' of vision tokens (all text kept)' if args.vision_only else ''}"
                                f"{', text-row normalisers from the prefill' if args.lse_from_prefill else ''}"
-                               f", {T} decode steps",
+                               f", {T} decode steps"
+                               f"{f', paged cache ({args.page_size}-row pages)' if paged else ''}",
                    "batch": B, "layers": L, "heads_q": H, "heads_kv": Hkv, "head_dim": D,
                    "n_sys": cfg.n_sys, "n_vis": Nv, "n_qst": Nq, "retention": rho, "total_budget_per_seq": tot,
                    "vision_only": bool(args.vision_only),
                    "normalisers_from_prefill": bool(args.lse_from_prefill),
                    "budget_rule": args.budget_rule, "vision_rank": args.vision_rank, "tpr": not args.no_tpr,
-                   "decode_steps": T, "vision_scored_layers": vis_layers, "schedule": sched},
+                   "decode_steps": T, "vision_scored_layers": vis_layers, "schedule": sched,
+                   "cache": args.cache, "page_size": args.page_size if paged else None},
         "evict_ms": round(evict_ms, 4),
         "decode_us_per_step": round(dec_ms * 1e3, 2),
         "decode_us_per_step_with_launch_gaps": round((dec_ms + dec_gap_ms) * 1e3, 2),

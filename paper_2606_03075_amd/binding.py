@@ -382,8 +382,8 @@ class EvictionBuffers:
         layers whose budget reaches past the text (never more work than scoring every layer)."""
         return "two_step"
 
-    def evict(self, q_text, k, v, schedule="auto", stream=None, marks=None):
-        """Score, budget, select and compact.
+    def evict(self, q_text, k, v, schedule="auto", stream=None, marks=None, compact=True):
+        """Score, budget, select and (unless compact=False, e.g. for a paged cache) compact.
 
         schedule: 'auto' (= 'two_step'), 'two_step', 'phases' (every scoring phase as its own
         launch, vision scores for every layer), 'fused' (one persistent scoring launch),
@@ -431,8 +431,9 @@ class EvictionBuffers:
             raise ValueError(f"unknown schedule {schedule!r}")
         self.select(stream)
         mark("select")
-        self.compact(k, v, stream)
-        mark("compact")
+        if compact:
+            self.compact(k, v, stream)
+            mark("compact")
         return sched
 
     def decode(self, step, q, k_new, v_new, stream=None):

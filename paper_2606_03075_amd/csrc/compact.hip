@@ -44,8 +44,6 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(Shape s, Rows rows, c
     const int r_beg = min(split * per, bsz), r_end = min(r_beg + per, bsz);
     const int cc = threadIdx.x % CPR, rl = threadIdx.x / CPR;
     const size_t src0 = ((size_t)bl * s.Hkv + kvh) * (size_t)s.N * D + cc * 8;
-    rows.init(s, bl, kvh, bsz, bsz, lds_pages);
-    __syncthreads();
 
     // positions come from tgvkv_select; clamp so a corrupt index can never read outside the slice
     int pos[kPasses];
@@ -54,6 +52,9 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(Shape s, Rows rows, c
         const int r = r_beg + i * RPP + rl;
         pos[i] = r < r_end ? min(max(idx[ioff + r], 0), s.N - 1) : -1;
     }
+    // destination rows (the paged layout's table is read while the positions are in flight)
+    rows.init(s, bl, kvh, bsz, bsz, lds_pages);
+    __syncthreads();
     for (int r0 = r_beg; r0 < r_end; r0 += ROWS) {
         u32x4 kr[kPasses], vr[kPasses];
 #pragma unroll

@@ -48,16 +48,18 @@ def _contig(cache_bits, so, bl, Hkv, D, cap, rows):
 
 
 # ----------------------------------------------------------------------------- page assignment
+@pytest.mark.parametrize("B,L", [(3, 500), (2, 37), (1, 1)])
 @pytest.mark.parametrize("page,reserve", [(1, 0), (16, 5), (64, 3)])
-def test_page_table_kernel(lib, page, reserve):
-    """More than 1024 segments (several scan chunks); budgets summing to the total per sequence."""
+def test_page_table_kernel(lib, page, reserve, B, L):
+    """Segments split over many workgroups (1500 segments: 167 groups of 9; 74: 9 groups, the last
+    one short; 1: one group); budgets summing to the total per sequence."""
     import torch
-    B, L, N, total = 3, 500, 700, 600
+    N, total = 700, 600
     prob = bd.make_problem(B, L, 4, 2, 128, 10, 600, 90)
     rng = np.random.default_rng(11 + page)
     budgets = np.stack([rng.multinomial(total, rng.dirichlet(np.ones(L) * 0.3)) for _ in range(B)]).astype(np.int32)
     budgets[0, :] = 0
-    budgets[0, 0] = total  # one layer takes the whole budget
+    budgets[0, -1] = total  # one layer takes the whole budget
     width, pool_bound = bd.page_plan(prob, None, total, reserve, page)
     n_free = pool_bound + 7
     free = rng.permutation(n_free + 100)[:n_free].astype(np.int32)
