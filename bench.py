@@ -322,13 +322,13 @@ def main():
             bd.tgvkv_page_table(p, opts, buf.budgets, tot, max(T, 1), args.page_size, free_ids, table, used)
             mark("pages")
             bd.tgvkv_compact_paged(p, opts, k_d, v_d, buf.idx, buf.budgets, buf.idx_offsets, tot, table,
-                                   args.page_size, pool.k_pool, pool.v_pool)
+                                   args.page_size, pool.k_pool, pool.v_pool, unit_order=buf.unit_order)
             mark("compact")
         for s_ in range(T):
             mark("decode_gap")  # launch gap before the step: in the step time, not in the kernel's
             if paged:
                 pool.decode(p, opts, table, buf.budgets, max(T, 1), steps_d[s_], dq[s_], dk[s_], dv[s_], buf.out,
-                            buf.ws_decode)
+                            buf.ws_decode, unit_order=buf.unit_order)
             else:
                 buf.decode(s_, dq[s_], dk[s_], dv[s_])
             mark("decode")

@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define TGVKV_ABI_VERSION 4
+#define TGVKV_ABI_VERSION 5
 
 typedef enum tgvkv_status {
     TGVKV_OK = 0,
@@ -181,11 +181,16 @@ tgvkv_status tgvkv_score(const tgvkv_problem* problem, const tgvkv_opts* opts, i
  * seg_offsets    int64 [B*L + 1]  out: start of each (b, l) cache segment, in units of
  *                                 heads_kv * head_dim elements; segment size b_l + reserve;
  *                                 seg_offsets[B*L] = B * (K + L * reserve)
+ * unit_order_or_null int32 [B*L]  optional out: decode's dispatch order, longest segments
+ *                                 first.  With r_b(l) the rank of layer l in sequence b by
+ *                                 (b_l desc, l asc): unit_order[r_b(l) * B + b] = b*L + l.
+ *                                 A permutation of [0, B*L); pass it to tgvkv_compact and
+ *                                 tgvkv_decode_attn.
  */
 tgvkv_status tgvkv_budget(const tgvkv_problem* problem, const tgvkv_opts* opts,
                           const float* tv_mass, int64_t total_budget, int32_t decode_reserve,
                           int32_t* budgets, int64_t* idx_offsets, int64_t* seg_offsets,
-                          hipStream_t stream);
+                          int32_t* unit_order_or_null, hipStream_t stream);
 
 /*
  * tgvkv_select -- TPR: retained positions of every (sequence, layer, group), Eq. (10).
@@ -215,12 +220,15 @@ tgvkv_status tgvkv_select(const tgvkv_problem* problem, const tgvkv_opts* opts,
  * total_budget / decode_reserve: the values given to tgvkv_budget (they size the
  * launch on the host: B * K rows per KV head are moved, K as in tgvkv_budget).
  * kc, vc  bf16, seg_offsets[B*L] * heads_kv * head_dim elements each.
+ * unit_order_or_null  int32 [B*L], optional: dispatch order of the (sequence, layer) units,
+ *         e.g. tgvkv_budget's longest-first order; as for tgvkv_decode_attn, the result does
+ *         not depend on it, and it must be a permutation of [0, B*L).
  */
 tgvkv_status tgvkv_compact(const tgvkv_problem* problem, const tgvkv_opts* opts,
                            const void* k, const void* v, const int32_t* idx,
                            const int32_t* budgets, const int64_t* idx_offsets,
                            const int64_t* seg_offsets, int64_t total_budget, int32_t decode_reserve,
-                           void* kc, void* vc, hipStream_t stream);
+                           void* kc, void* vc, const int32_t* unit_order_or_null, hipStream_t stream);
 
 /*
  * tgvkv_decode_attn -- one decode step over the pruned cache, Eq. (3)-(4).
@@ -233,12 +241,18 @@ tgvkv_status tgvkv_compact(const tgvkv_problem* problem, const tgvkv_opts* opts,
  * q      bf16 [B][L][heads_q][head_dim];  k_new, v_new bf16 [B][L][heads_kv][head_dim]
  * out    f32  [B][L][heads_q][head_dim]
  * workspace >= tgvkv_workspace_size(p, o, TGVKV_CALL_DECODE) (may be 0 bytes).
+ * unit_order_or_null  int32 [B*L], optional: the order in which (sequence, layer) units
+ *        are dispatched, e.g. tgvkv_budget's longest-first order.  Results do not depend
+ *        on it (each unit's arithmetic is the same); it only shortens the tail of a
+ *        launch whose segments differ in length.  It must be a permutation of [0, B*L):
+ *        entries are clamped into that range, and a unit the order misses is not computed.
  */
 tgvkv_status tgvkv_decode_attn(const tgvkv_problem* problem, const tgvkv_opts* opts,
                                void* kc, void* vc, const int32_t* budgets,
                                const int64_t* seg_offsets, int32_t decode_reserve, int32_t step,
                                const void* q, const void* k_new, const void* v_new, float* out,
-                               void* workspace, size_t workspace_bytes, hipStream_t stream);
+                               void* workspace, size_t workspace_bytes, const int32_t* unit_order_or_null,
+                               hipStream_t stream);
 
 /*
  * Paged cache, for serving with continuous batching.
@@ -293,12 +307,13 @@ tgvkv_status tgvkv_page_table(const tgvkv_problem* problem, const tgvkv_opts* op
 /* tgvkv_compact_paged -- tgvkv_compact into the pages of block_table: row n < b_l
  * of (b, l), KV head h goes to k_pool[page][h][n % page_size][:] with page the
  * table entry n / page_size.  Rows b_l .. are left for tgvkv_decode_attn_paged.
- * TGVKV_E_CAPACITY if max_pages is below ceil(b_max / page_size). */
+ * TGVKV_E_CAPACITY if max_pages is below ceil(b_max / page_size).  unit_order_or_null as
+ * for tgvkv_compact. */
 tgvkv_status tgvkv_compact_paged(const tgvkv_problem* problem, const tgvkv_opts* opts, const void* k, const void* v,
                                  const int32_t* idx, const int32_t* budgets, const int64_t* idx_offsets,
                                  int64_t total_budget, const int32_t* block_table, int32_t max_pages,
                                  int32_t page_size, void* k_pool, void* v_pool, int64_t n_pages,
-                                 hipStream_t stream);
+                                 const int32_t* unit_order_or_null, hipStream_t stream);
 
 /* tgvkv_decode_attn_paged -- one decode step of a continuous batch over the paged cache.
  * Each sequence b is at its own step steps[b] (int32 [B], device): for every layer
@@ -310,12 +325,14 @@ tgvkv_status tgvkv_compact_paged(const tgvkv_problem* problem, const tgvkv_opts*
  * head_dim of `problem` are used, and budgets / block_table rows are the
  * callers' concatenation.  A segment's table row must cover its
  * ceil((b_l + steps[b] + 1) / page_size) pages (tgvkv_page_table's do).
- * Workspace: tgvkv_workspace_size(p, o, TGVKV_CALL_DECODE). */
+ * Workspace: tgvkv_workspace_size(p, o, TGVKV_CALL_DECODE).  unit_order_or_null as for
+ * tgvkv_decode_attn (a permutation of this batch's [0, B*L)). */
 tgvkv_status tgvkv_decode_attn_paged(const tgvkv_problem* problem, const tgvkv_opts* opts, void* k_pool,
                                      void* v_pool, int64_t n_pages, int32_t page_size, const int32_t* block_table,
                                      int32_t max_pages, const int32_t* budgets, int32_t decode_reserve,
                                      const int32_t* steps, const void* q, const void* k_new, const void* v_new,
-                                     float* out, void* workspace, size_t workspace_bytes, hipStream_t stream);
+                                     float* out, void* workspace, size_t workspace_bytes,
+                                     const int32_t* unit_order_or_null, hipStream_t stream);
 
 /* Workspace bytes needed by tgvkv_score (which = TGVKV_CALL_SCORE) or
  * tgvkv_decode_attn / tgvkv_decode_attn_paged (TGVKV_CALL_DECODE); 0 for an invalid problem. */

@@ -61,15 +61,15 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     O = ctypes.POINTER(TgvkvOpts)
     vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     lib.tgvkv_score.argtypes = [P, O, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
-    lib.tgvkv_budget.argtypes = [P, O, vp, i64, i32, vp, vp, vp, vp]
+    lib.tgvkv_budget.argtypes = [P, O, vp, i64, i32, vp, vp, vp, vp, vp]
     lib.tgvkv_select.argtypes = [P, O, vp, vp, vp, vp, vp, vp]
-    lib.tgvkv_compact.argtypes = [P, O, vp, vp, vp, vp, vp, vp, i64, i32, vp, vp, vp]
-    lib.tgvkv_decode_attn.argtypes = [P, O, vp, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, sz, vp]
+    lib.tgvkv_compact.argtypes = [P, O, vp, vp, vp, vp, vp, vp, i64, i32, vp, vp, vp, vp]
+    lib.tgvkv_decode_attn.argtypes = [P, O, vp, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, sz, vp, vp]
     lib.tgvkv_page_plan.argtypes = [P, O, i64, i32, i32, vp, vp]
     lib.tgvkv_page_table.argtypes = [P, O, vp, i64, i32, i32, vp, i64, vp, i32, vp, vp]
-    lib.tgvkv_compact_paged.argtypes = [P, O, vp, vp, vp, vp, vp, i64, vp, i32, i32, vp, vp, i64, vp]
+    lib.tgvkv_compact_paged.argtypes = [P, O, vp, vp, vp, vp, vp, i64, vp, i32, i32, vp, vp, i64, vp, vp]
     lib.tgvkv_decode_attn_paged.argtypes = [P, O, vp, vp, i64, i32, vp, i32, vp, i32, vp, vp, vp, vp, vp, vp, sz,
-                                            vp]
+                                            vp, vp]
     lib.tgvkv_workspace_size.argtypes = [P, O, i32]
     lib.tgvkv_workspace_size.restype = sz
     lib.tgvkv_status_string.argtypes = [ctypes.c_int]
@@ -202,13 +202,14 @@ def tgvkv_score(problem, opts, phases, q_text, k, lse, s_txt, w_txt, tv_mass, s_
 
 
 def tgvkv_budget(problem, opts, tv_mass, total_budget, decode_reserve, budgets, idx_offsets, seg_offsets,
-                 stream=None):
+                 stream=None, unit_order=None):
     import torch
     st = load_library().tgvkv_budget(ctypes.byref(problem), _opts_ref(opts), _ptr(tv_mass, _f32(), "tv_mass"),
                                      int(total_budget), int(decode_reserve),
                                      _ptr(budgets, (torch.int32,), "budgets"),
                                      _ptr(idx_offsets, (torch.int64,), "idx_offsets"),
-                                     _ptr(seg_offsets, (torch.int64,), "seg_offsets"), _stream(stream))
+                                     _ptr(seg_offsets, (torch.int64,), "seg_offsets"),
+                                     _ptr(unit_order, (torch.int32,), "unit_order"), _stream(stream))
     _check("tgvkv_budget", st)
 
 
@@ -222,7 +223,7 @@ def tgvkv_select(problem, opts, s_vis, s_txt, budgets, idx_offsets, idx, stream=
 
 
 def tgvkv_compact(problem, opts, k, v, idx, budgets, idx_offsets, seg_offsets, total_budget, decode_reserve,
-                  kc, vc, stream=None):
+                  kc, vc, stream=None, unit_order=None):
     import torch
     st = load_library().tgvkv_compact(ctypes.byref(problem), _opts_ref(opts), _ptr(k, _bf16(), "k"),
                                       _ptr(v, _bf16(), "v"), _ptr(idx, (torch.int32,), "idx"),
@@ -230,12 +231,12 @@ def tgvkv_compact(problem, opts, k, v, idx, budgets, idx_offsets, seg_offsets, t
                                       _ptr(idx_offsets, (torch.int64,), "idx_offsets"),
                                       _ptr(seg_offsets, (torch.int64,), "seg_offsets"), int(total_budget),
                                       int(decode_reserve), _ptr(kc, _bf16(), "kc"), _ptr(vc, _bf16(), "vc"),
-                                      _stream(stream))
+                                      _ptr(unit_order, (torch.int32,), "unit_order"), _stream(stream))
     _check("tgvkv_compact", st)
 
 
 def tgvkv_decode_attn(problem, opts, kc, vc, budgets, seg_offsets, decode_reserve, step, q, k_new, v_new, out,
-                      workspace=None, stream=None):
+                      workspace=None, stream=None, unit_order=None):
     import torch
     ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
     st = load_library().tgvkv_decode_attn(ctypes.byref(problem), _opts_ref(opts), _ptr(kc, _bf16(), "kc"),
@@ -243,7 +244,8 @@ def tgvkv_decode_attn(problem, opts, kc, vc, budgets, seg_offsets, decode_reserv
                                           _ptr(seg_offsets, (torch.int64,), "seg_offsets"), int(decode_reserve),
                                           int(step), _ptr(q, _bf16(), "q"), _ptr(k_new, _bf16(), "k_new"),
                                           _ptr(v_new, _bf16(), "v_new"), _ptr(out, _f32(), "out"),
-                                          _ptr(workspace, None, "workspace"), ws_bytes, _stream(stream))
+                                          _ptr(workspace, None, "workspace"), ws_bytes,
+                                          _ptr(unit_order, (torch.int32,), "unit_order"), _stream(stream))
     _check("tgvkv_decode_attn", st)
 
 
@@ -286,7 +288,7 @@ def tgvkv_page_table(problem, opts, budgets, total_budget, decode_reserve, page_
 
 
 def tgvkv_compact_paged(problem, opts, k, v, idx, budgets, idx_offsets, total_budget, block_table, page_size,
-                        k_pool, v_pool, stream=None):
+                        k_pool, v_pool, stream=None, unit_order=None):
     import torch
     n_pages = _pool_pages(k_pool, v_pool, problem, page_size)
     st = load_library().tgvkv_compact_paged(ctypes.byref(problem), _opts_ref(opts), _ptr(k, _bf16(), "k"),
@@ -296,12 +298,13 @@ def tgvkv_compact_paged(problem, opts, k, v, idx, budgets, idx_offsets, total_bu
                                             _ptr(block_table, (torch.int32,), "block_table"),
                                             _table_width(block_table, problem), int(page_size),
                                             _ptr(k_pool, _bf16(), "k_pool"), _ptr(v_pool, _bf16(), "v_pool"),
-                                            n_pages, _stream(stream))
+                                            n_pages, _ptr(unit_order, (torch.int32,), "unit_order"),
+                                            _stream(stream))
     _check("tgvkv_compact_paged", st)
 
 
 def tgvkv_decode_attn_paged(problem, opts, k_pool, v_pool, page_size, block_table, budgets, decode_reserve, steps,
-                            q, k_new, v_new, out, workspace=None, stream=None):
+                            q, k_new, v_new, out, workspace=None, stream=None, unit_order=None):
     import torch
     n_pages = _pool_pages(k_pool, v_pool, problem, page_size)
     ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
@@ -314,7 +317,8 @@ def tgvkv_decode_attn_paged(problem, opts, k_pool, v_pool, page_size, block_tabl
                                                 int(decode_reserve), _ptr(steps, (torch.int32,), "steps"),
                                                 _ptr(q, _bf16(), "q"), _ptr(k_new, _bf16(), "k_new"),
                                                 _ptr(v_new, _bf16(), "v_new"), _ptr(out, _f32(), "out"),
-                                                _ptr(workspace, None, "workspace"), ws_bytes, _stream(stream))
+                                                _ptr(workspace, None, "workspace"), ws_bytes,
+                                                _ptr(unit_order, (torch.int32,), "unit_order"), _stream(stream))
     _check("tgvkv_decode_attn_paged", st)
 
 
@@ -341,6 +345,7 @@ class EvictionBuffers:
         self.tv_mass = torch.empty((B, L), **f32)
         self.s_vis = torch.zeros((B, L, g, Nv), **f32)
         self.budgets = torch.empty((B, L), dtype=torch.int32, device=device)
+        self.unit_order = torch.empty((max(1, B * L),), dtype=torch.int32, device=device)  # decode dispatch
         self.idx_offsets = torch.empty((B * L + 1,), dtype=torch.int64, device=device)
         self.seg_offsets = torch.empty((B * L + 1,), dtype=torch.int64, device=device)
         self.kept = kept_per_sequence(p, opts, self.total_budget)
@@ -360,7 +365,7 @@ class EvictionBuffers:
 
     def budget(self, stream=None):
         tgvkv_budget(self.problem, self.opts, self.tv_mass, self.total_budget, self.decode_reserve, self.budgets,
-                     self.idx_offsets, self.seg_offsets, stream)
+                     self.idx_offsets, self.seg_offsets, stream, self.unit_order)
 
     def select(self, stream=None):
         tgvkv_select(self.problem, self.opts, self.s_vis, self.s_txt, self.budgets, self.idx_offsets, self.idx,
@@ -368,7 +373,7 @@ class EvictionBuffers:
 
     def compact(self, k, v, stream=None):
         tgvkv_compact(self.problem, self.opts, k, v, self.idx, self.budgets, self.idx_offsets, self.seg_offsets,
-                      self.total_budget, self.decode_reserve, self.kc, self.vc, stream)
+                      self.total_budget, self.decode_reserve, self.kc, self.vc, stream, self.unit_order)
 
     def forced_or_text(self) -> int:
         """A layer needs vision scores only when its budget exceeds this: |forced U T| with TPR,
@@ -438,7 +443,8 @@ class EvictionBuffers:
 
     def decode(self, step, q, k_new, v_new, stream=None):
         tgvkv_decode_attn(self.problem, self.opts, self.kc, self.vc, self.budgets, self.seg_offsets,
-                          self.decode_reserve, step, q, k_new, v_new, self.out, self.ws_decode, stream)
+                          self.decode_reserve, step, q, k_new, v_new, self.out, self.ws_decode, stream,
+                          self.unit_order)
         return self.out
 
 
@@ -473,7 +479,7 @@ class PagedPool:
         tgvkv_page_table(p, o, buf.budgets, buf.total_budget, buf.decode_reserve, self.page_size, ids, table, used,
                          stream)
         tgvkv_compact_paged(p, o, k, v, buf.idx, buf.budgets, buf.idx_offsets, buf.total_budget, table,
-                            self.page_size, self.k_pool, self.v_pool, stream)
+                            self.page_size, self.k_pool, self.v_pool, stream, buf.unit_order)
         n = int(used.item()) if p.batch > 0 else 0
         del self.free[:n]
         return table
@@ -484,8 +490,8 @@ class PagedPool:
         self.free.extend(int(i) for i in ids if i >= 0)
 
     def decode(self, problem, opts, table, budgets, decode_reserve, steps, q, k_new, v_new, out, workspace,
-               stream=None):
+               stream=None, unit_order=None):
         """One decode step of a continuous batch whose sequence b is at step steps[b]."""
         tgvkv_decode_attn_paged(problem, opts, self.k_pool, self.v_pool, self.page_size, table, budgets,
-                                decode_reserve, steps, q, k_new, v_new, out, workspace, stream)
+                                decode_reserve, steps, q, k_new, v_new, out, workspace, stream, unit_order)
         return out

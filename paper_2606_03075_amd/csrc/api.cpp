@@ -286,7 +286,7 @@ tgvkv_status tgvkv_score(const tgvkv_problem* problem, const tgvkv_opts* opts, i
 
 tgvkv_status tgvkv_budget(const tgvkv_problem* problem, const tgvkv_opts* opts, const float* tv_mass,
                           int64_t total_budget, int32_t decode_reserve, int32_t* budgets, int64_t* idx_offsets,
-                          int64_t* seg_offsets, hipStream_t stream) {
+                          int64_t* seg_offsets, int32_t* unit_order_or_null, hipStream_t stream) {
     Shape s;
     tgvkv_status st = make_shape(problem, opts, &s);
     if (st != TGVKV_OK) return st;
@@ -303,7 +303,7 @@ tgvkv_status tgvkv_budget(const tgvkv_problem* problem, const tgvkv_opts* opts, 
     const int32_t add = always_kept(s);
     const int32_t floor_n = s.vision_only ? 0 : forced_count(s);
     return hip_status(tgvkv::launch_budget(s, tv_mass, total_budget, cap, add, decode_reserve, floor_n, budgets,
-                                           idx_offsets, seg_offsets, stream));
+                                           idx_offsets, seg_offsets, unit_order_or_null, stream));
 }
 
 tgvkv_status tgvkv_select(const tgvkv_problem* problem, const tgvkv_opts* opts, const float* s_vis,
@@ -322,7 +322,7 @@ tgvkv_status tgvkv_select(const tgvkv_problem* problem, const tgvkv_opts* opts, 
 tgvkv_status tgvkv_compact(const tgvkv_problem* problem, const tgvkv_opts* opts, const void* k, const void* v,
                            const int32_t* idx, const int32_t* budgets, const int64_t* idx_offsets,
                            const int64_t* seg_offsets, int64_t total_budget, int32_t decode_reserve, void* kc,
-                           void* vc, hipStream_t stream) {
+                           void* vc, const int32_t* unit_order_or_null, hipStream_t stream) {
     Shape s;
     tgvkv_status st = make_shape(problem, opts, &s);
     if (st != TGVKV_OK) return st;
@@ -335,16 +335,18 @@ tgvkv_status tgvkv_compact(const tgvkv_problem* problem, const tgvkv_opts* opts,
         return TGVKV_E_INVAL;
     if (!aligned16(k) || !aligned16(v) || !aligned16(kc) || !aligned16(vc)) return TGVKV_E_INVAL;
     const int64_t rows = (int64_t)s.B * kept;
-    if ((int64_t)s.B * s.L * 16 > kMaxBlocks || s.Hkv > 65535) return TGVKV_E_UNSUPPORTED;
+    if ((int64_t)s.B * s.L * s.Hkv * 16 > kMaxBlocks) return TGVKV_E_UNSUPPORTED;
     return hip_status(tgvkv::launch_compact(s, static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), idx,
                                             budgets, idx_offsets, seg_offsets, decode_reserve, rows,
-                                            static_cast<uint16_t*>(kc), static_cast<uint16_t*>(vc), stream));
+                                            unit_order_or_null, static_cast<uint16_t*>(kc),
+                                            static_cast<uint16_t*>(vc), stream));
 }
 
 tgvkv_status tgvkv_decode_attn(const tgvkv_problem* problem, const tgvkv_opts* opts, void* kc, void* vc,
                                const int32_t* budgets, const int64_t* seg_offsets, int32_t decode_reserve,
                                int32_t step, const void* q, const void* k_new, const void* v_new, float* out,
-                               void* workspace, size_t workspace_bytes, hipStream_t stream) {
+                               void* workspace, size_t workspace_bytes, const int32_t* unit_order_or_null,
+                               hipStream_t stream) {
     Shape s;
     tgvkv_status st = make_shape(problem, opts, &s);
     if (st != TGVKV_OK) return st;
@@ -361,7 +363,7 @@ tgvkv_status tgvkv_decode_attn(const tgvkv_problem* problem, const tgvkv_opts* o
     return hip_status(tgvkv::launch_decode(s, static_cast<uint16_t*>(kc), static_cast<uint16_t*>(vc), budgets,
                                            seg_offsets, decode_reserve, step, static_cast<const uint16_t*>(q),
                                            static_cast<const uint16_t*>(k_new), static_cast<const uint16_t*>(v_new),
-                                           out, static_cast<float*>(workspace), stream));
+                                           out, static_cast<float*>(workspace), unit_order_or_null, stream));
 }
 
 tgvkv_status tgvkv_page_plan(const tgvkv_problem* problem, const tgvkv_opts* opts, int64_t total_budget,
@@ -407,7 +409,7 @@ tgvkv_status tgvkv_compact_paged(const tgvkv_problem* problem, const tgvkv_opts*
                                  const int32_t* idx, const int32_t* budgets, const int64_t* idx_offsets,
                                  int64_t total_budget, const int32_t* block_table, int32_t max_pages,
                                  int32_t page_size, void* k_pool, void* v_pool, int64_t n_pages,
-                                 hipStream_t stream) {
+                                 const int32_t* unit_order_or_null, hipStream_t stream) {
     Shape s;
     tgvkv_status st = make_shape(problem, opts, &s);
     if (st != TGVKV_OK) return st;
@@ -422,10 +424,10 @@ tgvkv_status tgvkv_compact_paged(const tgvkv_problem* problem, const tgvkv_opts*
         block_table == nullptr || k_pool == nullptr || v_pool == nullptr)
         return TGVKV_E_INVAL;
     if (!aligned16(k) || !aligned16(v) || !aligned16(k_pool) || !aligned16(v_pool)) return TGVKV_E_INVAL;
-    if ((int64_t)s.B * s.L * 16 > kMaxBlocks || s.Hkv > 65535) return TGVKV_E_UNSUPPORTED;
+    if ((int64_t)s.B * s.L * s.Hkv * 16 > kMaxBlocks) return TGVKV_E_UNSUPPORTED;
     return hip_status(tgvkv::launch_compact_paged(
         s, static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), idx, budgets, idx_offsets,
-        (int64_t)s.B * kept, block_table, max_pages, sh, n_pages, static_cast<uint16_t*>(k_pool),
+        (int64_t)s.B * kept, block_table, max_pages, sh, n_pages, unit_order_or_null, static_cast<uint16_t*>(k_pool),
         static_cast<uint16_t*>(v_pool), stream));
 }
 
@@ -433,7 +435,8 @@ tgvkv_status tgvkv_decode_attn_paged(const tgvkv_problem* problem, const tgvkv_o
                                      void* v_pool, int64_t n_pages, int32_t page_size, const int32_t* block_table,
                                      int32_t max_pages, const int32_t* budgets, int32_t decode_reserve,
                                      const int32_t* steps, const void* q, const void* k_new, const void* v_new,
-                                     float* out, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+                                     float* out, void* workspace, size_t workspace_bytes,
+                                     const int32_t* unit_order_or_null, hipStream_t stream) {
     Shape s;
     tgvkv_status st = make_shape(problem, opts, &s);
     if (st != TGVKV_OK) return st;
@@ -451,7 +454,7 @@ tgvkv_status tgvkv_decode_attn_paged(const tgvkv_problem* problem, const tgvkv_o
     return hip_status(tgvkv::launch_decode_paged(
         s, static_cast<uint16_t*>(k_pool), static_cast<uint16_t*>(v_pool), n_pages, block_table, max_pages, sh,
         budgets, decode_reserve, steps, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_new),
-        static_cast<const uint16_t*>(v_new), out, static_cast<float*>(workspace), stream));
+        static_cast<const uint16_t*>(v_new), out, static_cast<float*>(workspace), unit_order_or_null, stream));
 }
 
 }  // extern "C\"

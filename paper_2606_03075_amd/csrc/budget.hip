@@ -13,7 +13,9 @@
 // budgets are a pure function of the float32 masses (element-wise steps are
 // order-free).  The largest-remainder step ranks each eligible layer by
 // (fraction desc, layer asc) with an all-pairs count, which gives the same set
-// as sorting.
+// as sorting.  The same count by (budget desc, layer asc) gives decode's
+// dispatch order: rank-major over the batch, so every sequence's longest
+// segments are started first (longest-processing-time-first scheduling).
 #pragma clang fp contract(off)
 
 #include "tgvkv_device.h"
@@ -29,7 +31,8 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(Shape s, const float* 
                                                           int cap_tokens, int add, int reserve, int n_forced,
                                                           int32_t* __restrict__ budgets,
                                                           int64_t* __restrict__ idx_off,
-                                                          int64_t* __restrict__ seg_off) {
+                                                          int64_t* __restrict__ seg_off,
+                                                          int32_t* __restrict__ unit_order) {
     __shared__ double f[kMaxLayers];
     __shared__ double x[kMaxLayers];
     __shared__ long long bcount[kMaxLayers];
@@ -129,6 +132,15 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(Shape s, const float* 
     }
     __syncthreads();
 
+    if (unit_order != nullptr) {
+        for (int l = tid; l < L; l += kThreads) {
+            const long long bl_count = bcount[l];
+            int rank = 0;
+            for (int j = 0; j < L; ++j) rank += (bcount[j] > bl_count) || (bcount[j] == bl_count && j < l);
+            unit_order[(size_t)rank * s.B + b] = b * L + l;
+        }
+    }
+
     if (tid == 0) {
         const long long g = s.ngroups;
         const long long kept = total + (long long)L * add;  // tokens each sequence keeps
@@ -154,10 +166,10 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(Shape s, const float* 
 
 hipError_t launch_budget(const Shape& s, const float* tv_mass, int64_t total, int32_t cap_tokens, int32_t add,
                          int32_t reserve, int32_t n_floor, int32_t* budgets, int64_t* idx_off, int64_t* seg_off,
-                         hipStream_t st) {
+                         int32_t* unit_order, hipStream_t st) {
     if (s.B == 0) return hipSuccess;
     hipLaunchKernelGGL(budget_kernel, dim3(s.B), dim3(kThreads), 0, st, s, tv_mass, (long long)total, cap_tokens,
-                       add, reserve, n_floor, budgets, idx_off, seg_off);
+                       add, reserve, n_floor, budgets, idx_off, seg_off, unit_order);
     return hipGetLastError();
 }
 

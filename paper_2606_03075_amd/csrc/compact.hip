@@ -11,6 +11,9 @@
 // the positions of the next rows are fetched while the current ones are moved.
 // The destination is either a contiguous segment per (sequence, layer) or the
 // pages that a block table names (paged cache); only the row addressing differs.
+// Budgets differ across layers (TVB), so an optional unit order (the budget
+// call's, longest first) sets which (sequence, layer) the i-th group of
+// workgroups moves: the long units start first instead of forming the tail.
 #include <algorithm>
 #include <climits>
 
@@ -30,14 +33,18 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(Shape s, Rows rows, c
                                                            const int32_t* __restrict__ idx,
                                                            const int32_t* __restrict__ budgets,
                                                            const int64_t* __restrict__ idx_off, int nsplit,
+                                                           const int32_t* __restrict__ unit_order,
                                                            uint16_t* __restrict__ kc, uint16_t* __restrict__ vc) {
     extern __shared__ int lds_pages[];  // paged layout: the unit's page ids
     constexpr int CPR = D / 8;             // lanes per row
     constexpr int RPP = kThreads / CPR;    // rows per pass
     constexpr int ROWS = RPP * kPasses;    // rows per iteration
-    const int kvh = blockIdx.y;
-    const int split = blockIdx.x % nsplit;
-    const int bl = blockIdx.x / nsplit;
+    // workgroup id = (unit rank * H_kv + KV head) * nsplit + split: a unit's heads and shares are adjacent
+    int bid = blockIdx.x;
+    const int split = bid % nsplit;
+    bid /= nsplit;
+    const int kvh = bid % s.Hkv;
+    const int bl = unit_order != nullptr ? min(max(unit_order[bid / s.Hkv], 0), s.B * s.L - 1) : bid / s.Hkv;
     const int bsz = budgets[bl];
     const long long ioff = idx_off[bl] + (s.head_mode == 0 ? 0 : (long long)kvh * bsz);
     const int per = (bsz + nsplit - 1) / nsplit;
@@ -95,11 +102,11 @@ int compact_splits(const Shape& s, int64_t rows_total) {
 template <int D, class Rows>
 hipError_t launch_compact_d(const Shape& s, const Rows& rows, size_t lds, const uint16_t* k, const uint16_t* v,
                             const int32_t* idx, const int32_t* budgets, const int64_t* idx_off, int64_t rows_total,
-                            uint16_t* kc, uint16_t* vc, hipStream_t st) {
+                            const int32_t* unit_order, uint16_t* kc, uint16_t* vc, hipStream_t st) {
     const int nsplit = compact_splits(s, rows_total);
-    dim3 grid((unsigned)((long long)s.B * s.L * nsplit), (unsigned)s.Hkv);
+    dim3 grid((unsigned)((long long)s.B * s.L * s.Hkv * nsplit));
     hipLaunchKernelGGL((compact_kernel<D, Rows>), grid, dim3(kThreads), lds, st, s, rows, k, v, idx, budgets, idx_off,
-                       nsplit, kc, vc);
+                       nsplit, unit_order, kc, vc);
     return hipGetLastError();
 }
 
@@ -107,27 +114,27 @@ hipError_t launch_compact_d(const Shape& s, const Rows& rows, size_t lds, const 
 
 hipError_t launch_compact(const Shape& s, const uint16_t* k, const uint16_t* v, const int32_t* idx,
                           const int32_t* budgets, const int64_t* idx_off, const int64_t* seg_off, int32_t reserve,
-                          int64_t rows_total, uint16_t* kc, uint16_t* vc, hipStream_t st) {
+                          int64_t rows_total, const int32_t* unit_order, uint16_t* kc, uint16_t* vc, hipStream_t st) {
     if (rows_total <= 0 || s.B * s.L == 0) return hipSuccess;
     if (s.D == 128)
         return launch_compact_d<128>(s, ContigRows<128>{seg_off, reserve, 0}, 0, k, v, idx, budgets, idx_off,
-                                     rows_total, kc, vc, st);
+                                     rows_total, unit_order, kc, vc, st);
     return launch_compact_d<64>(s, ContigRows<64>{seg_off, reserve, 0}, 0, k, v, idx, budgets, idx_off, rows_total,
-                                kc, vc, st);
+                                unit_order, kc, vc, st);
 }
 
 hipError_t launch_compact_paged(const Shape& s, const uint16_t* k, const uint16_t* v, const int32_t* idx,
                                 const int32_t* budgets, const int64_t* idx_off, int64_t rows_total,
                                 const int32_t* block_table, int32_t max_pages, int32_t page_shift, int64_t n_pages,
-                                uint16_t* k_pool, uint16_t* v_pool, hipStream_t st) {
+                                const int32_t* unit_order, uint16_t* k_pool, uint16_t* v_pool, hipStream_t st) {
     if (rows_total <= 0 || s.B * s.L == 0) return hipSuccess;
     const int np = (int)std::min<int64_t>(n_pages, INT32_MAX);
     const size_t lds = PagedRows<128>::lds_bytes(max_pages);
     if (s.D == 128)
         return launch_compact_d<128>(s, PagedRows<128>{block_table, max_pages, page_shift, np, 0, 0, nullptr}, lds, k,
-                                     v, idx, budgets, idx_off, rows_total, k_pool, v_pool, st);
+                                     v, idx, budgets, idx_off, rows_total, unit_order, k_pool, v_pool, st);
     return launch_compact_d<64>(s, PagedRows<64>{block_table, max_pages, page_shift, np, 0, 0, nullptr}, lds, k, v,
-                                idx, budgets, idx_off, rows_total, k_pool, v_pool, st);
+                                idx, budgets, idx_off, rows_total, unit_order, k_pool, v_pool, st);
 }
 
 }  // namespace tgvkv

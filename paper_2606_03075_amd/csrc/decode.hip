@@ -18,7 +18,9 @@
 // is written to is not re-read in the same launch).  The cache is either one
 // contiguous segment per (sequence, layer) or fixed-size pages found through a
 // block table (staged in LDS); with per-sequence steps (continuous batching) a
-// sequence whose step is outside [0, reserve) is skipped.
+// sequence whose step is outside [0, reserve) is skipped.  An optional unit order
+// (from the budget call: longest segments first) sets which (sequence, layer) each
+// workgroup serves, so the long segments do not all start last.
 #include <algorithm>
 #include <climits>
 
@@ -47,7 +49,8 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(Shape s, Rows rows, ui
                                                           const uint16_t* __restrict__ q,
                                                           const uint16_t* __restrict__ k_new,
                                                           const uint16_t* __restrict__ v_new, float* __restrict__ out,
-                                                          float* __restrict__ ws_part, int nsplit) {
+                                                          float* __restrict__ ws_part, int nsplit,
+                                                          const int32_t* __restrict__ unit_order) {
     constexpr int LPR = D / 8;         // lanes per token row
     constexpr int GPW = 64 / LPR;      // lane groups per wave
     constexpr int NGRP = 4 * GPW;      // lane groups per workgroup
@@ -63,7 +66,9 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(Shape s, Rows rows, ui
     const int split = bid % nsplit;
     bid /= nsplit;
     const int kvh = bid % s.Hkv;
-    const int bl = bid / s.Hkv;
+    // dispatch order: unit_order[i] is the (sequence, layer) the i-th group of workgroups serves
+    // (clamped, so a wrong order can never address outside the batch)
+    const int bl = unit_order != nullptr ? min(max(unit_order[bid / s.Hkv], 0), s.B * s.L - 1) : bid / s.Hkv;
     const int G = s.G;
 
     // continuous batching: each sequence at its own step, outside [0, reserve) = not decoding
@@ -240,11 +245,11 @@ template <int D, class Rows>
 hipError_t launch_decode_d(const Shape& s, const Rows& rows, size_t lds_bytes, uint16_t* kc, uint16_t* vc,
                            const int32_t* budgets, int32_t reserve, int32_t step, const int32_t* steps,
                            const uint16_t* q, const uint16_t* k_new, const uint16_t* v_new, float* out, float* ws_part,
-                           int nsplit, hipStream_t st) {
+                           int nsplit, const int32_t* unit_order, hipStream_t st) {
     dim3 grid((unsigned)((long long)s.B * s.L * s.Hkv * nsplit)), block(kThreads);
 #define TGVKV_DECODE_LAUNCH(GM)                                                                                   \
     hipLaunchKernelGGL((decode_kernel<D, GM, Rows>), grid, block, lds_bytes, st, s, rows, kc, vc, budgets, reserve, \
-                       step, steps, q, k_new, v_new, out, ws_part, nsplit)
+                       step, steps, q, k_new, v_new, out, ws_part, nsplit, unit_order)
     if (s.G <= 1) TGVKV_DECODE_LAUNCH(1);
     else if (s.G <= 2) TGVKV_DECODE_LAUNCH(2);
     else if (s.G <= 4) TGVKV_DECODE_LAUNCH(4);
@@ -271,24 +276,24 @@ int decode_splits(const Shape& s) {
 
 hipError_t launch_decode(const Shape& s, uint16_t* kc, uint16_t* vc, const int32_t* budgets, const int64_t* seg_off,
                          int32_t reserve, int32_t step, const uint16_t* q, const uint16_t* k_new, const uint16_t* v_new,
-                         float* out, float* ws_part, hipStream_t st) {
+                         float* out, float* ws_part, const int32_t* unit_order, hipStream_t st) {
     if ((long long)s.B * s.L == 0) return hipSuccess;
     const int nsplit = decode_splits(s);
     if (s.D == 128) {
         ContigRows<128> rows{seg_off, reserve, 0};
         return launch_decode_d<128>(s, rows, 0, kc, vc, budgets, reserve, step, nullptr, q, k_new, v_new, out,
-                                    ws_part, nsplit, st);
+                                    ws_part, nsplit, unit_order, st);
     }
     ContigRows<64> rows{seg_off, reserve, 0};
     return launch_decode_d<64>(s, rows, 0, kc, vc, budgets, reserve, step, nullptr, q, k_new, v_new, out, ws_part,
-                               nsplit, st);
+                               nsplit, unit_order, st);
 }
 
 hipError_t launch_decode_paged(const Shape& s, uint16_t* k_pool, uint16_t* v_pool, int64_t n_pages,
                                const int32_t* block_table, int32_t max_pages, int32_t page_shift,
                                const int32_t* budgets, int32_t reserve, const int32_t* steps, const uint16_t* q,
                                const uint16_t* k_new, const uint16_t* v_new, float* out, float* ws_part,
-                               hipStream_t st) {
+                               const int32_t* unit_order, hipStream_t st) {
     if ((long long)s.B * s.L == 0) return hipSuccess;
     const int nsplit = decode_splits(s);
     const size_t lds = PagedRows<128>::lds_bytes(max_pages);
@@ -296,11 +301,11 @@ hipError_t launch_decode_paged(const Shape& s, uint16_t* k_pool, uint16_t* v_poo
     if (s.D == 128) {
         PagedRows<128> rows{block_table, max_pages, page_shift, np, 0, 0, nullptr};
         return launch_decode_d<128>(s, rows, lds, k_pool, v_pool, budgets, reserve, 0, steps, q, k_new, v_new, out,
-                                    ws_part, nsplit, st);
+                                    ws_part, nsplit, unit_order, st);
     }
     PagedRows<64> rows{block_table, max_pages, page_shift, np, 0, 0, nullptr};
     return launch_decode_d<64>(s, rows, lds, k_pool, v_pool, budgets, reserve, 0, steps, q, k_new, v_new, out,
-                               ws_part, nsplit, st);
+                               ws_part, nsplit, unit_order, st);
 }
 
 }  // namespace tgvkv

@@ -34,8 +34,9 @@ struct ContigRows {
 
 // The page ids of rows [0, rows) are copied into LDS (clamped into the pool, so an
 // unfilled table entry of -1 can never address outside it, and a row past the
-// table's width reads its last entry) so that a row's address costs no global load.  init() is called by every thread and must be followed by a
-// barrier before row() is used.
+// table's width reads its last entry) so that a row's address costs no global
+// load.  init() is called by every thread and must be followed by a barrier
+// before row() is used.
 template <int D>
 struct PagedRows {
     const int32_t* block_table;

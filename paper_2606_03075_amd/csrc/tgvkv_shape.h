@@ -71,15 +71,17 @@ hipError_t launch_score_vis_reduce(const Shape& s, const RowPlan& rp, const floa
                                    hipStream_t st);
 
 // Water-fills `total` over the layers with per-layer cap `cap_tokens` and floor
-// n_floor, then writes b_l = add + share (add = N_t in vision-only eviction).
+// n_floor, then writes b_l = add + share (add = N_t in vision-only eviction), and,
+// if unit_order is given, decode's longest-first dispatch order.
 hipError_t launch_budget(const Shape& s, const float* tv_mass, int64_t total, int32_t cap_tokens, int32_t add,
                          int32_t reserve, int32_t n_floor, int32_t* budgets, int64_t* idx_off, int64_t* seg_off,
-                         hipStream_t st);
+                         int32_t* unit_order, hipStream_t st);
 hipError_t launch_select(const Shape& s, const float* s_vis, const float* s_txt, const int32_t* budgets,
                          const int64_t* idx_off, int32_t* idx, hipStream_t st);
 hipError_t launch_compact(const Shape& s, const uint16_t* k, const uint16_t* v, const int32_t* idx,
                           const int32_t* budgets, const int64_t* idx_off, const int64_t* seg_off,
-                          int32_t reserve, int64_t rows_total, uint16_t* kc, uint16_t* vc, hipStream_t st);
+                          int32_t reserve, int64_t rows_total, const int32_t* unit_order, uint16_t* kc,
+                          uint16_t* vc, hipStream_t st);
 
 // Paged cache: pages of 2^page_shift rows, [n_pages][H_kv][2^page_shift][D]; row n of
 // (sequence, layer) bl lives in page block_table[bl * max_pages + (n >> page_shift)].
@@ -89,18 +91,18 @@ hipError_t launch_page_table(const Shape& s, const int32_t* budgets, int32_t res
 hipError_t launch_compact_paged(const Shape& s, const uint16_t* k, const uint16_t* v, const int32_t* idx,
                                 const int32_t* budgets, const int64_t* idx_off, int64_t rows_total,
                                 const int32_t* block_table, int32_t max_pages, int32_t page_shift, int64_t n_pages,
-                                uint16_t* k_pool, uint16_t* v_pool, hipStream_t st);
+                                const int32_t* unit_order, uint16_t* k_pool, uint16_t* v_pool, hipStream_t st);
 
 int decode_splits(const Shape& s);
 hipError_t launch_decode(const Shape& s, uint16_t* kc, uint16_t* vc, const int32_t* budgets,
                          const int64_t* seg_off, int32_t reserve, int32_t step, const uint16_t* q,
                          const uint16_t* k_new, const uint16_t* v_new, float* out, float* ws_part,
-                         hipStream_t st);
+                         const int32_t* unit_order, hipStream_t st);
 // steps: per-sequence decode step [B]; a sequence whose step is outside [0, reserve) is skipped.
 hipError_t launch_decode_paged(const Shape& s, uint16_t* k_pool, uint16_t* v_pool, int64_t n_pages,
                                const int32_t* block_table, int32_t max_pages, int32_t page_shift,
                                const int32_t* budgets, int32_t reserve, const int32_t* steps, const uint16_t* q,
                                const uint16_t* k_new, const uint16_t* v_new, float* out, float* ws_part,
-                               hipStream_t st);
+                               const int32_t* unit_order, hipStream_t st);
 
 }  // namespace tgvkv

@@ -44,7 +44,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(bd.EXPORTS) <= set(names) and len(names) == len(bd.EXPORTS), names
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.tgvkv_abi_version() == 4
+    assert lib.tgvkv_abi_version() == 5
     for st in (0, -1, -2, -3, -4, -5):
         assert lib.tgvkv_status_string(st)
     assert lib.tgvkv_status_string(7) == b"unknown status"
@@ -108,25 +108,27 @@ def test_validation_before_any_launch(lib):
     assert lib.tgvkv_score(ok, None, 7, fake, fake, fake, fake, fake, fake, fake, None, fake, 16, s) == -3
     # budgets: capacity and arguments
     L, N = 2, 48
-    assert lib.tgvkv_budget(ok, None, fake, L * N + 1, 0, fake, fake, fake, s) == -4
-    assert lib.tgvkv_budget(ok, None, fake, -1, 0, fake, fake, fake, s) == -1
-    assert lib.tgvkv_budget(ok, None, fake, 10, -1, fake, fake, fake, s) == -1
-    assert lib.tgvkv_budget(ok, None, None, 10, 0, fake, fake, fake, s) == -1
+    assert lib.tgvkv_budget(ok, None, fake, L * N + 1, 0, fake, fake, fake, None, s) == -4
+    assert lib.tgvkv_budget(ok, None, fake, -1, 0, fake, fake, fake, None, s) == -1
+    assert lib.tgvkv_budget(ok, None, fake, 10, -1, fake, fake, fake, None, s) == -1
+    assert lib.tgvkv_budget(ok, None, None, 10, 0, fake, fake, fake, None, s) == -1
     # vision-only eviction: the budget counts vision tokens, at most L * n_vis
     vo = ctypes.byref(bd.make_opts(vision_only=True))
     Nv = 40
-    assert lib.tgvkv_budget(ok, vo, fake, L * Nv + 1, 0, fake, fake, fake, s) == -4
-    assert lib.tgvkv_compact(ok, vo, fake, fake, fake, fake, fake, fake, L * Nv + 1, 0, fake, fake, s) == -4
+    assert lib.tgvkv_budget(ok, vo, fake, L * Nv + 1, 0, fake, fake, fake, None, s) == -4
+    assert lib.tgvkv_compact(ok, vo, fake, fake, fake, fake, fake, fake, L * Nv + 1, 0, fake, fake, None, s) == -4
     # select / compact / decode arguments
     assert lib.tgvkv_select(ok, None, fake, fake, None, fake, fake, s) == -1
     assert lib.tgvkv_select(ok, None, None, fake, fake, fake, fake, s) == -1
-    assert lib.tgvkv_compact(ok, None, fake, fake, fake, fake, fake, fake, L * N + 1, 0, fake, fake, s) == -4
-    assert lib.tgvkv_compact(ok, None, fake, fake, fake, fake, fake, fake, 10, 0, fake, None, s) == -1
-    assert lib.tgvkv_compact(ok, None, fake, odd, fake, fake, fake, fake, 10, 0, fake, fake, s) == -1
-    assert lib.tgvkv_decode_attn(ok, None, fake, fake, fake, fake, 4, 4, fake, fake, fake, fake, fake, big, s) == -4
-    assert lib.tgvkv_decode_attn(ok, None, fake, fake, fake, fake, 4, -1, fake, fake, fake, fake, fake, big, s) == -4
-    assert lib.tgvkv_decode_attn(ok, None, fake, fake, fake, fake, 4, 0, fake, fake, fake, None, fake, big, s) == -1
-    assert lib.tgvkv_decode_attn(ok, None, fake, fake, fake, fake, 4, 0, fake, fake, fake, fake, None, 0, s) == -3
+    assert lib.tgvkv_compact(ok, None, fake, fake, fake, fake, fake, fake, L * N + 1, 0, fake, fake, None, s) == -4
+    assert lib.tgvkv_compact(ok, None, fake, fake, fake, fake, fake, fake, 10, 0, fake, None, None, s) == -1
+    assert lib.tgvkv_compact(ok, None, fake, odd, fake, fake, fake, fake, 10, 0, fake, fake, None, s) == -1
+    dec = lambda step, kn, out, ws, n: lib.tgvkv_decode_attn(ok, None, fake, fake, fake, fake, 4, step, fake, kn, fake,
+                                                             out, ws, n, None, s)
+    assert dec(4, fake, fake, fake, big) == -4
+    assert dec(-1, fake, fake, fake, big) == -4
+    assert dec(0, fake, None, fake, big) == -1
+    assert dec(0, fake, fake, None, 0) == -3
 
 
 def _plan(problem, opts, total, reserve, page):
@@ -196,24 +198,25 @@ def test_paged_validation_before_any_launch(lib):
     assert lib.tgvkv_page_table(ok, None, fake, 10, 4, 8, fake, pool, fake, width, None, s) == -1
     assert lib.tgvkv_page_table(ok, None, fake, 2 * 48 + 1, 4, 8, fake, 999, fake, 64, fake, s) == -4
     # paged compaction: the table must hold b_max rows
-    assert lib.tgvkv_compact_paged(ok, None, fake, fake, fake, fake, fake, 10, fake, 1, 8, fake, fake, 64, s) == -4
-    assert lib.tgvkv_compact_paged(ok, None, fake, fake, fake, fake, fake, 10, fake, 2, 8, fake, fake, 0, s) == -1
-    assert lib.tgvkv_compact_paged(ok, None, fake, fake, fake, fake, fake, 10, fake, 2, 8, fake, odd, 64, s) == -1
-    assert lib.tgvkv_compact_paged(ok, None, fake, fake, fake, fake, fake, 10, None, 2, 8, fake, fake, 64, s) == -1
-    assert lib.tgvkv_compact_paged(ok, None, fake, fake, fake, fake, fake, 10, fake, 2, 5, fake, fake, 64, s) == -1
-    assert lib.tgvkv_compact_paged(ok, None, fake, fake, fake, fake, fake, 10, fake, 2, 8, fake, fake, 1 << 31,
-                                   s) == -2
+    cp = lambda table, width, page, vpool, n_pages: lib.tgvkv_compact_paged(
+        ok, None, fake, fake, fake, fake, fake, 10, table, width, page, fake, vpool, n_pages, None, s)
+    assert cp(fake, 1, 8, fake, 64) == -4
+    assert cp(fake, 2, 8, fake, 0) == -1
+    assert cp(fake, 2, 8, odd, 64) == -1
+    assert cp(None, 2, 8, fake, 64) == -1
+    assert cp(fake, 2, 5, fake, 64) == -1
+    assert cp(fake, 2, 8, fake, 1 << 31) == -2
     # paged decode: steps are required, workspace as for contiguous decode
     assert lib.tgvkv_decode_attn_paged(ok, None, fake, fake, 64, 8, fake, 2, fake, 4, None, fake, fake, fake, fake,
-                                       fake, big, s) == -1
+                                       fake, big, None, s) == -1
     assert lib.tgvkv_decode_attn_paged(ok, None, fake, fake, 64, 8, fake, 2, fake, 4, fake, fake, fake, fake, fake,
-                                       None, 0, s) == -3
+                                       None, 0, None, s) == -3
     assert lib.tgvkv_decode_attn_paged(ok, None, fake, fake, 64, 12, fake, 2, fake, 4, fake, fake, fake, fake, fake,
-                                       fake, big, s) == -1
+                                       fake, big, None, s) == -1
     assert lib.tgvkv_decode_attn_paged(ok, None, odd, fake, 64, 8, fake, 2, fake, 4, fake, fake, fake, fake, fake,
-                                       fake, big, s) == -1
+                                       fake, big, None, s) == -1
     assert lib.tgvkv_decode_attn_paged(ok, None, fake, fake, 64, 8, fake, 0, fake, 4, fake, fake, fake, fake, fake,
-                                       fake, big, s) == -1
+                                       fake, big, None, s) == -1
 
 
 def test_empty_batch_is_a_no_op(lib):
@@ -221,15 +224,15 @@ def test_empty_batch_is_a_no_op(lib):
     s = ctypes.c_void_p(0)
     assert lib.tgvkv_score(z, None, 7, None, ctypes.c_void_p(0x10000), None, None, None, None, None, None, None,
                            0, s) == 0
-    assert lib.tgvkv_budget(z, None, None, 5, 0, None, ctypes.c_void_p(0x10000), ctypes.c_void_p(0x10000), s) == 0
+    assert lib.tgvkv_budget(z, None, None, 5, 0, None, ctypes.c_void_p(0x10000), ctypes.c_void_p(0x10000), None, s) == 0
     assert lib.tgvkv_select(z, None, None, None, None, None, None, s) == 0
-    assert lib.tgvkv_compact(z, None, None, None, None, None, None, None, 5, 0, None, None, s) == 0
-    assert lib.tgvkv_decode_attn(z, None, None, None, None, None, 2, 0, None, None, None, None, None, 0, s) == 0
+    assert lib.tgvkv_compact(z, None, None, None, None, None, None, None, 5, 0, None, None, None, s) == 0
+    assert lib.tgvkv_decode_attn(z, None, None, None, None, None, 2, 0, None, None, None, None, None, 0, None, s) == 0
     used = ctypes.c_void_p(0x10000)
     assert lib.tgvkv_page_table(z, None, None, 5, 2, 4, None, 0, None, 8, used, s) == 0
-    assert lib.tgvkv_compact_paged(z, None, None, None, None, None, None, 5, None, 8, 4, None, None, 1, s) == 0
+    assert lib.tgvkv_compact_paged(z, None, None, None, None, None, None, 5, None, 8, 4, None, None, 1, None, s) == 0
     assert lib.tgvkv_decode_attn_paged(z, None, None, None, 1, 4, None, 8, None, 2, None, None, None, None, None,
-                                       None, 0, s) == 0
+                                       None, 0, None, s) == 0
 
 
 def test_binding_fails_loudly_without_library(tmp_path):

@@ -134,7 +134,8 @@ def _paged_matches_contiguous(cfg, rho, page, steps, seed, shuffle=True, **kw):
         q, kn, vn = (dev_bf16(x) for x in _decode_inputs(rng, B, L, H, Hkv, D))
         buf.decode(st, q, kn, vn)
         steps_d.fill_(st)
-        pool.decode(p, o, table, buf.budgets, steps, steps_d, q, kn, vn, out_p, buf.ws_decode)
+        pool.decode(p, o, table, buf.budgets, steps, steps_d, q, kn, vn, out_p, buf.ws_decode,
+                    unit_order=buf.unit_order if st % 2 else None)
         torch.cuda.synchronize()
         assert torch.equal(out_p, buf.out), f"step {st}: paged decode differs from contiguous"
     kc, vc = bf16_host_bits(buf.kc), bf16_host_bits(buf.vc)

@@ -42,6 +42,17 @@ def _mass_cases(rng, L):
     yield (rng.integers(1, 4, L) / 4).astype(np.float32)   # many equal fractions
 
 
+def _longest_first(budgets):
+    """Decode dispatch order: rank-major over sequences, each sequence's layers by (budget desc, layer asc)."""
+    B, L = budgets.shape
+    out = np.empty(B * L, np.int32)
+    for b in range(B):
+        ranks = sorted(range(L), key=lambda l: (-int(budgets[b, l]), l))
+        for r, l in enumerate(ranks):
+            out[r * B + b] = b * L + l
+    return out
+
+
 @pytest.mark.parametrize("budget_rule", [0, 1, 2])
 @pytest.mark.parametrize("L,N,n_sink,n_recent", [(32, 2979, 0, 0), (28, 8256, 4, 1), (5, 13, 0, 0),
                                                  (1, 168, 0, 0), (40, 3171, 4, 1), (7, 3, 1, 1)])
@@ -61,7 +72,8 @@ def test_budget_kernel_exact(lib, L, N, n_sink, n_recent, budget_rule):
             budgets = torch.empty((B, L), dtype=torch.int32, device="cuda")
             io = torch.empty(B * L + 1, dtype=torch.int64, device="cuda")
             so = torch.empty(B * L + 1, dtype=torch.int64, device="cuda")
-            bd.tgvkv_budget(p, o, tv, total, reserve, budgets, io, so)
+            order = torch.full((B * L,), -1, dtype=torch.int32, device="cuda")
+            bd.tgvkv_budget(p, o, tv, total, reserve, budgets, io, so, unit_order=order)
             torch.cuda.synchronize()
             gb = host(budgets)
             for b in range(B):
@@ -69,6 +81,7 @@ def test_budget_kernel_exact(lib, L, N, n_sink, n_recent, budget_rule):
                 assert np.array_equal(gb[b], ob), (b, total, gb[b], ob)
             assert np.array_equal(host(io), O.flat_offsets(gb.reshape(-1)))
             assert np.array_equal(host(so), O.flat_offsets(gb.reshape(-1) + reserve))
+            assert np.array_equal(host(order), _longest_first(gb))
 
 
 @pytest.mark.parametrize("L,ns,nv,nq,n_sink,n_recent", [(32, 35, 2880, 64, 0, 0), (28, 16, 8192, 48, 4, 1),
@@ -92,9 +105,11 @@ def test_budget_kernel_vision_only_exact(lib, L, ns, nv, nq, n_sink, n_recent):
             budgets = torch.empty((B, L), dtype=torch.int32, device="cuda")
             io = torch.empty(B * L + 1, dtype=torch.int64, device="cuda")
             so = torch.empty(B * L + 1, dtype=torch.int64, device="cuda")
-            bd.tgvkv_budget(p, o, tv, total, reserve, budgets, io, so)
+            order = torch.full((B * L,), -1, dtype=torch.int32, device="cuda")
+            bd.tgvkv_budget(p, o, tv, total, reserve, budgets, io, so, unit_order=order)
             torch.cuda.synchronize()
             gb = host(budgets)
+            assert np.array_equal(host(order), _longest_first(gb))
             for b in range(B):
                 ob = O.vision_only_budgets(masses[b].astype(np.float64), total, nt, nv, nfv)
                 assert np.array_equal(gb[b], ob), (b, total, gb[b], ob)
@@ -200,6 +215,15 @@ def test_compact_bit_exact(lib, head_mode, D):
                 assert np.array_equal(got_k, ck[h]) and np.array_equal(got_v, cv[h])
                 # reserved decode slots untouched
                 assert not hk[base + len(s) * D: base + cap * D].any()
+    # the same compaction dispatched in a shuffled unit order writes the same cache
+    kc2, vc2 = torch.zeros_like(kc), torch.zeros_like(vc)
+    perm = torch.from_numpy(rng.permutation(B * L).astype(np.int32)).cuda()
+    bd.tgvkv_compact(p, o, dev_bf16(k), dev_bf16(v), torch.from_numpy(idx).cuda(),
+                     torch.from_numpy(bud.astype(np.int32)).cuda(), torch.from_numpy(io).cuda(),
+                     torch.from_numpy(so).cuda(), total, reserve, kc2, vc2, unit_order=perm)
+    torch.cuda.synchronize()
+    # compare bit patterns: the random 16-bit rows include NaN encodings
+    assert np.array_equal(bf16_host_bits(kc2), hk) and np.array_equal(bf16_host_bits(vc2), hv)
 
 
 # ----------------------------------------------------------------------------- decode
@@ -228,10 +252,17 @@ def test_decode_kernel(lib, H, Hkv, D, B, L):
     d_so = torch.from_numpy(so).cuda()
     tau = 1.0 / np.sqrt(D)
     worst = 0.0
+    # a second copy of the cache decoded in a shuffled unit order must give the same bits
+    kc2, vc2 = kc.clone(), vc.clone()
+    out2 = torch.empty_like(out)
+    perm = torch.from_numpy(rng.permutation(B * L).astype(np.int32)).cuda()
     for t in range(T):
         bd.tgvkv_decode_attn(p, o, kc, vc, d_b, d_so, reserve, t, dev_bf16(q[t]), dev_bf16(kn[t]),
                              dev_bf16(vn[t]), out, ws)
+        bd.tgvkv_decode_attn(p, o, kc2, vc2, d_b, d_so, reserve, t, dev_bf16(q[t]), dev_bf16(kn[t]),
+                             dev_bf16(vn[t]), out2, ws, unit_order=perm)
         torch.cuda.synchronize()
+        assert torch.equal(out, out2), "decode output depends on the dispatch order"
         got = host(out)
         for b in range(B):
             for l in range(L):
@@ -259,6 +290,7 @@ def test_decode_kernel(lib, H, Hkv, D, B, L):
             for h in range(Hkv):
                 base = (int(so[bl]) * Hkv + h * cap + n) * D
                 assert np.array_equal(hk[base: base + T * D].reshape(T, D), kn[:, b, l, h])
+    assert torch.equal(kc, kc2) and torch.equal(vc, vc2)
     log(f"decode H={H} Hkv={Hkv} D={D}: max abs err {worst:.2e}")
 
 

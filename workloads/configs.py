@@ -33,6 +33,7 @@ class WorkloadConfig:
     rhos: Tuple[float, ...] = (0.05,)
     decode_steps: int = 1
     fp32_data: bool = False         # the tiny case is specified in fp32
+    tv_gap: float = 0.0             # >0: depth of the text-to-vision logit gap across layers (see gen)
 
     @property
     def n_tokens(self) -> int:
@@ -57,17 +58,17 @@ CONFIGS = {
                            rhos=(0.10, 0.50, 1.0), decode_steps=1, fp32_data=True),
     # LLaVA-1.5-7B: 32 layers, 32 MHA heads, 35 + 576 + 40 tokens.
     "llava15": WorkloadConfig("llava15", 1, 32, 32, 32, 128, 35, 576, 40, vis_sigma=0.3,
-                              rhos=(0.05, 0.10, 0.20), decode_steps=64),
+                              rhos=(0.05, 0.10, 0.20), decode_steps=64, tv_gap=6.0),
     # LLaVA-NeXT-7B with 5 image tiles: batch 4, 35 + 2880 + 64 tokens.
     "llavanext": WorkloadConfig("llavanext", 4, 32, 32, 32, 128, 35, 2880, 64, vis_sigma=0.25,
-                                rhos=(0.05,), decode_steps=128),
+                                rhos=(0.05,), decode_steps=128, tv_gap=6.0),
     # Qwen2-VL-7B GQA video: 28 layers, 28 query heads over 4 KV heads, 16 frames x 512.
     "qwen2vl_video": WorkloadConfig("qwen2vl_video", 8, 28, 28, 4, 128, 16, 8192, 48,
                                     vis_sigma=0.3, frames=16, frame_alpha=0.1,
-                                    rhos=(0.05, 0.10), decode_steps=128),
+                                    rhos=(0.05, 0.10), decode_steps=128, tv_gap=6.0),
     # 13B-class stress: 40 layers, 40 heads, batch 16, 35 + 2880 + 256 tokens.
     "stress13b": WorkloadConfig("stress13b", 16, 40, 40, 40, 128, 35, 2880, 256, vis_sigma=0.3,
-                                rhos=(0.05,), decode_steps=256),
+                                rhos=(0.05,), decode_steps=256, tv_gap=6.0),
 }
 
 # Ordered as the configs are listed: tiny first, then the four model shapes.
@@ -81,11 +82,11 @@ def get_config(name: str) -> WorkloadConfig:
 def custom_config(name: str = "custom", *, batch=1, layers=2, heads_q=4, heads_kv=2,
                   head_dim=128, n_sys=5, n_vis=100, n_qst=11, vis_sigma=0.3, sink=True,
                   frames=0, rhos=(0.2,), decode_steps=2, fp32_data=False,
-                  frame_alpha=0.1) -> WorkloadConfig:
+                  frame_alpha=0.1, tv_gap=0.0) -> WorkloadConfig:
     """A small shape for parity tests: spans several kernel tiles with ragged tails."""
     return WorkloadConfig(name, batch, layers, heads_q, heads_kv, head_dim, n_sys, n_vis, n_qst,
                           vis_sigma=vis_sigma, sink=sink, frames=frames, frame_alpha=frame_alpha,
-                          rhos=tuple(rhos), decode_steps=decode_steps, fp32_data=fp32_data)
+                          rhos=tuple(rhos), decode_steps=decode_steps, fp32_data=fp32_data, tv_gap=tv_gap)
 
 
 def with_shape(cfg: WorkloadConfig, **changes) -> WorkloadConfig:

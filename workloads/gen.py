@@ -16,6 +16,14 @@ Recipes (per sequence b and layer l):
   with ``frames > 0`` each frame has its own mean, drawn as an AR(1) walk
   ``mu_f = sqrt(1 - a^2) mu_{f-1} + a eps_f`` whose marginals stay N(0, I);
 * token 0's key is scaled by ``sink_scale`` (an attention sink);
+* with ``tv_gap > 0``, the layers' text-to-vision attention differs by depth:
+  each question-row query of layer l gets ``c * mu`` added (mu the mean vision
+  key of its KV head, averaged over frames), with c chosen so that every vision
+  logit of the row moves by ``s_l`` on average,
+  ``s_l = -tv_gap * (1 - 0.85 exp(-x / 0.08) - 0.25 x) + 0.5 z``, x = l / (L - 1),
+  z ~ N(0, 1) per (sequence, layer).  Shallow layers then put much of a
+  question row's mass on the image and middle layers very little (the modality
+  gap), so TVB's layer budgets spread out as the paper describes;
 * values, decode queries and decode keys/values: i.i.d. N(0, 1).
 """
 
@@ -29,7 +37,7 @@ import numpy as np
 
 from .configs import WorkloadConfig, frame_size
 
-_NAME_ID = {"k": 1, "v": 2, "q_text": 3, "vis_mean": 4, "dec_q": 5, "dec_k": 6, "dec_v": 7}
+_NAME_ID = {"k": 1, "v": 2, "q_text": 3, "vis_mean": 4, "dec_q": 5, "dec_k": 6, "dec_v": 7, "tv_shift": 8}
 
 
 def _rng(seed: int, name: str, *idx: int) -> np.random.Generator:
@@ -95,10 +103,26 @@ def gen_v_slice(cfg: WorkloadConfig, seed: int, b: int, l: int) -> np.ndarray:
     return rng.standard_normal((cfg.heads_kv, cfg.n_tokens, cfg.head_dim), dtype=np.float32)
 
 
+def vision_logit_shift(cfg: WorkloadConfig, seed: int, b: int, l: int) -> float:
+    """Mean shift s_l of the question rows' vision logits in layer l (0 unless tv_gap > 0)."""
+    if cfg.tv_gap <= 0 or cfg.n_vis == 0:
+        return 0.0
+    x = l / max(cfg.layers - 1, 1)
+    z = float(_rng(seed, "tv_shift", b, l).standard_normal())
+    return -cfg.tv_gap * (1.0 - 0.85 * np.exp(-x / 0.08) - 0.25 * x) + 0.5 * z
+
+
 def gen_qtext_slice(cfg: WorkloadConfig, seed: int, b: int, l: int) -> np.ndarray:
     """Text-row queries of one (sequence, layer): fp32 [H][N_t][d] in text order (system, then question)."""
     rng = _rng(seed, "q_text", b, l)
-    return rng.standard_normal((cfg.heads_q, cfg.n_text, cfg.head_dim), dtype=np.float32)
+    q = rng.standard_normal((cfg.heads_q, cfg.n_text, cfg.head_dim), dtype=np.float32)
+    shift = vision_logit_shift(cfg, seed, b, l)
+    if shift != 0.0 and cfg.n_qst > 0:
+        mu = _vision_means(cfg, seed, b, l).mean(axis=1)  # [H_kv][d]
+        c = shift * np.sqrt(cfg.head_dim) / np.sum(mu * mu, axis=-1)  # q.mu / sqrt(d) moves by shift
+        add = np.repeat((c[:, None] * mu).astype(np.float32), cfg.group, axis=0)  # query head h -> KV head h / G
+        q[:, cfg.n_sys:] += add[:, None, :]
+    return q
 
 
 def gen_decode_slice(cfg: WorkloadConfig, seed: int, b: int, l: int, steps: int):
