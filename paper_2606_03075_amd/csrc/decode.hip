@@ -7,9 +7,10 @@
 //   * one workgroup per (sequence, layer, KV head[, split]): the KV head's rows
 //     are read once and serve all query heads that share it (GQA);
 //   * a token row of head_dim bf16 is read by head_dim/8 lanes with 16-byte
-//     non-temporal loads; each lane group handles 8 tokens per iteration (4 when
-//     a KV head serves more than 2 query heads, to bound registers) with all of
-//     their K and V loads issued before any math;
+//     non-temporal loads; each lane group works on blocks of 4 tokens from two
+//     register buffers, issuing the next block's K and V loads before consuming
+//     the current one (a trip count that is uniform over the workgroup and even,
+//     with every load unconditional, so the compiler's waits stay per block);
 //   * online softmax per lane group, merged across groups with wave shuffles and
 //     across the 4 waves through LDS; when the (sequence, layer, KV head) count is
 //     too small to fill the GPU the token range is split and a second kernel
@@ -54,7 +55,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(Shape s, Rows rows, ui
     constexpr int LPR = D / 8;         // lanes per token row
     constexpr int GPW = 64 / LPR;      // lane groups per wave
     constexpr int NGRP = 4 * GPW;      // lane groups per workgroup
-    constexpr int kUnroll = GMAX <= 2 ? 8 : 4;  // tokens in flight per lane group
+    constexpr int kUnroll = 4;  // tokens per lane group in each of the two register buffers
     __shared__ float wm[4][GMAX], wl[4][GMAX];
     __shared__ float wacc[4][GMAX][D];
     extern __shared__ int lds_pages[];  // paged layout: the unit's page ids
@@ -112,20 +113,23 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(Shape s, Rows rows, ui
         for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
     }
 
-    for (int n0 = t0 + grp; n0 < t1; n0 += NGRP * kUnroll) {
-        u32x4 kr[kUnroll], vr[kUnroll];
-        bool ok[kUnroll];
+    constexpr int S = NGRP * kUnroll;
+    // loads of one block of kUnroll tokens per lane group; rows past t1 (and the step's own
+    // token) read the fresh k_new / v_new row, so every load is unconditional
+    auto issue = [&](u32x4 (&kr)[kUnroll], u32x4 (&vr)[kUnroll], int n0) {
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
             const int n = n0 + u * NGRP;
-            ok[u] = n < t1;
-            const bool fresh = n >= len - 1 || !ok[u];
+            const bool fresh = n >= len - 1 || n >= t1;
             const size_t r = fresh ? 0 : rows.row(n);
-            const uint16_t* kp = fresh ? knew : kc + r;
-            const uint16_t* vp = fresh ? vnew : vc + r;
-            kr[u] = load16_stream(kp + sub * 8);
-            vr[u] = load16_stream(vp + sub * 8);
+            kr[u] = load16_stream((fresh ? knew : kc + r) + sub * 8);
+            vr[u] = load16_stream((fresh ? vnew : vc + r) + sub * 8);
         }
+    };
+    auto consume = [&](const u32x4 (&kr)[kUnroll], const u32x4 (&vr)[kUnroll], int n0) {
+        bool ok[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) ok[u] = n0 + u * NGRP < t1;
 #pragma unroll
         for (int h = 0; h < GMAX; ++h) {
             if (h >= G) continue;
@@ -160,6 +164,19 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(Shape s, Rows rows, ui
                 for (int e = 0; e < 8; ++e) acc[h][e] += p * vf[e];
             }
         }
+    };
+    // two register buffers: the next block's loads are in flight while this block is consumed;
+    // the trip count is uniform over the workgroup and even (the extra half only masks)
+    const int pairs = (t1 - t0 + 2 * S - 1) / (2 * S);
+    u32x4 ka[kUnroll], va[kUnroll], kb[kUnroll], vb[kUnroll];
+    int n0 = t0 + grp;
+    issue(ka, va, n0);
+    for (int pi = 0; pi < pairs; ++pi) {
+        issue(kb, vb, n0 + S);
+        consume(ka, va, n0);
+        issue(ka, va, n0 + 2 * S);
+        consume(kb, vb, n0 + S);
+        n0 += 2 * S;
     }
 
     // merge the lane groups of the wave

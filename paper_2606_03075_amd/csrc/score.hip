@@ -405,6 +405,15 @@ hipError_t launch_score_vision(const Shape& s, const RowPlan& rp, const uint16_t
     if (ws_vm != nullptr) {
         if (s.D == 128) TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 128, true, rp, grid, block, 0, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm);
         else TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 64, true, rp, grid, block, 0, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm);
+    } else if (rp.nslot == 1 && rp.ks == 1) {
+        // four 16-row blocks per unit: the vision sweep runs faster with every wave holding all
+        // four blocks over a quarter of each key tile (same row groups, so the same partials)
+        if (s.D == 128)
+            hipLaunchKernelGGL((score_vision_kernel<128, 4, 4, false>), grid, block, 0, st, s, rp.rowgroups, q_text, k,
+                               lse, w_txt, budgets, vis_threshold, ws_part, ws_vm);
+        else
+            hipLaunchKernelGGL((score_vision_kernel<64, 4, 4, false>), grid, block, 0, st, s, rp.rowgroups, q_text, k,
+                               lse, w_txt, budgets, vis_threshold, ws_part, ws_vm);
     } else {
         if (s.D == 128) TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 128, false, rp, grid, block, 0, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm);
         else TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 64, false, rp, grid, block, 0, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm);

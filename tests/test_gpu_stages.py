@@ -308,6 +308,11 @@ SCORE_SHAPES = {
                                n_qst=40),
     "long_text": custom_config(batch=1, layers=1, heads_q=2, heads_kv=2, head_dim=128, n_sys=35, n_vis=200,
                                n_qst=300),
+    # four 16-row blocks per KV head (the vision sweep's own launch shape)
+    "four_blocks": custom_config(batch=2, layers=2, heads_q=4, heads_kv=4, head_dim=128, n_sys=7, n_vis=333,
+                                 n_qst=61),
+    "four_blocks_gqa_d64": custom_config(batch=1, layers=2, heads_q=8, heads_kv=4, head_dim=64, n_sys=3, n_vis=201,
+                                         n_qst=29),
 }
 
 
