@@ -218,11 +218,11 @@ __global__ __launch_bounds__(kThreads) void score_vision_kernel(Shape s, int row
                                                                 const int32_t* __restrict__ budgets,
                                                                 int vis_threshold,
                                                                 float* __restrict__ ws_part,
-                                                                float* __restrict__ ws_vm) {
+                                                                float* __restrict__ ws_vm, int out_tiles) {
     constexpr int RSETS = 4 / KS;
     __shared__ __attribute__((aligned(16))) char tiles[2][Geo<D>::TILE_BYTES];
     __shared__ float red[2][RSETS][kTile];
-    __shared__ float obuf[kOutTiles * kTile];
+    extern __shared__ float obuf[];  // out_tiles * kTile scores
     int bid = blockIdx.x;
     const int rg = bid % rowgroups;
     bid /= rowgroups;
@@ -250,7 +250,8 @@ __global__ __launch_bounds__(kThreads) void score_vision_kernel(Shape s, int row
     const uint16_t* kvis = k + (((size_t)bl * s.Hkv + kvh) * (size_t)s.N + s.Ns) * D;
     float* out = ws_part + (((size_t)bl * s.Hkv + kvh) * rowgroups + rg) * (size_t)s.Nv;
     float rsum[NSLOT][4];
-    vision_sweep<D, NSLOT, KS, MASS>(s, kvis, 0, s.Nv, qf, lse2, coef, rb0, NB, tiles, red, obuf, out, rsum);
+    vision_sweep<D, NSLOT, KS, MASS>(s, kvis, 0, s.Nv, qf, lse2, coef, rb0, NB, tiles, red, obuf, out_tiles, out,
+                                     rsum);
     if (MASS) {
         // each row's vision mass: the sum of its probabilities over all vision keys
         const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -402,21 +403,27 @@ hipError_t launch_score_vision(const Shape& s, const RowPlan& rp, const uint16_t
     const long long nblk = (long long)s.B * s.L * s.Hkv * rp.rowgroups;
     if (nblk == 0 || s.Nv == 0) return hipSuccess;
     dim3 grid((unsigned)nblk), block(kThreads);
-    if (ws_vm != nullptr) {
-        if (s.D == 128) TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 128, true, rp, grid, block, 0, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm);
-        else TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 64, true, rp, grid, block, 0, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm);
+    // a unit's scores are kept in LDS and written once at the end when they fit (no global
+    // store among the key loads); otherwise in bursts of kOutTiles tiles
+    const int ntiles = (s.Nv + kTile - 1) / kTile;
+    const bool mass = ws_vm != nullptr;
+    const int out_tiles = (!mass && ntiles * kTile * (int)sizeof(float) <= kWholeOutBytes) ? ntiles : kOutTiles;
+    const size_t obytes = (size_t)out_tiles * kTile * sizeof(float);
+    if (mass) {
+        if (s.D == 128) TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 128, true, rp, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles);
+        else TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 64, true, rp, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles);
     } else if (rp.nslot == 1 && rp.ks == 1) {
         // four 16-row blocks per unit: the vision sweep runs faster with every wave holding all
         // four blocks over a quarter of each key tile (same row groups, so the same partials)
         if (s.D == 128)
-            hipLaunchKernelGGL((score_vision_kernel<128, 4, 4, false>), grid, block, 0, st, s, rp.rowgroups, q_text, k,
-                               lse, w_txt, budgets, vis_threshold, ws_part, ws_vm);
+            hipLaunchKernelGGL((score_vision_kernel<128, 4, 4, false>), grid, block, obytes, st, s, rp.rowgroups,
+                               q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles);
         else
-            hipLaunchKernelGGL((score_vision_kernel<64, 4, 4, false>), grid, block, 0, st, s, rp.rowgroups, q_text, k,
-                               lse, w_txt, budgets, vis_threshold, ws_part, ws_vm);
+            hipLaunchKernelGGL((score_vision_kernel<64, 4, 4, false>), grid, block, obytes, st, s, rp.rowgroups,
+                               q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles);
     } else {
-        if (s.D == 128) TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 128, false, rp, grid, block, 0, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm);
-        else TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 64, false, rp, grid, block, 0, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm);
+        if (s.D == 128) TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 128, false, rp, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles);
+        else TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 64, false, rp, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles);
     }
     return hipGetLastError();
 }

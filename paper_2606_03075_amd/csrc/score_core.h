@@ -27,6 +27,7 @@ namespace core {
 constexpr int kThreads = 256;
 constexpr int kTile = 64;  // keys per LDS tile
 constexpr int kOutTiles = 8;  // vision-score tiles buffered in LDS per burst of global writes
+constexpr int kWholeOutBytes = 16384;  // up to this many bytes of a unit's scores are written once, at the end
 
 template <int D>
 struct Geo {
@@ -347,7 +348,8 @@ __device__ __forceinline__ void load_row_coefs(const Shape& s, int bl, int kvh, 
 // Vision sweep over vision keys [vbeg, vend) (vbeg a multiple of kTile; kvis
 // points at the first vision key of the unit): out[j] = sum over this
 // workgroup's rows of coef * exp(z - lse), for every key j of the range.
-// obuf: kOutTiles * kTile floats of LDS.  With MASS the sweep also sums each
+// obuf: out_tiles * kTile floats of LDS; scores are written in bursts of
+// out_tiles tiles (all of them at the end when out_tiles covers the range).  With MASS the sweep also sums each
 // row's probabilities over the range (its vision mass when the range is all
 // vision keys): on return rsum[sl][j] of the key-part-0 waves holds the sum of
 // accumulator row 4*(lane/16) + j of slot sl, in every lane of the 16.
@@ -355,7 +357,8 @@ template <int D, int NSLOT, int KS, bool MASS = false>
 __device__ void vision_sweep(const Shape& s, const uint16_t* kvis, int vbeg, int vend,
                              const bf16x8 (&qf)[NSLOT][Geo<D>::KSTEPS], const float (&lse2)[NSLOT][4],
                              const float (&coef)[NSLOT][4], int rb0, int NB, char (*tiles)[Geo<D>::TILE_BYTES],
-                             float (*red)[4 / KS][kTile], float* obuf, float* out, float (&rsum)[NSLOT][4]) {
+                             float (*red)[4 / KS][kTile], float* obuf, int out_tiles, float* out,
+                             float (&rsum)[NSLOT][4]) {
     using GG = Geo<D>;
     constexpr int RSETS = 4 / KS;
     constexpr int KBW = 4 / KS;
@@ -398,16 +401,16 @@ __device__ void vision_sweep(const Shape& s, const uint16_t* kvis, int vbeg, int
         },
         [&](int, int t) {
             // Each of the first 64 threads parks its key's score in its own LDS slot and
-            // writes kOutTiles of them at once, then waits for the writes: a global store
+            // writes out_tiles of them at once, then waits for the writes: a global store
             // pending among the tile loads would make the compiler drain every load in
-            // flight at each tile, not once per kOutTiles tiles.
+            // flight at each tile, not once per out_tiles tiles.
             if (tid < kTile) {
                 float a = 0.f;
 #pragma unroll
                 for (int r = 0; r < RSETS; ++r) a += red[t & 1][r][tid];
-                const int slot = t % kOutTiles;
+                const int slot = t % out_tiles;
                 obuf[slot * kTile + tid] = a;
-                if (slot == kOutTiles - 1 || t == ntiles - 1) {
+                if (slot == out_tiles - 1 || t == ntiles - 1) {
                     for (int i = 0; i <= slot; ++i) {
                         const int key = vbeg + (t - slot + i) * kTile + tid;
                         if (key < vend) out[key] = obuf[i * kTile + tid];

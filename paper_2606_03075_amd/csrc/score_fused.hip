@@ -217,7 +217,7 @@ __global__ __launch_bounds__(kThreads) void score_fused_kernel(
                     const int vb = sp * fp.cv, ve = min(s.Nv, vb + fp.cv);
                     float* out = s.head_mode == 0 ? ws_part + (size_t)u * s.Nv : s_vis + (size_t)u * s.Nv;
                     float rsum_unused[NSLOT][4];
-                    vision_sweep<D, NSLOT, KS>(s, kvis, vb, ve, qf, lse2, coef, 0, NB, tiles, red, obuf, out,
+                    vision_sweep<D, NSLOT, KS>(s, kvis, vb, ve, qf, lse2, coef, 0, NB, tiles, red, obuf, kOutTiles, out,
                                                rsum_unused);
                 }
                 if (s.head_mode == 0) {
