@@ -84,7 +84,7 @@ __global__ __launch_bounds__(kThreads) void score_stats_text_kernel(Shape s, con
                                                                     float* __restrict__ lse,
                                                                     float* __restrict__ ws_vm,
                                                                     float* __restrict__ ws_colsum,
-                                                                    float* __restrict__ ws_vmh) {
+                                                                    float* __restrict__ ws_vmh, int lds_text) {
     constexpr int RSETS = 4 / KS;
     __shared__ __attribute__((aligned(16))) char tiles[2][Geo<D>::TILE_BYTES];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -127,7 +127,13 @@ __global__ __launch_bounds__(kThreads) void score_stats_text_kernel(Shape s, con
         for (int qi = 0; qi < s.Nq; ++qi) a += vms[tid * s.Nq + qi];
         ws_vmh[head0 + tid] = a;
     }
-    text_pass<D>(s, bl, kvh, q_text, k, lse, lse2s, ws_colsum);
+    if (lds_text) {
+        // the unit's text keys go into the freed tiles after the normalisers and masses
+        const size_t off = ((size_t)s.G * (s.Nt + s.Nq) * sizeof(float) + 15) & ~(size_t)15;
+        text_pass_lds<D>(s, bl, kvh, q_text, k, lse, lse2s, &tiles[0][0] + off, ws_colsum);
+    } else {
+        text_pass<D>(s, bl, kvh, q_text, k, lse, lse2s, ws_colsum);
+    }
 }
 
 template <int D>
@@ -354,12 +360,17 @@ hipError_t launch_score_stats_text(const Shape& s, const RowPlan& rp, const uint
     const long long nblk = (long long)s.B * s.L * s.Hkv;
     if (nblk == 0) return hipSuccess;
     dim3 grid((unsigned)nblk), block(kThreads);
-    if (s.D == 128)
+    // the text pass stages the unit's text keys in the freed key tiles when they fit there
+    const long long head = ((long long)s.G * (s.Nt + s.Nq) * 4 + 15) / 16 * 16;
+    if (s.D == 128) {
+        const int lds_text = head + text_lds_bytes<128>(s.G, s.Nt) <= 2LL * Geo<128>::TILE_BYTES;
         TGVKV_ROWPLAN_DISPATCH(score_stats_text_kernel, 128, rp, grid, block, 0, st, s, q_text, k, lse, ws_vm,
-                               ws_colsum, ws_vmh);
-    else
+                               ws_colsum, ws_vmh, lds_text);
+    } else {
+        const int lds_text = head + text_lds_bytes<64>(s.G, s.Nt) <= 2LL * Geo<64>::TILE_BYTES;
         TGVKV_ROWPLAN_DISPATCH(score_stats_text_kernel, 64, rp, grid, block, 0, st, s, q_text, k, lse, ws_vm,
-                               ws_colsum, ws_vmh);
+                               ws_colsum, ws_vmh, lds_text);
+    }
     return hipGetLastError();
 }
 

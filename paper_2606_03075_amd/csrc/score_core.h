@@ -559,6 +559,159 @@ __device__ void text_pass(const Shape& s, int bl, int kvh, const uint16_t* __res
     __syncthreads();
 }
 
+// LDS bytes text_pass_lds needs beyond the [G][N_t] normalisers and [G][N_q] vision
+// masses that precede it: the unit's text keys (16-row blocks, padded rows) and one
+// column-sum partial per wave and query head.
+template <int D>
+__host__ __device__ constexpr long long text_lds_bytes(int G, int Nt) {
+    return (long long)((Nt + 15) / 16) * 16 * Geo<D>::ROWB + 4LL * G * ((Nt + 15) / 16) * 16 * (long long)sizeof(float);
+}
+
+// The text pass of text_pass with the unit's text keys staged in LDS first (one
+// round of loads by the whole workgroup), for units whose text keys fit beside the
+// normalisers in the freed key tiles.  Each wave then owns 16-row blocks of text
+// rows: it fetches a block's query fragments from global memory (the next item's
+// while the current one is used) and reads every key block it needs from LDS, so
+// the pass costs a few load latencies instead of one per (row block, key block).
+// Column sums: per (row block, key block) the 16 rows' probabilities are summed
+// across the lane groups and added to the wave's own LDS partial for those keys;
+// the four waves' partials are then added in wave order.  lse2s holds [G][N_t]
+// base-2 normalisers (the question rows' on entry); kl points at 16-byte aligned
+// LDS of text_lds_bytes<D>(G, N_t) bytes.
+template <int D>
+__device__ void text_pass_lds(const Shape& s, int bl, int kvh, const uint16_t* __restrict__ q_text,
+                              const uint16_t* __restrict__ k, float* __restrict__ lse, float* lse2s, char* kl,
+                              float* __restrict__ ws_colsum) {
+    using GG = Geo<D>;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const size_t head0 = (size_t)bl * s.H + kvh * s.G;
+    const uint16_t* kbase = k + ((size_t)bl * s.Hkv + kvh) * (size_t)s.N * D;
+    const int TB = (s.Nt + 15) >> 4;
+    const int TK = TB * 16;                                       // staged key rows (last one repeated)
+    float* part = reinterpret_cast<float*>(kl + (size_t)TK * GG::ROWB);  // [4 waves][G][TK]
+
+    // stage the text keys (text order: system keys, then question keys) and clear the partials
+    constexpr int kStage = 8;  // 16-byte loads in flight per thread
+    for (int c0 = 0; c0 < TK * GG::CPR; c0 += kStage * kThreads) {
+        u32x4 r[kStage];
+#pragma unroll
+        for (int i = 0; i < kStage; ++i) {
+            const int c = min(c0 + i * kThreads + tid, TK * GG::CPR - 1);
+            const int t = min(c / GG::CPR, s.Nt - 1);
+            const int pos = t < s.Ns ? t : t + s.Nv;
+            r[i] = load16(kbase + (size_t)pos * D + (c % GG::CPR) * 8);
+        }
+#pragma unroll
+        for (int i = 0; i < kStage; ++i) {
+            const int c = c0 + i * kThreads + tid;
+            if (c < TK * GG::CPR) store16(kl + (c / GG::CPR) * GG::ROWB + (c % GG::CPR) * 16, r[i]);
+        }
+    }
+    for (int x = tid; x < 4 * s.G * TK; x += kThreads) part[x] = 0.f;
+    __syncthreads();
+
+    const int koff = (lane >> 4) * 8;
+    auto load_q = [&](bf16x8 (&f)[GG::KSTEPS], int g, int row) {
+        const uint16_t* src = q_text + ((head0 + g) * s.Nt + row) * D + koff;
+#pragma unroll
+        for (int ks = 0; ks < GG::KSTEPS; ++ks) f[ks] = as_bf16x8(load16(src + ks * 32));
+    };
+
+    // system rows x system keys: row normalisers (C[key][row]: a lane owns row i)
+    const int SB = (s.Ns + 15) >> 4;
+    for (int item = wave; item < s.G * SB; item += 4) {
+        const int g = item / SB, rb = item % SB;
+        const int i = rb * 16 + (lane & 15);
+        bf16x8 qf[GG::KSTEPS];
+        load_q(qf, g, min(i, s.Ns - 1));
+        float m = kNegInf, l = 0.f;
+        for (int kb = 0; kb <= rb; ++kb) {
+            bf16x8 kf[GG::KSTEPS];
+            load_kfrag<D>(kf, kl, kb, lane);
+            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(kf[ks], qf[ks], acc);
+            float z[4];
+            float mx = kNegInf;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int key = kb * 16 + (lane >> 4) * 4 + j;
+                z[j] = (key <= i && key < s.Ns) ? acc[j] * s.scale2 : kNegInf;
+                mx = fmaxf(mx, z[j]);
+            }
+            if (mx > m) {
+                l *= fast_exp2(m - mx);
+                m = mx;
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (z[j] != kNegInf) l += fast_exp2(z[j] - m);
+        }
+        float dummy = 0.f;
+#pragma unroll
+        for (int off = 16; off < 64; off <<= 1) {
+            const float m2 = shfl_xor(m, off), l2 = shfl_xor(l, off), d2 = shfl_xor(dummy, off);
+            merge_stats(m, l, dummy, m2, l2, d2);
+        }
+        if (lane < 16 && i < s.Ns) {
+            const float L2 = m + log2f(l);
+            lse2s[g * s.Nt + i] = L2;
+            lse[(head0 + g) * s.Nt + i] = L2 * kLn2;
+        }
+    }
+    __syncthreads();
+
+    // all text rows x text keys (C[row][key]: a lane owns key j, rows 4*(lane/16) + jj)
+    const int items = s.G * TB;
+    bf16x8 qa[GG::KSTEPS], qb[GG::KSTEPS];
+    auto item_row = [&](int item) { return min((item % TB) * 16 + (lane & 15), s.Nt - 1); };
+    auto consume = [&](const bf16x8 (&qf)[GG::KSTEPS], int item) {
+        const int g = item / TB, rb = item % TB;
+        float* wpart = part + ((size_t)wave * s.G + g) * TK;
+        float l2[4];
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) l2[jj] = lse2s[g * s.Nt + min(rb * 16 + (lane >> 4) * 4 + jj, s.Nt - 1)];
+        for (int kb = 0; kb <= rb; ++kb) {
+            bf16x8 kf[GG::KSTEPS];
+            load_kfrag<D>(kf, kl, kb, lane);
+            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(qf[ks], kf[ks], acc);
+            const int j = kb * 16 + (lane & 15);
+            float col = 0.f;
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+                const int ii = rb * 16 + (lane >> 4) * 4 + jj;
+                if (ii < s.Nt && j <= ii) col += fast_exp2(acc[jj] * s.scale2 - l2[jj]);
+            }
+            col = sum_xor32(sum_xor16(col));
+            if (lane < 16) wpart[j] += col;
+        }
+    };
+    // every wave runs the same (even) number of steps; an item past the last is a no-op
+    const int steps = (items + 3) / 4;
+    int item = wave;
+    load_q(qa, (min(item, items - 1)) / TB, item_row(min(item, items - 1)));
+    for (int st = 0; st < steps; st += 2) {
+        const int nx = item + 4;
+        load_q(qb, min(nx, items - 1) / TB, item_row(min(nx, items - 1)));
+        if (item < items) consume(qa, item);
+        const int nx2 = item + 8;
+        load_q(qa, min(nx2, items - 1) / TB, item_row(min(nx2, items - 1)));
+        if (nx < items) consume(qb, nx);
+        item = nx2;
+    }
+    __syncthreads();
+    for (int x = tid; x < s.G * s.Nt; x += kThreads) {
+        const int g = x / s.Nt, j = x % s.Nt;
+        float a = 0.f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) a += part[((size_t)w * s.G + g) * TK + j];
+        ws_colsum[(head0 + g) * s.Nt + j] = a;
+    }
+    __syncthreads();
+}
+
 // Column sums of the text->text probabilities for one 16-key block kb of query
 // head g of a unit, by one wave, with every text row's normaliser given (natural
 // log, lse [.., N_t] of the head): the items of a unit are independent, so each
