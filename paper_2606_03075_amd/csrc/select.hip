@@ -7,8 +7,11 @@
 // 32-bit keys (4 passes of 8 bits with an LDS histogram; the digit holding the
 // k-th key is found by a wave-wide scan of the histogram), which yields the k-th
 // largest key and how many of its ties to take; ties go to the lower position.
-// A single ordered scan over all N positions then emits the retained positions
-// already in ascending order, with no sort.  Without TPR (an ablation of Table 5)
+// One ordered pass over the positions, 1024 at a time, then emits the retained
+// positions already in ascending order, with no sort: within a pass the ranks of
+// ties and of kept positions come from wave ballots and per-wave totals in LDS.
+// The workgroup has 1024 threads: the work is a few latency-bound rounds per
+// (sequence, layer, group), and there are few such units.  Without TPR (an ablation of Table 5)
 // all non-forced positions compete on one scale: text by s^T, vision by s^V times
 // a factor (N_t under TWR, whose weights sum to 1).  Candidate keys are read from global
 // memory once and kept in LDS when the row fits (N <= kLdsKeys).
@@ -18,7 +21,8 @@
 namespace tgvkv {
 namespace {
 
-constexpr int kThreads = 256;
+constexpr int kThreads = 1024;
+constexpr int kWaves = kThreads / 64;
 constexpr int kLdsKeys = 12288;  // 48 KB of LDS keys per workgroup
 enum { MODE_FORCED = 0, MODE_TEXT = 1, MODE_VIS = 2, MODE_JOINT = 3 };
 constexpr uint32_t kNotCand = 0u;  // keys of real candidates have the top bit or are >= 1
@@ -37,9 +41,10 @@ struct RowCtx {
         if (mode == MODE_JOINT) return true;
         return mode == MODE_VIS ? is_vis(p) : !is_vis(p);
     }
-    // key of a candidate (only called when cand(p))
+    // key of a candidate (only called when cand(p)); never kNotCand for finite scores.  The
+    // forced positions all get one key, so the ties-to-lower-position rule takes the first ones.
     __device__ uint32_t key(int p) const {
-        if (mode == MODE_FORCED) return 0u;
+        if (mode == MODE_FORCED) return 1u;
         if (mode == MODE_VIS) return ordered_key(sv[p - Ns]);
         if (mode == MODE_JOINT && is_vis(p)) return ordered_key(sv[p - Ns] * vscale);
         return ordered_key(st[p < Ns ? p : p - Nv]);
@@ -51,29 +56,6 @@ struct RowCtx {
         return mode == MODE_VIS && !is_vis(p);
     }
 };
-
-// Exclusive scan of one int per thread across the block; the total goes to *tot.
-__device__ int block_exclusive_scan(int v, int* tot, int* sh) {
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    int x = v;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const int y = __shfl_up(x, o, 64);
-        if (lane >= o) x += y;
-    }
-    if (lane == 63) sh[wave] = x;
-    __syncthreads();
-    int before = 0, all = 0;
-#pragma unroll
-    for (int w = 0; w < kThreads / 64; ++w) {
-        const int t = sh[w];
-        if (w < wave) before += t;
-        all += t;
-    }
-    __syncthreads();
-    *tot = all;
-    return before + x - v;
-}
 
 // Wave 0 finds the digit d (scanning 255 down to 0) where the running count of
 // larger digits first reaches kr; writes d and kr minus the count above d.
@@ -110,6 +92,26 @@ __device__ void find_digit(const int* hist, int kr, uint32_t* sel) {
     }
 }
 
+// Prefix counts of a per-thread flag in thread order for one round: returns the
+// number of set flags in lower threads of the workgroup; *total gets the round's
+// count.  part holds kWaves ints (one buffer per call in flight).
+__device__ __forceinline__ int round_prefix(bool flag, int* part, int* total) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const unsigned long long m = __ballot(flag);
+    const int below = __popcll(m & ((1ull << lane) - 1ull));
+    if (lane == 0) part[wave] = __popcll(m);
+    __syncthreads();
+    int before = 0, all = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+        const int t = part[w];
+        before += w < wave ? t : 0;
+        all += t;
+    }
+    *total = all;
+    return before + below;
+}
+
 template <bool LDS_KEYS>
 __global__ __launch_bounds__(kThreads) void select_kernel(Shape s, const float* __restrict__ s_vis,
                                                           const float* __restrict__ s_txt,
@@ -117,7 +119,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(Shape s, const float* 
                                                           const int64_t* __restrict__ idx_off,
                                                           int32_t* __restrict__ idx) {
     __shared__ int hist[256];
-    __shared__ int sh[8];
+    __shared__ int part[2][2][kWaves];
     __shared__ uint32_t sel[2];
     __shared__ uint32_t keys[LDS_KEYS ? kLdsKeys : 1];
     const int tid = threadIdx.x;
@@ -137,13 +139,10 @@ __global__ __launch_bounds__(kThreads) void select_kernel(Shape s, const float* 
     c.sv = s_vis + ((size_t)bl * s.ngroups + gi) * s.Nv;
     c.st = s_txt + ((size_t)bl * s.ngroups + gi) * s.Nt;
 
-    // counts of forced positions and of non-forced text, from the layout alone
+    // forced positions, and text positions that are not forced: [fs, min(Ns, fr)) and
+    // [max(Ns + Nv, fs), fr), from the layout alone
     const int nf = c.fs + (s.N - c.fr);
-    int ntf = 0;
-    for (int p = tid; p < s.N; p += kThreads) ntf += !c.forced(p) && !c.is_vis(p);
-    int tot;
-    block_exclusive_scan(ntf, &tot, sh);
-    ntf = tot;
+    const int ntf = max(0, min(s.Ns, c.fr) - c.fs) + max(0, c.fr - max(s.Ns + s.Nv, c.fs));
 
     int k;
     if (bgt <= nf) { c.mode = MODE_FORCED; k = bgt; }
@@ -155,8 +154,8 @@ __global__ __launch_bounds__(kThreads) void select_kernel(Shape s, const float* 
                  : c.mode == MODE_TEXT   ? ntf
                                          : s.N - nf - ntf;
 
-    // key lookup: from LDS when the row fits, else re-read
-    auto key_at = [&](int p) -> uint32_t { return LDS_KEYS ? keys[p] : c.key(p); };
+    // key lookup: from LDS when the row fits (kNotCand marks non-candidates), else re-read
+    auto key_at = [&](int p) -> uint32_t { return LDS_KEYS ? keys[p] : (c.cand(p) ? c.key(p) : kNotCand); };
     if (LDS_KEYS) {
         for (int p = tid; p < s.N; p += kThreads) keys[p] = c.cand(p) ? c.key(p) : kNotCand;
         __syncthreads();
@@ -170,12 +169,11 @@ __global__ __launch_bounds__(kThreads) void select_kernel(Shape s, const float* 
         uint32_t prefix = 0u, mask = 0u;
         int kr = k;
         for (int shift = 24; shift >= 0; shift -= 8) {
-            hist[tid] = 0;
+            if (tid < 256) hist[tid] = 0;
             __syncthreads();
             for (int p = tid; p < s.N; p += kThreads) {
-                if (!c.cand(p)) continue;
                 const uint32_t key = key_at(p);
-                if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1);
+                if (key != kNotCand && (key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1);
             }
             __syncthreads();
             if (tid < 64) find_digit(hist, kr, sel);
@@ -183,43 +181,29 @@ __global__ __launch_bounds__(kThreads) void select_kernel(Shape s, const float* 
             prefix |= sel[0] << shift;
             mask |= 0xFFu << shift;
             kr = (int)sel[1];
-            __syncthreads();
         }
         thr = prefix;
         take_ties = kr;
     }
 
-    // ordered emission: thread t owns positions [t*chunk, (t+1)*chunk)
-    const int chunk = (s.N + kThreads - 1) / kThreads;
-    const int p0 = min(tid * chunk, s.N), p1 = min(p0 + chunk, s.N);
-    int nties = 0;
-    for (int p = p0; p < p1; ++p) nties += c.cand(p) && key_at(p) == thr;
-    const int tie_rank = block_exclusive_scan(nties, &tot, sh);
-    int nkeep = 0;
-    {
-        int tr = tie_rank;
-        for (int p = p0; p < p1; ++p) {
-            bool keep = c.kept_outright(p);
-            if (!keep && c.cand(p)) {
-                const uint32_t key = key_at(p);
-                if (key > thr) keep = true;
-                else if (key == thr) keep = (tr++ < take_ties);
-            }
-            nkeep += keep;
-        }
-    }
-    int pos = block_exclusive_scan(nkeep, &tot, sh);
-    {
-        int tr = tie_rank;
-        for (int p = p0; p < p1; ++p) {
-            bool keep = c.kept_outright(p);
-            if (!keep && c.cand(p)) {
-                const uint32_t key = key_at(p);
-                if (key > thr) keep = true;
-                else if (key == thr) keep = (tr++ < take_ties);
-            }
-            if (keep && pos < bgt) out[pos++] = p;
-        }
+    // ordered emission, kThreads positions per round: a tie is kept while its rank among the
+    // ties (in position order) is below take_ties; kept positions are written in order
+    int ties_before = 0, kept_before = 0;
+    const int rounds = (s.N + kThreads - 1) / kThreads;
+    for (int r = 0; r < rounds; ++r) {
+        const int p = r * kThreads + tid;
+        const bool valid = p < s.N;
+        const uint32_t key = valid ? key_at(p) : kNotCand;
+        const bool outright = valid && c.kept_outright(p);
+        const bool cand = !outright && key != kNotCand && valid && c.cand(p);
+        const bool tie = cand && key == thr;
+        int round_ties, round_kept;
+        const int tie_rank = ties_before + round_prefix(tie, part[r & 1][0], &round_ties);
+        const bool keep = outright || (cand && key > thr) || (tie && tie_rank < take_ties);
+        const int pos = kept_before + round_prefix(keep, part[r & 1][1], &round_kept);
+        if (keep && pos < bgt) out[pos] = p;
+        ties_before += round_ties;
+        kept_before += round_kept;
     }
 }
 
