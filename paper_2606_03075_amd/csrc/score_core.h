@@ -774,37 +774,74 @@ __device__ void text_cols_item(const Shape& s, int bl, int kvh, int g, int kb, c
 // and for group 0 the layer's text->vision mass (Eq. (5)-(6)).  red: 256 floats of LDS.
 __device__ inline void finalize_group(const Shape& s, int bl, int gi, const float* ws_colsum, const float* ws_vmh,
                                       float* s_txt, float* w_txt, float* tv_mass, float* red, bool with_mass = true) {
-    const int tid = threadIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int h0 = s.head_mode == 0 ? 0 : gi * s.G;
     const int hn = s.head_mode == 0 ? s.H : s.G;
     const float inv = 1.0f / (float)hn;
     const float* cs = ws_colsum + ((size_t)bl * s.H + h0) * s.Nt;
     const size_t obase = ((size_t)bl * s.ngroups + gi) * s.Nt;
+    // s^T[j]: the head mean of the column sums, eight heads' loads in flight per thread
+    auto column = [&](int j) {
+        float a[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        int h = 0;
+        for (; h + 8 <= hn; h += 8) {
+#pragma unroll
+            for (int u = 0; u < 8; ++u) a[u] += cs[(size_t)(h + u) * s.Nt + j];
+        }
+        for (; h < hn; ++h) a[0] += cs[(size_t)h * s.Nt + j];
+        return (((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]))) * inv;
+    };
+    constexpr int kCols = 4;  // columns per thread kept in registers
+    float wv[kCols];
+    const bool cached = s.Nt <= kCols * kThreads;
     float part = 0.f;
-    for (int j = tid; j < s.Nt; j += kThreads) {
-        float a = 0.f;
-        for (int h = 0; h < hn; ++h) a += cs[(size_t)h * s.Nt + j];
-        const float st = a * inv;
-        s_txt[obase + j] = st;
-        part += st / (float)(s.Nt - j);
+    if (cached) {
+#pragma unroll
+        for (int c = 0; c < kCols; ++c) {
+            const int j = tid + c * kThreads;
+            wv[c] = 0.f;
+            if (j < s.Nt) {
+                const float st = column(j);
+                s_txt[obase + j] = st;
+                wv[c] = st / (float)(s.Nt - j);
+                part += wv[c];
+            }
+        }
+    } else {
+        for (int j = tid; j < s.Nt; j += kThreads) {
+            const float st = column(j);
+            s_txt[obase + j] = st;
+            part += st / (float)(s.Nt - j);
+        }
     }
-    red[tid] = part;
+    // W = sum_j w_j: within each wave, then over the waves in order
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) part += shfl_xor(part, off);
+    if (lane == 0) red[wave] = part;
     __syncthreads();
-    for (int o = kThreads / 2; o > 0; o >>= 1) {
-        if (tid < o) red[tid] += red[tid + o];
-        __syncthreads();
+    float W = 0.f;
+#pragma unroll
+    for (int w = 0; w < kThreads / 64; ++w) W += red[w];
+    // the plain attention sum (Table 5) weighs every text row 1
+    auto weight = [&](float w) { return s.vision_rank == 1 ? 1.f : (W > 0.f ? w / W : 0.f); };
+    if (cached) {
+#pragma unroll
+        for (int c = 0; c < kCols; ++c) {
+            const int j = tid + c * kThreads;
+            if (j < s.Nt) w_txt[obase + j] = weight(wv[c]);
+        }
+    } else {
+        __syncthreads();  // every s_txt store of the workgroup precedes the reads below
+        for (int j = tid; j < s.Nt; j += kThreads) w_txt[obase + j] = weight(s_txt[obase + j] / (float)(s.Nt - j));
     }
-    const float W = red[0];
-    for (int j = tid; j < s.Nt; j += kThreads) {
-        const float w = s_txt[obase + j] / (float)(s.Nt - j);
-        // the plain attention sum (Table 5) weighs every text row 1
-        w_txt[obase + j] = s.vision_rank == 1 ? 1.f : (W > 0.f ? w / W : 0.f);
-    }
-    if (with_mass && gi == 0 && tid == 0) {
+    if (with_mass && gi == 0 && wave == 0) {
+        // the layer's TV mass: the mean over all query heads of their vision masses
         float a = 0.f;
         if (s.Nt > 0)
-            for (int h = 0; h < s.H; ++h) a += ws_vmh[(size_t)bl * s.H + h];
-        tv_mass[bl] = a / (float)s.H;
+            for (int h = lane; h < s.H; h += 64) a += ws_vmh[(size_t)bl * s.H + h];
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) a += shfl_xor(a, off);
+        if (lane == 0) tv_mass[bl] = a / (float)s.H;
     }
     __syncthreads();
 }
