@@ -62,6 +62,7 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(Shape s, const float* 
     __syncthreads();
     if (tid == 0) {
         double S = 0.0;
+#pragma unroll 8
         for (int l = 0; l < L; ++l) S += x[l];
         sh_sum = S;
     }
@@ -76,6 +77,7 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(Shape s, const float* 
     while (n_active > 0) {
         if (tid == 0) {
             double Fa = 0.0;
+#pragma unroll 8
             for (int l = 0; l < L; ++l)
                 if (active[l]) Fa += f[l];
             sh_sum = Fa;
@@ -103,13 +105,15 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(Shape s, const float* 
         __syncthreads();
     }
 
+    // x becomes the fractional part of each layer still below the cap, -1 for the others
+    // (fractions lie in [0, 1), so -1 ranks below every eligible layer and ties none)
     int part = 0;
     for (int l = tid; l < L; l += kThreads) {
         const double fl = floor(x[l]);
         long long base = (long long)fl;
         if (base > cap) base = cap;
         bcount[l] = F + base;
-        x[l] = x[l] - fl;  // fractional part from here on
+        x[l] = F + base < N ? x[l] - fl : -1.0;
         part += (int)base;
     }
     __shared__ long long sh_base;
@@ -119,43 +123,55 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(Shape s, const float* 
     __syncthreads();
     const long long r = total - ((long long)L * F + sh_base);
 
-    // +1 to the r eligible layers ranked first by (fraction desc, layer asc)
+    // +1 to the r eligible layers ranked first by (fraction desc, layer asc); every rank is
+    // taken before any count changes
+    __shared__ int cnt[kMaxLayers];
     for (int l = tid; l < L; l += kThreads) {
-        if (bcount[l] >= N) continue;
         const double fr = x[l];
         int rank = 0;
-        for (int j = 0; j < L; ++j) {
-            if (bcount[j] >= N) continue;
-            rank += (x[j] > fr) || (x[j] == fr && j < l);
-        }
-        if (rank < r) bcount[l] += 1;
+#pragma unroll 8
+        for (int j = 0; j < L; ++j) rank += (x[j] > fr) || (x[j] == fr && j < l);
+        cnt[l] = (int)bcount[l] + (fr >= 0.0 && rank < r ? 1 : 0);
     }
     __syncthreads();
 
     if (unit_order != nullptr) {
         for (int l = tid; l < L; l += kThreads) {
-            const long long bl_count = bcount[l];
+            const int c = cnt[l];
             int rank = 0;
-            for (int j = 0; j < L; ++j) rank += (bcount[j] > bl_count) || (bcount[j] == bl_count && j < l);
+#pragma unroll 8
+            for (int j = 0; j < L; ++j) rank += (cnt[j] > c) || (cnt[j] == c && j < l);
             unit_order[(size_t)rank * s.B + b] = b * L + l;
         }
     }
 
-    if (tid == 0) {
+    // budgets and the two offset tables: prefix sums of the per-layer counts (integers, so
+    // the order of the additions does not matter), 64 layers at a time by wave 0
+    if (tid < 64) {
         const long long g = s.ngroups;
         const long long kept = total + (long long)L * add;  // tokens each sequence keeps
-        long long io = (long long)b * kept * g;
-        long long so = (long long)b * (kept + (long long)L * reserve);
-        for (int l = 0; l < L; ++l) {
-            const size_t bl = (size_t)b * L + l;
-            const long long bl_tokens = add + bcount[l];
-            budgets[bl] = (int32_t)bl_tokens;
-            idx_off[bl] = io;
-            seg_off[bl] = so;
-            io += g * bl_tokens;
-            so += bl_tokens + reserve;
+        const long long io0 = (long long)b * kept * g;
+        const long long so0 = (long long)b * (kept + (long long)L * reserve);
+        long long carry = 0;
+        for (int c0 = 0; c0 < L; c0 += 64) {
+            const int l = c0 + tid;
+            const int v = l < L ? add + cnt[l] : 0;  // tokens layer l keeps (< 2^24)
+            int incl = v;
+#pragma unroll
+            for (int o = 1; o < 64; o <<= 1) {
+                const int y = __shfl_up(incl, o, 64);
+                if (tid >= o) incl += y;
+            }
+            if (l < L) {
+                const size_t bl = (size_t)b * L + l;
+                const long long before = carry + (incl - v);
+                budgets[bl] = v;
+                idx_off[bl] = io0 + g * before;
+                seg_off[bl] = so0 + before + (long long)l * reserve;
+            }
+            carry += __shfl(incl, 63, 64);
         }
-        if (b == s.B - 1) {
+        if (b == s.B - 1 && tid == 0) {
             idx_off[(size_t)s.B * L] = (long long)s.B * kept * g;
             seg_off[(size_t)s.B * L] = (long long)s.B * (kept + (long long)L * reserve);
         }

@@ -55,7 +55,8 @@ def _longest_first(budgets):
 
 @pytest.mark.parametrize("budget_rule", [0, 1, 2])
 @pytest.mark.parametrize("L,N,n_sink,n_recent", [(32, 2979, 0, 0), (28, 8256, 4, 1), (5, 13, 0, 0),
-                                                 (1, 168, 0, 0), (40, 3171, 4, 1), (7, 3, 1, 1)])
+                                                 (1, 168, 0, 0), (40, 3171, 4, 1), (7, 3, 1, 1),
+                                                 (257, 97, 2, 1), (512, 40, 0, 0)])
 def test_budget_kernel_exact(lib, L, N, n_sink, n_recent, budget_rule):
     torch = _torch()
     rng = np.random.default_rng(L * 1000 + N)
