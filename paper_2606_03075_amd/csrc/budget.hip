@@ -74,6 +74,7 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(Shape s, const float* 
     // water-fill: capped layers are fixed and the remainder is re-shared
     double remaining = (double)R;
     int n_active = L;
+    __shared__ int sh_over;
     while (n_active > 0) {
         if (tid == 0) {
             double Fa = 0.0;
@@ -81,6 +82,7 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(Shape s, const float* 
             for (int l = 0; l < L; ++l)
                 if (active[l]) Fa += f[l];
             sh_sum = Fa;
+            sh_over = 0;
         }
         __syncthreads();
         const double Fa = sh_sum;
@@ -91,7 +93,10 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(Shape s, const float* 
                 over += x[l] > capd;
             }
         }
-        const int n_over = __syncthreads_count(over);
+        // a thread holds up to kMaxLayers / kThreads layers: the count is a sum, not a vote
+        if (over) atomicAdd(&sh_over, over);
+        __syncthreads();
+        const int n_over = sh_over;
         if (n_over == 0) break;
         for (int l = tid; l < L; l += kThreads) {
             if (active[l] && x[l] > capd) {

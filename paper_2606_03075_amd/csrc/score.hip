@@ -289,11 +289,17 @@ __global__ __launch_bounds__(kThreads) void score_vis_reduce_kernel(Shape s, int
     if (budgets != nullptr && budgets[bl] <= vis_threshold) return;
     const int kv0 = s.head_mode == 0 ? 0 : gi;
     const int kvn = s.head_mode == 0 ? s.Hkv : 1;
-    float a = 0.f;
-    for (int kv = kv0; kv < kv0 + kvn; ++kv)
-        for (int rg = 0; rg < rowgroups; ++rg)
-            a += ws_part[(((size_t)bl * s.Hkv + kv) * rowgroups + rg) * (size_t)s.Nv + j];
-    s_vis[((size_t)bl * s.ngroups + gi) * s.Nv + j] = a;
+    // the partials of (KV head, row group) pairs are consecutive rows of n_vis: eight in flight
+    const float* src = ws_part + ((size_t)bl * s.Hkv + kv0) * rowgroups * (size_t)s.Nv + j;
+    const int n = kvn * rowgroups;
+    float a[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    int i = 0;
+    for (; i + 8 <= n; i += 8) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) a[u] += src[(size_t)(i + u) * s.Nv];
+    }
+    for (; i < n; ++i) a[0] += src[(size_t)i * s.Nv];
+    s_vis[((size_t)bl * s.ngroups + gi) * s.Nv + j] = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
 }
 
 #define TGVKV_ROWPLAN_DISPATCH(KERNEL, D, rp, ...)                                                \
