@@ -75,3 +75,53 @@ def test_stress13b_full(lib):
             want = idx[io[ref * L + l]: io[ref * L + l + 1]]
             assert np.array_equal(got, want), (b, l)
     log(f"  stress13b budgets seq0: {buf.budgets[0].tolist()}")
+
+
+def test_llavanext_paged_full(lib):
+    """The bench's paged launch configuration at full size (16-row pages, longest-first order):
+    the pool gathered through the table equals the contiguous cache bit for bit, and 16 decode
+    steps with a per-sequence step vector equal the contiguous decode bit for bit."""
+    import torch
+    from paper_2606_03075_amd import binding as bd
+    from tests.test_gpu_e2e import _inputs
+    from workloads import total_budget
+
+    cfg = CONFIGS["llavanext"]
+    T, page = 16, 16
+    t, dec, dev_t, dev_dec = _inputs(cfg, 0, T, [0, 1])
+    p = bd.problem_from(cfg)
+    tot = total_budget(cfg.rhos[0], cfg.n_tokens, cfg.layers)
+    buf = bd.EvictionBuffers(p, None, tot, T)
+    buf.evict(dev_t["q_text"], dev_t["k"], dev_t["v"])
+    width, n_pages = bd.page_plan(p, None, tot, T, page)
+    pool = bd.PagedPool(cfg.heads_kv, cfg.head_dim, page, n_pages)
+    pool.free = list(np.random.default_rng(0).permutation(n_pages))
+    table = pool.admit(buf, dev_t["k"], dev_t["v"])
+    del dev_t
+    out_p = torch.empty_like(buf.out)
+    for st in range(T):
+        buf.decode(st, dev_dec[st]["q"], dev_dec[st]["k_new"], dev_dec[st]["v_new"])
+        steps = torch.full((cfg.batch,), st, dtype=torch.int32, device="cuda")
+        pool.decode(p, None, table, buf.budgets, T, steps, dev_dec[st]["q"], dev_dec[st]["k_new"],
+                    dev_dec[st]["v_new"], out_p, buf.ws_decode, unit_order=buf.unit_order)
+        torch.cuda.synchronize()
+        assert torch.equal(out_p, buf.out), f"step {st}"
+    # every row of every (sequence, layer): the pool through the table against the contiguous segments
+    Hkv, D, L = cfg.heads_kv, cfg.head_dim, cfg.layers
+    budgets = buf.budgets.cpu().numpy().reshape(-1)
+    so = buf.seg_offsets.cpu().numpy()
+    tab = table.cpu().numpy()
+    kc = buf.kc.view(torch.int16)
+    vc = buf.vc.view(torch.int16)
+    kp = pool.k_pool.view(torch.int16)
+    vp = pool.v_pool.view(torch.int16)
+    for bl in range(cfg.batch * L):
+        rows = int(budgets[bl]) + T
+        n_pg = -(-rows // page)
+        pages = torch.from_numpy(tab[bl, :n_pg].astype(np.int64)).cuda()
+        base = int(so[bl]) * Hkv * D
+        for src, pool_t in ((kc, kp), (vc, vp)):
+            seg = src[base: base + Hkv * rows * D].view(Hkv, rows, D)
+            got = pool_t[pages].permute(1, 0, 2, 3).reshape(Hkv, n_pg * page, D)[:, :rows]
+            assert torch.equal(got, seg), bl
+    log(f"  llavanext paged: {cfg.batch * L} segments, {n_pages} pages, table width {width}")
