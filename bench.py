@@ -348,17 +348,29 @@ def main():
     dec_ms = 0.0
     dec_gap_ms = 0.0
     step_ms = 0.0
+    evict_per_step, decode_launch_us = [], []  # spread over the timed steps / launches
     for evs in timed:
+        ev_step = 0.0
         for (n0, e0), (n1, e1) in zip(evs[:-1], evs[1:]):
-            ms = e0.elapsed_time(e1) / args.steps
+            raw = e0.elapsed_time(e1)
+            ms = raw / args.steps
             if n1 == "decode":
                 dec_ms += ms / max(T, 1)
+                decode_launch_us.append(raw * 1e3)
             elif n1 == "decode_gap":
                 dec_gap_ms += ms / max(T, 1)
             else:
                 stage_ms[n1] = stage_ms.get(n1, 0.0) + ms
+                ev_step += raw
+        evict_per_step.append(ev_step)
         step_ms += evs[0][1].elapsed_time(evs[-1][1]) / args.steps
     evict_ms = sum(stage_ms.values())
+
+    def spread(xs, nd):
+        if not xs:
+            return None
+        q = np.percentile(np.asarray(xs, np.float64), [10, 50, 90])
+        return {"p10": round(float(q[0]), nd), "median": round(float(q[1]), nd), "p90": round(float(q[2]), nd)}
     tokens_per_s = B * N / (evict_ms * 1e-3)
 
     # algorithmic bytes per launch: what the method must move, each once (K and the text
@@ -422,6 +434,8 @@ def main():
                    "decode_steps": T, "vision_scored_layers": vis_layers, "schedule": sched,
                    "cache": args.cache, "page_size": args.page_size if paged else None},
         "evict_ms": round(evict_ms, 4),
+        "evict_ms_spread": spread(evict_per_step, 4),
+        "decode_launch_us_spread": spread(decode_launch_us, 2),
         "decode_us_per_step": round(dec_ms * 1e3, 2),
         "decode_us_per_step_with_launch_gaps": round((dec_ms + dec_gap_ms) * 1e3, 2),
         "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},
