@@ -76,8 +76,9 @@ __global__ __launch_bounds__(kThreads) void score_stats_kernel(Shape s, int rowg
 // workgroup holds all question rows of a (sequence, layer, KV head): the text
 // pass is latency-bound, so running it as each unit's sweep ends hides it behind
 // the other workgroups' key streams, and the question rows' normalisers go to
-// the text pass through LDS.  Results are bit-identical to score_stats followed
-// by score_text (same operations in the same order).
+// the text pass through LDS.  The row statistics are bit-identical to
+// score_stats'; the text pass stages the unit's text keys in the freed tiles
+// when they fit (a different summation order of the same column sums).
 template <int D, int NSLOT, int KS>
 __global__ __launch_bounds__(kThreads) void score_stats_text_kernel(Shape s, const uint16_t* __restrict__ q_text,
                                                                     const uint16_t* __restrict__ k,
@@ -122,10 +123,13 @@ __global__ __launch_bounds__(kThreads) void score_stats_text_kernel(Shape s, con
         }
     }
     __syncthreads();
-    if (tid < s.G) {
+    // per query head: the sum of its question rows' vision masses (one wave per head)
+    for (int g = tid >> 6; g < s.G; g += kThreads / 64) {
         float a = 0.f;
-        for (int qi = 0; qi < s.Nq; ++qi) a += vms[tid * s.Nq + qi];
-        ws_vmh[head0 + tid] = a;
+        for (int qi = tid & 63; qi < s.Nq; qi += 64) a += vms[g * s.Nq + qi];
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) a += shfl_xor(a, off);
+        if ((tid & 63) == 0) ws_vmh[head0 + g] = a;
     }
     if (lds_text) {
         // the unit's text keys go into the freed tiles after the normalisers and masses

@@ -589,9 +589,28 @@ __device__ void text_pass_lds(const Shape& s, int bl, int kvh, const uint16_t* _
     const int TB = (s.Nt + 15) >> 4;
     const int TK = TB * 16;                                       // staged key rows (last one repeated)
     float* part = reinterpret_cast<float*>(kl + (size_t)TK * GG::ROWB);  // [4 waves][G][TK]
+    const int SB = (s.Ns + 15) >> 4;
+    const int items = s.G * TB;
 
-    // stage the text keys (text order: system keys, then question keys) and clear the partials
-    constexpr int kStage = 8;  // 16-byte loads in flight per thread
+    const int koff = (lane >> 4) * 8;
+    auto load_q = [&](bf16x8 (&f)[GG::KSTEPS], int g, int row) {
+        const uint16_t* src = q_text + ((head0 + g) * s.Nt + row) * D + koff;
+#pragma unroll
+        for (int ks = 0; ks < GG::KSTEPS; ++ks) f[ks] = as_bf16x8(load16(src + ks * 32));
+    };
+    auto sys_item_q = [&](bf16x8 (&f)[GG::KSTEPS], int item) {
+        const int it = min(item, s.G * SB - 1);
+        load_q(f, it / SB, min((it % SB) * 16 + (lane & 15), s.Ns - 1));
+    };
+    auto col_item_q = [&](bf16x8 (&f)[GG::KSTEPS], int item) {
+        const int it = min(item, items - 1);
+        load_q(f, it / TB, min((it % TB) * 16 + (lane & 15), s.Nt - 1));
+    };
+
+    // one round of loads: the text keys (text order: system keys, then question keys), this
+    // wave's first system-row block and its first column item; then the keys go to LDS
+    constexpr int kStage = 8;  // 16-byte key loads per thread per round
+    bf16x8 qs[GG::KSTEPS], qa[GG::KSTEPS], qb[GG::KSTEPS];
     for (int c0 = 0; c0 < TK * GG::CPR; c0 += kStage * kThreads) {
         u32x4 r[kStage];
 #pragma unroll
@@ -600,6 +619,10 @@ __device__ void text_pass_lds(const Shape& s, int bl, int kvh, const uint16_t* _
             const int t = min(c / GG::CPR, s.Nt - 1);
             const int pos = t < s.Ns ? t : t + s.Nv;
             r[i] = load16(kbase + (size_t)pos * D + (c % GG::CPR) * 8);
+        }
+        if (c0 == 0) {
+            if (SB > 0) sys_item_q(qs, wave);
+            col_item_q(qa, wave);
         }
 #pragma unroll
         for (int i = 0; i < kStage; ++i) {
@@ -610,27 +633,18 @@ __device__ void text_pass_lds(const Shape& s, int bl, int kvh, const uint16_t* _
     for (int x = tid; x < 4 * s.G * TK; x += kThreads) part[x] = 0.f;
     __syncthreads();
 
-    const int koff = (lane >> 4) * 8;
-    auto load_q = [&](bf16x8 (&f)[GG::KSTEPS], int g, int row) {
-        const uint16_t* src = q_text + ((head0 + g) * s.Nt + row) * D + koff;
-#pragma unroll
-        for (int ks = 0; ks < GG::KSTEPS; ++ks) f[ks] = as_bf16x8(load16(src + ks * 32));
-    };
-
     // system rows x system keys: row normalisers (C[key][row]: a lane owns row i)
-    const int SB = (s.Ns + 15) >> 4;
     for (int item = wave; item < s.G * SB; item += 4) {
         const int g = item / SB, rb = item % SB;
         const int i = rb * 16 + (lane & 15);
-        bf16x8 qf[GG::KSTEPS];
-        load_q(qf, g, min(i, s.Ns - 1));
+        if (item != wave) sys_item_q(qs, item);
         float m = kNegInf, l = 0.f;
         for (int kb = 0; kb <= rb; ++kb) {
             bf16x8 kf[GG::KSTEPS];
             load_kfrag<D>(kf, kl, kb, lane);
             f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(kf[ks], qf[ks], acc);
+            for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(kf[ks], qs[ks], acc);
             float z[4];
             float mx = kNegInf;
 #pragma unroll
@@ -662,9 +676,6 @@ __device__ void text_pass_lds(const Shape& s, int bl, int kvh, const uint16_t* _
     __syncthreads();
 
     // all text rows x text keys (C[row][key]: a lane owns key j, rows 4*(lane/16) + jj)
-    const int items = s.G * TB;
-    bf16x8 qa[GG::KSTEPS], qb[GG::KSTEPS];
-    auto item_row = [&](int item) { return min((item % TB) * 16 + (lane & 15), s.Nt - 1); };
     auto consume = [&](const bf16x8 (&qf)[GG::KSTEPS], int item) {
         const int g = item / TB, rb = item % TB;
         float* wpart = part + ((size_t)wave * s.G + g) * TK;
@@ -688,16 +699,16 @@ __device__ void text_pass_lds(const Shape& s, int bl, int kvh, const uint16_t* _
             if (lane < 16) wpart[j] += col;
         }
     };
-    // every wave runs the same (even) number of steps; an item past the last is a no-op
+    // this wave's items are wave, wave + 4, ...: two register sets, the next item's fragments
+    // fetched while the current one is used (qa already holds the first)
     const int steps = (items + 3) / 4;
     int item = wave;
-    load_q(qa, (min(item, items - 1)) / TB, item_row(min(item, items - 1)));
     for (int st = 0; st < steps; st += 2) {
         const int nx = item + 4;
-        load_q(qb, min(nx, items - 1) / TB, item_row(min(nx, items - 1)));
+        col_item_q(qb, nx);
         if (item < items) consume(qa, item);
         const int nx2 = item + 8;
-        load_q(qa, min(nx2, items - 1) / TB, item_row(min(nx2, items - 1)));
+        col_item_q(qa, nx2);
         if (nx < items) consume(qb, nx);
         item = nx2;
     }
