@@ -35,9 +35,11 @@ def common_flags():
 
 
 def device_flags():
-    # Packed-fp32 VALU forms are disabled for all device code.
+    # Packed-fp32 VALU forms are disabled for all device code.  MFMA results are
+    # kept in ordinary VGPRs (gfx950 allows it): the accumulator-register form
+    # costs a v_accvgpr_read per result register before the softmax arithmetic.
     return [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-            "-munsafe-fp-atomics"]
+            "-munsafe-fp-atomics", "-mllvm", "-amdgpu-mfma-vgpr-form"]
 
 
 def _compile(src: str, verbose: bool) -> str:

@@ -21,6 +21,8 @@
 #include "tgvkv_device.h"
 #include "tgvkv_shape.h"
 
+#include <type_traits>
+
 namespace tgvkv {
 namespace core {
 
@@ -60,19 +62,17 @@ __device__ __forceinline__ void store_tile_lds(char* buf, const u32x4 (&r)[Geo<D
     }
 }
 
-// Streams the 64-key tiles of keys [kbeg, kend) through the two LDS buffers.
-// With DEPTH 2 two tiles are in flight per workgroup: while tile t is consumed
-// from LDS, tile t+1 waits in registers and tile t+2 is being fetched (costs
-// one more tile of registers); with DEPTH 1 only tile t+1 is fetched meanwhile.
-// compute(buf, key0, t) runs on tile t; post(key0, t) runs after the barrier
-// that ends tile t.  Returns right after the last post (no barrier after it).
-// Every barrier is reached by all threads (the tile count is uniform).
-template <int D, int DEPTH, typename Compute, typename Post>
-__device__ __forceinline__ void tile_pipeline(const uint16_t* kbase, int kbeg, int kend,
-                                              char (*tiles)[Geo<D>::TILE_BYTES], Compute&& compute, Post&& post) {
+// The tile pipeline with its tiles split into phases (see tile_pipeline below for
+// the pipeline itself).
+template <int D, int DEPTH, typename Edge, typename Mid, typename Post>
+__device__ __forceinline__ void tile_pipeline_phased(const uint16_t* kbase, int kbeg, int kend,
+                                                     char (*tiles)[Geo<D>::TILE_BYTES], int mid_beg, int mid_end,
+                                                     Edge&& edge, Mid&& mid, Post&& post) {
     static_assert(DEPTH == 1 || DEPTH == 2, "tile pipeline depth");
     const int tid = threadIdx.x;
     const int ntiles = (kend - kbeg + kTile - 1) / kTile;
+    // tiles [mid_beg, mid_end) run `mid`, the others `edge`; each phase is its own loop, so the
+    // compiler lays out and allocates the middle loop without the edge tiles' code in it
     if (DEPTH == 1) {
         u32x4 pre[Geo<D>::LOADS];
         if (ntiles > 0) {
@@ -80,14 +80,18 @@ __device__ __forceinline__ void tile_pipeline(const uint16_t* kbase, int kbeg, i
             store_tile_lds<D>(tiles[0], pre, tid);
         }
         __syncthreads();
-        for (int t = 0; t < ntiles; ++t) {
+        auto step = [&](int t, auto& compute) {
             const int key0 = kbeg + t * kTile;
             if (t + 1 < ntiles) load_tile_regs<D>(pre, kbase, key0 + kTile, kend - 1, tid);
             compute(tiles[t & 1], key0, t);
             if (t + 1 < ntiles) store_tile_lds<D>(tiles[(t + 1) & 1], pre, tid);
             __syncthreads();
             post(key0, t);
-        }
+        };
+        int t = 0;
+        for (; t < min(mid_beg, ntiles); ++t) step(t, edge);
+        for (; t < min(mid_end, ntiles); ++t) step(t, mid);
+        for (; t < ntiles; ++t) step(t, edge);
         return;
     }
     // Loads past the last tile are issued anyway (their key index is clamped to
@@ -107,8 +111,10 @@ __device__ __forceinline__ void tile_pipeline(const uint16_t* kbase, int kbeg, i
     // An odd tile count runs one more half-step without compute or post (its load
     // and store touch only clamped rows and the free buffer), so the loop has no
     // exit in the middle; with one, the compiler's wait counting loses track of
-    // the loads in flight at the loop head and drains them all.
-    for (int t = 0; t < ntiles; t += 2) {
+    // the loads in flight at the loop head and drains them all.  Two tiles per
+    // step: the phase boundaries are taken at even tiles (a pure tile run as an
+    // edge tile gives the same result).
+    auto step2 = [&](int t, auto& compute) {
         // tile t in tiles[0], tile t+1 in rb, tile t+2 in ra; tiles[1] is free
         const int key0 = kbeg + t * kTile;
         compute(tiles[0], key0, t);
@@ -123,7 +129,25 @@ __device__ __forceinline__ void tile_pipeline(const uint16_t* kbase, int kbeg, i
         load_tile_regs<D>(ra, kbase, key0 + 4 * kTile, kend - 1, tid);
         __syncthreads();
         if (more) post(key0 + kTile, t + 1);
-    }
+    };
+    const int m0 = min((mid_beg + 1) & ~1, ntiles), m1 = max(min(mid_end & ~1, ntiles), m0);
+    int t = 0;
+    for (; t < m0; t += 2) step2(t, edge);
+    for (; t < m1; t += 2) step2(t, mid);
+    for (; t < ntiles; t += 2) step2(t, edge);
+}
+
+// Streams the 64-key tiles of keys [kbeg, kend) through the two LDS buffers.
+// With DEPTH 2 two tiles are in flight per workgroup: while tile t is consumed
+// from LDS, tile t+1 waits in registers and tile t+2 is being fetched (costs
+// one more tile of registers); with DEPTH 1 only tile t+1 is fetched meanwhile.
+// compute(buf, key0, t) runs on tile t; post(key0, t) runs after the barrier
+// that ends tile t.  Returns right after the last post (no barrier after it).
+// Every barrier is reached by all threads (the tile count is uniform).
+template <int D, int DEPTH, typename Compute, typename Post>
+__device__ __forceinline__ void tile_pipeline(const uint16_t* kbase, int kbeg, int kend,
+                                              char (*tiles)[Geo<D>::TILE_BYTES], Compute&& compute, Post&& post) {
+    tile_pipeline_phased<D, DEPTH>(kbase, kbeg, kend, tiles, 0, 0, compute, compute, post);
 }
 
 // Tiles in flight per workgroup for a row plan: two while the question rows
@@ -199,66 +223,70 @@ __device__ void stats_sweep(const Shape& s, const uint16_t* kbase, int kbeg, int
         lsum[sl] = 0.f;
         vsum[sl] = 0.f;
     }
-    tile_pipeline<D, PipeDepth<NSLOT>::value>(
-        kbase, kbeg, kend, tiles,
-        [&](const char* buf, int key0, int) {
-            const bool pure_vis = key0 >= vis0 && key0 + kTile <= vis1 && key0 + kTile <= kend;
+    // one tile's statistics; PURE: every key of the tile is a vision key (visible to every question row)
+    auto tile = [&](const char* buf, int key0, auto pure_tag) {
+        constexpr bool PURE = decltype(pure_tag)::value;
 #pragma unroll
-            for (int kbi = 0; kbi < KBW; ++kbi) {
-                const int kb = kp + kbi * KS;
-                bf16x8 kf[GG::KSTEPS];
-                load_kfrag<D>(kf, buf, kb, lane);
-                const int kfirst = key0 + kb * 16 + (lane >> 4) * 4;  // key of accumulator element 0
+        for (int kbi = 0; kbi < KBW; ++kbi) {
+            const int kb = kp + kbi * KS;
+            bf16x8 kf[GG::KSTEPS];
+            load_kfrag<D>(kf, buf, kb, lane);
+            const int kfirst = key0 + kb * 16 + (lane >> 4) * 4;  // key of accumulator element 0
 #pragma unroll
-                for (int sl = 0; sl < NSLOT; ++sl) {
-                    if (rb0 + rs + sl * RSETS >= NB) continue;
-                    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+            for (int sl = 0; sl < NSLOT; ++sl) {
+                if (rb0 + rs + sl * RSETS >= NB) continue;
+                f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                    for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(kf[ks], qf[sl][ks], acc);
-                    if (pure_vis) {
-                        const float z0 = acc[0] * s.scale2, z1 = acc[1] * s.scale2;
-                        const float z2 = acc[2] * s.scale2, z3 = acc[3] * s.scale2;
-                        const float mx = fmaxf(fmaxf(z0, z1), fmaxf(z2, z3));
-                        if (mx > m[sl]) {
-                            const float sc = fast_exp2(m[sl] - mx);
-                            lsum[sl] *= sc;
-                            vsum[sl] *= sc;
-                            m[sl] = mx;
-                        }
-                        const float e = (fast_exp2(z0 - m[sl]) + fast_exp2(z1 - m[sl])) +
-                                        (fast_exp2(z2 - m[sl]) + fast_exp2(z3 - m[sl]));
+                for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(kf[ks], qf[sl][ks], acc);
+                if (PURE) {
+                    const float z0 = acc[0] * s.scale2, z1 = acc[1] * s.scale2;
+                    const float z2 = acc[2] * s.scale2, z3 = acc[3] * s.scale2;
+                    const float mx = fmaxf(fmaxf(z0, z1), fmaxf(z2, z3));
+                    if (mx > m[sl]) {
+                        const float sc = fast_exp2(m[sl] - mx);
+                        lsum[sl] *= sc;
+                        vsum[sl] *= sc;
+                        m[sl] = mx;
+                    }
+                    const float e = (fast_exp2(z0 - m[sl]) + fast_exp2(z1 - m[sl])) +
+                                    (fast_exp2(z2 - m[sl]) + fast_exp2(z3 - m[sl]));
+                    lsum[sl] += e;
+                    vsum[sl] += e;
+                } else {
+                    float z[4];
+                    bool ok[4], isv[4];
+                    float mx = kNegInf;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const int key = kfirst + j;
+                        ok[j] = (key < kend) & ((key < vis1) | (key - vis1 <= qrow[sl]));
+                        isv[j] = (key >= vis0) & (key < vis1);
+                        z[j] = ok[j] ? acc[j] * s.scale2 : kNegInf;
+                        mx = fmaxf(mx, z[j]);
+                    }
+                    if (mx > m[sl]) {
+                        const float sc = fast_exp2(m[sl] - mx);
+                        lsum[sl] *= sc;
+                        vsum[sl] *= sc;
+                        m[sl] = mx;
+                    }
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const float e = ok[j] ? fast_exp2(z[j] - m[sl]) : 0.f;
                         lsum[sl] += e;
-                        vsum[sl] += e;
-                    } else {
-                        float z[4];
-                        bool ok[4], isv[4];
-                        float mx = kNegInf;
-#pragma unroll
-                        for (int j = 0; j < 4; ++j) {
-                            const int key = kfirst + j;
-                            ok[j] = key < kend && (key < vis1 || key - vis1 <= qrow[sl]);
-                            isv[j] = key >= vis0 && key < vis1;
-                            z[j] = ok[j] ? acc[j] * s.scale2 : kNegInf;
-                            mx = fmaxf(mx, z[j]);
-                        }
-                        if (mx > m[sl]) {
-                            const float sc = fast_exp2(m[sl] - mx);
-                            lsum[sl] *= sc;
-                            vsum[sl] *= sc;
-                            m[sl] = mx;
-                        }
-#pragma unroll
-                        for (int j = 0; j < 4; ++j) {
-                            if (ok[j]) {
-                                const float e = fast_exp2(z[j] - m[sl]);
-                                lsum[sl] += e;
-                                if (isv[j]) vsum[sl] += e;
-                            }
-                        }
+                        vsum[sl] += isv[j] ? e : 0.f;
                     }
                 }
             }
-        },
+        }
+    };
+    // tiles [t0, t1) lie wholly inside the vision keys (and below kend): they skip the masks
+    const int t0 = vis0 > kbeg ? (vis0 - kbeg + kTile - 1) / kTile : 0;
+    const int t1 = max((min(vis1, kend) - kbeg) / kTile, t0);
+    tile_pipeline_phased<D, PipeDepth<NSLOT>::value>(
+        kbase, kbeg, kend, tiles, t0, t1,
+        [&](const char* buf, int key0, int) { tile(buf, key0, std::false_type{}); },
+        [&](const char* buf, int key0, int) { tile(buf, key0, std::true_type{}); },
         [](int, int) {});
     // the four lane quarters of a wave saw different keys of the same rows
 #pragma unroll
