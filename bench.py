@@ -71,6 +71,10 @@ def parse():
                                                             "COPY_WRITE_CSV"),
                     help="turn rocprofv3 --pmc counter files of a bench run and of a --calibrate-copy run into "
                          "profiles/hbm_counters.json (HBM bytes per launch of each kernel)")
+    ap.add_argument("--ingest-mfma-counters", metavar="PMC_CSV",
+                    help="turn a rocprofv3 --pmc run of this bench with SQ_INSTS_MFMA SQ_VALU_MFMA_BUSY_CYCLES "
+                         "GRBM_GUI_ACTIVE SQ_INSTS_VALU SQ_INSTS_VALU_TRANS_F32 into profiles/mfma_counters.json "
+                         "(matrix-core work per launch of each scoring kernel)")
     ap.add_argument("--schedule", default="auto", choices=("auto", "two_step", "phases", "fused", "fused_text",
                                                            "lse_in"),
                     help="scoring schedule: vision scores after the budgets only for layers that need them "
@@ -237,8 +241,60 @@ def ingest_counters(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, worklo
     print(json.dumps(data[workload]))
 
 
+MFMA_COUNTERS = os.path.join(ROOT, "profiles", "mfma_counters.json")
+MFMA_FLOPS = 2 * 16 * 16 * 32   # v_mfma_f32_16x16x32_bf16, the only matrix instruction the scoring kernels issue
+SIMDS = 256 * 4                 # MI355X: 256 compute units x 4 SIMDs, each with its own matrix core
+XCDS = 8                        # GRBM_GUI_ACTIVE is counted per XCD and summed over the 8
+SCORE_KERNELS = ("score_text", "score_stats", "score_vision")
+MFMA_PMC = ("SQ_INSTS_MFMA", "SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE", "SQ_INSTS_VALU", "SQ_INSTS_VALU_TRANS_F32")
+
+
+def ingest_mfma_counters(csv_path, workload):
+    """Per-launch means of the matrix-core counters of each scoring kernel (wave-level instruction
+    counts summed over the chip; busy cycles summed over the SIMDs; GPU-active cycles of the dispatch)."""
+    rows = _counter_rows(csv_path)
+    per = {c: _per_kernel_kib(rows, c) for c in MFMA_PMC}
+    rec = {}
+    for key in SCORE_KERNELS:
+        kname = KERNEL_NAMES[key]
+        names = [n for n in per["SQ_INSTS_MFMA"] if kname + "<" in n or n.endswith(kname)]
+        if not names:
+            continue
+        n = max(names, key=lambda x: per["SQ_INSTS_MFMA"][x])  # the launch shape the bench times
+        durs = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) for r in rows
+                if r.get("Kernel_Name") == n and r.get("Counter_Name") == "SQ_INSTS_MFMA"]
+        rec[key] = {"pmc_run_launch_ns": sum(durs) / max(len(durs), 1),"mfma_instrs": per["SQ_INSTS_MFMA"][n], "mfma_busy_cycles": per["SQ_VALU_MFMA_BUSY_CYCLES"][n],
+                    "gpu_active_cycles": per["GRBM_GUI_ACTIVE"][n], "valu_instrs": per["SQ_INSTS_VALU"][n],
+                    "trans_instrs": per["SQ_INSTS_VALU_TRANS_F32"][n],
+                    "source_hash": source_hash(KERNEL_SOURCES[key])}
+    try:
+        with open(MFMA_COUNTERS) as f:
+            data = json.load(f)
+    except (OSError, ValueError):
+        data = {}
+    data[workload] = rec
+    with open(MFMA_COUNTERS, "w") as f:
+        json.dump(data, f, indent=1)
+    print(json.dumps(rec))
+
+
+def mfma_for(kernel, workload):
+    """Committed matrix-core counters of a scoring kernel, if they match the current source."""
+    try:
+        with open(MFMA_COUNTERS) as f:
+            rec = json.load(f).get(workload, {}).get(kernel)
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("source_hash") != source_hash(KERNEL_SOURCES[kernel]):
+        return None
+    return rec
+
+
 def main():
     args = parse()
+    if args.ingest_mfma_counters:
+        ingest_mfma_counters(args.ingest_mfma_counters, counter_key(args.workload, args.vision_only, args.cache))
+        return
     if args.ingest_counters:
         from workloads import CONFIGS
         T = CONFIGS[args.workload].decode_steps if args.decode_steps is None else args.decode_steps
@@ -405,9 +461,39 @@ def main():
                         "kernel": kname, "alg_bytes_per_launch": int(alg[kname]), "avg_launch_ms": round(ms, 4),
                         "ms_per_step": round(ms * (T if kname == "decode" else 1), 4)}
     dominant = max(roofs, key=lambda k: roofs[k]["ms_per_step"])
-    score_ms = stage_ms.get("score", stage_ms.get("score_stats", 0.0))
-    flops = 2.0 * B * L * H * D * (Nq * (cfg.n_sys + Nv) + Nq * (Nq + 1) / 2)
-    mfma_frac = flops / (score_ms * 1e-3) / (BF16_PEAK_TFLOPS * 1e12) if score_ms > 0 else None
+    # scoring's algorithmic matrix work: one QK^T over the logits every text row can see
+    # (system row i sees i + 1 keys, question row i sees the system and vision keys and i + 1
+    # question keys), 2 * head_dim flops each; the implementation's second sweep is not counted
+    Ns = cfg.n_sys
+    logits = Ns * (Ns + 1) / 2 + Nq * (Ns + Nv) + Nq * (Nq + 1) / 2
+    score_flops = 2.0 * B * L * H * D * logits
+    score_ms = sum(v for k, v in stage_ms.items() if k in ("score",) + SCORE_KERNELS)
+    ckey = counter_key(cfg.name, args.vision_only, args.cache)
+    per_kernel = {}
+    for kname in SCORE_KERNELS + ("score",):
+        ms = stage_ms.get(kname, 0.0)
+        if ms <= 0:
+            continue
+        c = mfma_for(kname, ckey) if kname != "score" else None
+        ent = {"avg_launch_ms": round(ms, 4), "counters": None}
+        if c is not None:
+            issued = c["mfma_instrs"] * MFMA_FLOPS / (ms * 1e-3) / 1e12
+            ent["counters"] = {
+                "mfma_instrs_per_launch": int(c["mfma_instrs"]),
+                "issued_tflops": round(issued, 1),
+                "issued_frac_of_peak": round(issued / BF16_PEAK_TFLOPS, 4),
+                # busy cycles are summed over the SIMDs; active cycles over the XCDs
+                "mfma_busy_frac": round(c["mfma_busy_cycles"] / (SIMDS / XCDS * c["gpu_active_cycles"]), 4),
+                "valu_instrs_per_mfma": round(c["valu_instrs"] / max(c["mfma_instrs"], 1), 2),
+                "trans_instrs_per_launch": int(c["trans_instrs"]),
+            }
+        per_kernel[kname] = ent
+    scoring_mfma = None
+    if score_ms > 0:
+        tf = score_flops / (score_ms * 1e-3) / 1e12
+        scoring_mfma = {"alg_flops": int(score_flops), "score_ms": round(score_ms, 4), "alg_tflops": round(tf, 1),
+                        "peak_tflops": BF16_PEAK_TFLOPS, "alg_frac_of_peak": round(tf / BF16_PEAK_TFLOPS, 4),
+                        "kernels": per_kernel}
 
     line = {
         "metric": METRIC,
@@ -442,7 +528,7 @@ def main():
         "decode_us_per_step_with_launch_gaps": round((dec_ms + dec_gap_ms) * 1e3, 2),
         "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},
         "schedule": sched,
-        "scoring_mfma_frac_of_peak": None if mfma_frac is None else round(mfma_frac, 4),
+        "scoring_mfma": scoring_mfma,
         "roofline": roofs[dominant],
         "roofline_kernels": roofs,
         "wall_ms_per_step": round(wall / args.steps * 1e3, 3),
