@@ -33,6 +33,8 @@ namespace tgvkv {
 namespace {
 
 constexpr int kThreads = 256;
+// query heads per KV head from which decode runs on the matrix cores
+constexpr int kMfmaMinGroup = 3;
 
 __device__ __forceinline__ void unpack8(u32x4 r, float (&f)[8]) {
 #pragma unroll
@@ -236,6 +238,243 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(Shape s, Rows rows, ui
     }
 }
 
+// Grouped-query decode on the matrix cores, for several query heads per KV head.
+// The VALU kernel above spends each lane group's instructions on one token and
+// one head at a time, replicated over the 16 lanes of a row: with G heads its
+// work per cached byte grows G-fold and it stops being bound by HBM.  Here a
+// 16-token block and all G heads (padded to 16) are one MFMA tile:
+//   * the block's K and V rows are loaded whole (16 lanes per 256-byte row) and
+//     staged in a per-wave LDS area; read straight into MFMA layout, each quarter
+//     wave of a K load would touch 16 rows, 8x the L1 lookups of a row-wise load;
+//   * S^T = K Q^T on v_mfma_f32_16x16x32_bf16, keys on the M side: lane l then
+//     holds the scores of head l%16 for tokens 4*(l/16) .. +3;
+//   * the block max of each head is taken over the lane's 4 values and across
+//     the lane quarters, so the 16 lanes of a head share one running max; the
+//     output rows are rescaled only when some head's max grew;
+//   * O += P V on v_mfma_f32_16x16x16_bf16: the A operand P[head][token] is
+//     exactly the lane's 4 probabilities, split into a bf16 high part and a bf16
+//     remainder (two MFMAs, about 16 significant bits); the B operand needs
+//     V[token][dim] with tokens along k, which the V stage gives: rows padded to
+//     272 bytes, so the four lane quarters read rows 4 apart from disjoint banks,
+//     and each lane reads one dword (two dims) per token, feeding two 16-dim
+//     output blocks;
+//   * the 4 waves of a workgroup take alternate 16-token blocks of the split.  One
+//     register buffer per wave: as soon as a block's rows are in LDS the next
+//     block's loads are issued (unconditional, clamped to the fresh row past the
+//     end), so they stream in during the block's softmax and P V.  That keeps the
+//     kernel at 122 VGPRs, 4 waves per SIMD; a second buffer cost a wave per SIMD
+//     and measured slower.  The waves then merge through LDS as the VALU kernel does.
+template <int D, int GMAX, class Rows>
+__global__ __launch_bounds__(kThreads) void decode_mfma_kernel(Shape s, Rows rows, uint16_t* __restrict__ kc,
+                                                               uint16_t* __restrict__ vc,
+                                                               const int32_t* __restrict__ budgets, int reserve,
+                                                               int step, const int32_t* __restrict__ steps,
+                                                               const uint16_t* __restrict__ q,
+                                                               const uint16_t* __restrict__ k_new,
+                                                               const uint16_t* __restrict__ v_new,
+                                                               float* __restrict__ out, float* __restrict__ ws_part,
+                                                               int nsplit, const int32_t* __restrict__ unit_order) {
+    constexpr int KSTEPS = D / 32;          // k-steps of S^T = K Q^T over the head dim
+    constexpr int NB2 = D / 32;             // pairs of 16-dim output blocks
+    constexpr int VROWB = D * 2 + 16;       // padded LDS row of the V stage, bytes
+    constexpr int VCH = D / 8;              // 16-byte chunks per row
+    constexpr int VLOADS = 16 * VCH / 64;   // 16-byte V loads per lane per block
+    constexpr int STAGE = 4 * 16 * VROWB * 2;  // per wave: the block's V rows, then its K rows
+    constexpr int MERGE = 4 * GMAX * (D + 2) * (int)sizeof(float);
+    __shared__ __align__(16) char smem[STAGE > MERGE ? STAGE : MERGE];
+    extern __shared__ int lds_pages[];  // paged layout: the unit's page ids
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int c = lane & 15, qq = lane >> 4;
+    int bid = blockIdx.x;
+    const int split = bid % nsplit;
+    bid /= nsplit;
+    const int kvh = bid % s.Hkv;
+    const int bl = unit_order != nullptr ? min(max(unit_order[bid / s.Hkv], 0), s.B * s.L - 1) : bid / s.Hkv;
+    const int G = s.G;
+
+    const int st = steps != nullptr ? steps[bl / s.L] : step;
+    if (st < 0 || st >= reserve) return;  // uniform over the workgroup, before any barrier
+    const int bsz = budgets[bl];
+    const int len = bsz + st + 1;
+    rows.init(s, bl, kvh, bsz, len, lds_pages);
+    __syncthreads();
+    const uint16_t* knew = k_new + ((size_t)bl * s.Hkv + kvh) * D;
+    const uint16_t* vnew = v_new + ((size_t)bl * s.Hkv + kvh) * D;
+
+    if (split == 0 && tid < VCH) {
+        const size_t r = rows.row(bsz + st);
+        store16(kc + r + tid * 8, load16(knew + tid * 8));
+        store16(vc + r + tid * 8, load16(vnew + tid * 8));
+    }
+
+    // B operand of S^T: query head c (zero for the padding heads), 8 dims of the lane's quarter per k-step
+    bf16x8 qf[KSTEPS];
+    {
+        const bool hv = c < G;
+        const uint16_t* qp = q + ((size_t)bl * s.H + kvh * G + (hv ? c : 0)) * D + qq * 8;
+#pragma unroll
+        for (int ks = 0; ks < KSTEPS; ++ks) {
+            u32x4 z = {0u, 0u, 0u, 0u};
+            qf[ks] = as_bf16x8(hv ? load16(qp + ks * 32) : z);
+        }
+    }
+
+    const int per = (len + nsplit - 1) / nsplit;
+    const int t0 = min(split * per, len), t1 = min(t0 + per, len);
+    const int nblk = (t1 - t0 + 15) >> 4;
+    const int wblk = (nblk + 3) >> 2;  // blocks per wave, uniform over the workgroup
+
+    float m_run = kNegInf, l_run = 0.f;
+    f32x4 o[2 * NB2];
+#pragma unroll
+    for (int nb = 0; nb < 2 * NB2; ++nb) o[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    char* vst = smem + wave * 16 * VROWB;
+    char* kst = smem + (4 + wave) * 16 * VROWB;
+
+    // loads of the block at token n0: its K and V rows, 16 lanes per row; rows past t1
+    // (and the step's own token) read the fresh k_new / v_new row, so every load is issued
+    auto settle_qf = [&]() {
+#pragma unroll
+        for (int ks = 0; ks < KSTEPS; ++ks) settle(qf[ks]);
+    };
+    auto issue = [&](u32x4 (&kr)[VLOADS], u32x4 (&vr)[VLOADS], int n0) {
+#pragma unroll
+        for (int i = 0; i < VLOADS; ++i) {
+            const int ch = i * 64 + lane;
+            const int n = n0 + ch / VCH;
+            const bool fresh = n >= len - 1 || n >= t1;
+            const size_t r = fresh ? 0 : rows.row(n);
+            kr[i] = load16_stream((fresh ? knew : kc + r) + (ch % VCH) * 8);
+            vr[i] = load16_stream((fresh ? vnew : vc + r) + (ch % VCH) * 8);
+        }
+    };
+    // rows into the wave's LDS stages, then S^T from the staged K (lane: row c, its k-step columns)
+    auto stage = [&](const u32x4 (&kr)[VLOADS], const u32x4 (&vr)[VLOADS]) {
+        // the stages are free: this wave's reads of the previous block were issued before
+        asm volatile("" ::: "memory");
+#pragma unroll
+        for (int i = 0; i < VLOADS; ++i) {
+            const int ch = i * 64 + lane;
+            store16(vst + (ch / VCH) * VROWB + (ch % VCH) * 16, vr[i]);
+            store16(kst + (ch / VCH) * VROWB + (ch % VCH) * 16, kr[i]);
+        }
+        asm volatile("" ::: "memory");
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KSTEPS; ++ks)
+            acc = mfma16x16x32(as_bf16x8(*reinterpret_cast<const u32x4*>(kst + c * VROWB + (ks * 32 + qq * 8) * 2)),
+                               qf[ks], acc);
+        return acc;
+    };
+    auto consume = [&](f32x4 acc, int n0) {
+        float z[4], mb = kNegInf;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            z[j] = n0 + 4 * qq + j < t1 ? acc[j] * s.scale2 : kNegInf;
+            mb = fmaxf(mb, z[j]);
+        }
+        mb = max_xor32(max_xor16(mb));
+        const float m_new = fmaxf(m_run, mb);
+        if (__builtin_amdgcn_ballot_w64(m_new > m_run) != 0) {  // some head's max grew (uniform branch)
+            const float sc = m_new == kNegInf ? 1.f : fast_exp2(m_run - m_new);
+            l_run *= sc;
+            float scr[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) scr[j] = __shfl(sc, 4 * qq + j, 64);  // output row 4*qq + j's head
+#pragma unroll
+            for (int nb = 0; nb < 2 * NB2; ++nb)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) o[nb][j] *= scr[j];
+            m_run = m_new;
+        }
+        const float mu = m_run == kNegInf ? 0.f : m_run;
+        bf16x4 ph, pl;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const float p = fast_exp2(z[j] - mu);
+            l_run += p;
+            ph[j] = (__bf16)p;
+            pl[j] = (__bf16)(p - (float)ph[j]);
+        }
+        asm volatile("" ::: "memory");
+        // B operand: tokens 4*qq .. +3 of dims 32*nb2 + 2c (even block) and + 1 (odd block)
+#pragma unroll
+        for (int nb2 = 0; nb2 < NB2; ++nb2) {
+            uint32_t w[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                w[i] = *reinterpret_cast<const uint32_t*>(vst + (4 * qq + i) * VROWB + (32 * nb2 + 2 * c) * 2);
+            typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+            const u32x2 ev = {(w[0] & 0xFFFFu) | (w[1] << 16), (w[2] & 0xFFFFu) | (w[3] << 16)};
+            const u32x2 od = {(w[0] >> 16) | (w[1] & 0xFFFF0000u), (w[2] >> 16) | (w[3] & 0xFFFF0000u)};
+            const bf16x4 be = __builtin_bit_cast(bf16x4, ev), bo = __builtin_bit_cast(bf16x4, od);
+            o[2 * nb2] = mfma16x16x16(ph, be, o[2 * nb2]);
+            o[2 * nb2] = mfma16x16x16(pl, be, o[2 * nb2]);
+            o[2 * nb2 + 1] = mfma16x16x16(ph, bo, o[2 * nb2 + 1]);
+            o[2 * nb2 + 1] = mfma16x16x16(pl, bo, o[2 * nb2 + 1]);
+        }
+    };
+
+    u32x4 ka[VLOADS], va[VLOADS];
+    int n0 = t0 + 16 * wave;  // this wave's blocks: wave, wave + 4, ... of the split
+    issue(ka, va, n0);
+    settle_qf();
+    for (int bi = 0; bi < wblk; ++bi) {
+        const f32x4 acc = stage(ka, va);
+        issue(ka, va, n0 + 64);
+        consume(acc, n0);
+        n0 += 64;
+    }
+
+    // the four lane quarters summed different tokens of each head
+    l_run = sum_xor32(sum_xor16(l_run));
+    __syncthreads();  // every wave is done with its stage: the merge reuses it
+    float* wm = reinterpret_cast<float*>(smem);  // [4][GMAX]
+    float* wl = wm + 4 * GMAX;                   // [4][GMAX]
+    float* wacc = wl + 4 * GMAX;                 // [4][GMAX][D]
+    if (qq == 0 && c < G) {
+        wm[wave * GMAX + c] = m_run;
+        wl[wave * GMAX + c] = l_run;
+    }
+#pragma unroll
+    for (int nb2 = 0; nb2 < NB2; ++nb2)
+#pragma unroll
+        for (int e = 0; e < 2; ++e)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int h = 4 * qq + j;
+                if (h < G) wacc[(wave * GMAX + h) * D + 32 * nb2 + 2 * c + e] = o[2 * nb2 + e][j];
+            }
+    __syncthreads();
+    for (int x = tid; x < G * D; x += kThreads) {
+        const int h = x / D, dd = x % D;
+        float M = kNegInf;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) M = fmaxf(M, wm[w * GMAX + h]);
+        float num = 0.f, den = 0.f;
+        if (M != kNegInf) {
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+                const float sc = fast_exp2(wm[w * GMAX + h] - M);
+                num += sc * wacc[(w * GMAX + h) * D + dd];
+                den += sc * wl[w * GMAX + h];
+            }
+        }
+        const size_t bh = (size_t)bl * s.H + kvh * G + h;
+        if (nsplit == 1) {
+            out[bh * D + dd] = num / den;
+        } else {
+            float* p = ws_part + (bh * nsplit + split) * (size_t)(D + 2);
+            p[2 + dd] = num;
+            if (dd == 0) {
+                p[0] = M;
+                p[1] = den;
+            }
+        }
+    }
+}
+
 template <int D>
 __global__ __launch_bounds__(D) void decode_combine_kernel(Shape s, const float* __restrict__ ws_part, int nsplit,
                                                            float* __restrict__ out, const int32_t* __restrict__ steps,
@@ -267,12 +506,20 @@ hipError_t launch_decode_d(const Shape& s, const Rows& rows, size_t lds_bytes, u
 #define TGVKV_DECODE_LAUNCH(GM)                                                                                   \
     hipLaunchKernelGGL((decode_kernel<D, GM, Rows>), grid, block, lds_bytes, st, s, rows, kc, vc, budgets, reserve, \
                        step, steps, q, k_new, v_new, out, ws_part, nsplit, unit_order)
-    if (s.G <= 1) TGVKV_DECODE_LAUNCH(1);
+#define TGVKV_DECODE_MFMA_LAUNCH(GM)                                                                           \
+    hipLaunchKernelGGL((decode_mfma_kernel<D, GM, Rows>), grid, block, lds_bytes, st, s, rows, kc, vc, budgets,     \
+                       reserve, step, steps, q, k_new, v_new, out, ws_part, nsplit, unit_order)
+    if (s.G >= kMfmaMinGroup) {
+        if (s.G <= 4) TGVKV_DECODE_MFMA_LAUNCH(4);
+        else if (s.G <= 8) TGVKV_DECODE_MFMA_LAUNCH(8);
+        else TGVKV_DECODE_MFMA_LAUNCH(16);
+    } else if (s.G <= 1) TGVKV_DECODE_LAUNCH(1);
     else if (s.G <= 2) TGVKV_DECODE_LAUNCH(2);
     else if (s.G <= 4) TGVKV_DECODE_LAUNCH(4);
     else if (s.G <= 8) TGVKV_DECODE_LAUNCH(8);
     else TGVKV_DECODE_LAUNCH(16);
 #undef TGVKV_DECODE_LAUNCH
+#undef TGVKV_DECODE_MFMA_LAUNCH
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || nsplit == 1) return e;
     hipLaunchKernelGGL(decode_combine_kernel<D>, dim3((unsigned)((long long)s.B * s.L * s.H)), dim3(D), 0, st, s,

@@ -229,7 +229,8 @@ def test_compact_bit_exact(lib, head_mode, D):
 
 # ----------------------------------------------------------------------------- decode
 @pytest.mark.parametrize("H,Hkv,D,B,L", [(4, 4, 128, 2, 3), (28, 4, 128, 1, 2), (8, 2, 64, 1, 4),
-                                         (32, 32, 128, 4, 32), (16, 1, 128, 1, 1)])
+                                         (32, 32, 128, 4, 32), (16, 1, 128, 1, 1), (12, 4, 128, 1, 2),
+                                         (10, 2, 64, 2, 2)])
 def test_decode_kernel(lib, H, Hkv, D, B, L):
     torch = _torch()
     rng = np.random.default_rng(H * 100 + D)
