@@ -57,7 +57,7 @@ __global__ __launch_bounds__(kThreads) void score_stats_kernel(Shape s, int rowg
     load_qrows<D, NSLOT, KS>(s, q_text, bl, kvh, rb0, qf, qrow);
     float m[NSLOT], lsum[NSLOT], vsum[NSLOT];
     const uint16_t* kbase = k + ((size_t)bl * s.Hkv + kvh) * (size_t)s.N * D;
-    stats_sweep<D, NSLOT, KS>(s, kbase, 0, s.N, qf, qrow, rb0, NB, tiles, m, lsum, vsum);
+    stats_sweep<D, NSLOT, KS>(s, kbase, 0, s.N, qf, qrow, tiles, m, lsum, vsum);
     if (kp == 0 && lane < 16) {
 #pragma unroll
         for (int sl = 0; sl < NSLOT; ++sl) {
@@ -101,7 +101,7 @@ __global__ __launch_bounds__(kThreads) void score_stats_text_kernel(Shape s, con
     load_qrows<D, NSLOT, KS>(s, q_text, bl, kvh, 0, qf, qrow);
     float m[NSLOT], lsum[NSLOT], vsum[NSLOT];
     const uint16_t* kbase = k + ((size_t)bl * s.Hkv + kvh) * (size_t)s.N * D;
-    stats_sweep<D, NSLOT, KS>(s, kbase, 0, s.N, qf, qrow, 0, NB, tiles, m, lsum, vsum);
+    stats_sweep<D, NSLOT, KS>(s, kbase, 0, s.N, qf, qrow, tiles, m, lsum, vsum);
 
     // the key tiles are free now: [G][N_t] normalisers (base 2), then [G][N_q] vision masses
     float* lse2s = reinterpret_cast<float*>(&tiles[0][0]);

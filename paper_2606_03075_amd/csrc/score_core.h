@@ -203,12 +203,14 @@ __device__ __forceinline__ void load_qrows(const Shape& s, const uint16_t* q_tex
 }
 
 // Statistics sweep over keys [kbeg, kend) of one unit (kbeg a multiple of kTile):
-// per question row the running max (base-2 units), the sum of exp over visible
-// keys and the same sum over vision keys.  On return the key-part-0 waves hold,
-// in lanes 0..15, the merged statistics of their rows; the workgroup is synced.
+// per question row a reference max m (base-2 units, within 8 of the row's largest
+// logit), the sum of exp2(z - m) over visible keys and the same sum over vision
+// keys, so that m + log2(sum) is the row's normaliser.  On return the key-part-0
+// waves hold, in lanes 0..15, the merged statistics of their rows; the workgroup
+// is synced.
 template <int D, int NSLOT, int KS>
 __device__ void stats_sweep(const Shape& s, const uint16_t* kbase, int kbeg, int kend,
-                            const bf16x8 (&qf)[NSLOT][Geo<D>::KSTEPS], const int (&qrow)[NSLOT], int rb0, int NB,
+                            const bf16x8 (&qf)[NSLOT][Geo<D>::KSTEPS], const int (&qrow)[NSLOT],
                             char (*tiles)[Geo<D>::TILE_BYTES], float (&m)[NSLOT], float (&lsum)[NSLOT],
                             float (&vsum)[NSLOT]) {
     using GG = Geo<D>;
@@ -217,13 +219,22 @@ __device__ void stats_sweep(const Shape& s, const uint16_t* kbase, int kbeg, int
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int rs = wave % RSETS, kp = wave / RSETS;
     const int vis0 = s.Ns, vis1 = s.Ns + s.Nv;
+    float tsum[NSLOT];
 #pragma unroll
     for (int sl = 0; sl < NSLOT; ++sl) {
         m[sl] = kNegInf;
-        lsum[sl] = 0.f;
+        tsum[sl] = 0.f;
         vsum[sl] = 0.f;
     }
-    // one tile's statistics; PURE: every key of the tile is a vision key (visible to every question row)
+    // One tile's statistics; PURE: every key of the tile is a vision key (visible to every
+    // question row).  Every row slot is computed, also past the last row block (zero query
+    // fragments, never written): with no per-slot branch the compiler interleaves one slot's
+    // softmax steps with the next slot's MFMAs.  The lane keeps a reference max m per row and
+    // rescales its sums only when some slot of the wave sees a logit more than kSlack above
+    // its reference (one uniform branch per key block, rarely taken); the sums then hold terms
+    // up to 2^kSlack, far from overflow, and m + log2(sum) is the same normaliser.  The text
+    // and vision terms go to separate sums (tsum, vsum), so an all-vision tile adds once.
+    constexpr float kSlack = 8.f;
     auto tile = [&](const char* buf, int key0, auto pure_tag) {
         constexpr bool PURE = decltype(pure_tag)::value;
 #pragma unroll
@@ -232,49 +243,59 @@ __device__ void stats_sweep(const Shape& s, const uint16_t* kbase, int kbeg, int
             bf16x8 kf[GG::KSTEPS];
             load_kfrag<D>(kf, buf, kb, lane);
             const int kfirst = key0 + kb * 16 + (lane >> 4) * 4;  // key of accumulator element 0
+            f32x4 z[NSLOT];
+            float mx[NSLOT];
+            bool grow = false;
 #pragma unroll
             for (int sl = 0; sl < NSLOT; ++sl) {
-                if (rb0 + rs + sl * RSETS >= NB) continue;
                 f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(kf[ks], qf[sl][ks], acc);
                 if (PURE) {
-                    const float z0 = acc[0] * s.scale2, z1 = acc[1] * s.scale2;
-                    const float z2 = acc[2] * s.scale2, z3 = acc[3] * s.scale2;
-                    const float mx = fmaxf(fmaxf(z0, z1), fmaxf(z2, z3));
-                    if (mx > m[sl]) {
-                        const float sc = fast_exp2(m[sl] - mx);
-                        lsum[sl] *= sc;
-                        vsum[sl] *= sc;
-                        m[sl] = mx;
-                    }
-                    const float e = (fast_exp2(z0 - m[sl]) + fast_exp2(z1 - m[sl])) +
-                                    (fast_exp2(z2 - m[sl]) + fast_exp2(z3 - m[sl]));
-                    lsum[sl] += e;
-                    vsum[sl] += e;
+                    z[sl] = acc;  // logits in MFMA units; scaled inside the exponent below
+                    mx[sl] = fmaxf(fmaxf(acc[0], acc[1]), fmaxf(acc[2], acc[3])) * s.scale2;
                 } else {
-                    float z[4];
-                    bool ok[4], isv[4];
-                    float mx = kNegInf;
+                    mx[sl] = kNegInf;
 #pragma unroll
                     for (int j = 0; j < 4; ++j) {
                         const int key = kfirst + j;
-                        ok[j] = (key < kend) & ((key < vis1) | (key - vis1 <= qrow[sl]));
-                        isv[j] = (key >= vis0) & (key < vis1);
-                        z[j] = ok[j] ? acc[j] * s.scale2 : kNegInf;
-                        mx = fmaxf(mx, z[j]);
+                        const bool ok = (key < kend) & ((key < vis1) | (key - vis1 <= qrow[sl]));
+                        z[sl][j] = ok ? acc[j] * s.scale2 : kNegInf;
+                        mx[sl] = fmaxf(mx[sl], z[sl][j]);
                     }
-                    if (mx > m[sl]) {
-                        const float sc = fast_exp2(m[sl] - mx);
-                        lsum[sl] *= sc;
+                }
+                grow |= mx[sl] > m[sl] + kSlack;
+            }
+            if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+#pragma unroll
+                for (int sl = 0; sl < NSLOT; ++sl) {
+                    const float mn = fmaxf(m[sl], mx[sl]);
+                    if (mn != kNegInf) {
+                        const float sc = fast_exp2(m[sl] - mn);
+                        tsum[sl] *= sc;
                         vsum[sl] *= sc;
-                        m[sl] = mx;
+                        m[sl] = mn;
                     }
+                }
+            }
+#pragma unroll
+            for (int sl = 0; sl < NSLOT; ++sl) {
+                if (PURE) {
+                    const float nm = -m[sl];
+                    const float e = (fast_exp2(__builtin_fmaf(z[sl][0], s.scale2, nm)) +
+                                     fast_exp2(__builtin_fmaf(z[sl][1], s.scale2, nm))) +
+                                    (fast_exp2(__builtin_fmaf(z[sl][2], s.scale2, nm)) +
+                                     fast_exp2(__builtin_fmaf(z[sl][3], s.scale2, nm)));
+                    vsum[sl] += e;
+                } else {
+                    const float mu = m[sl] == kNegInf ? 0.f : m[sl];  // a row with no visible key yet
 #pragma unroll
                     for (int j = 0; j < 4; ++j) {
-                        const float e = ok[j] ? fast_exp2(z[j] - m[sl]) : 0.f;
-                        lsum[sl] += e;
-                        vsum[sl] += isv[j] ? e : 0.f;
+                        const int key = kfirst + j;
+                        const float e = fast_exp2(z[sl][j] - mu);  // 0 for a masked key
+                        const bool isv = (key >= vis0) & (key < vis1);
+                        vsum[sl] += isv ? e : 0.f;
+                        tsum[sl] += isv ? 0.f : e;
                     }
                 }
             }
@@ -288,6 +309,8 @@ __device__ void stats_sweep(const Shape& s, const uint16_t* kbase, int kbeg, int
         [&](const char* buf, int key0, int) { tile(buf, key0, std::false_type{}); },
         [&](const char* buf, int key0, int) { tile(buf, key0, std::true_type{}); },
         [](int, int) {});
+#pragma unroll
+    for (int sl = 0; sl < NSLOT; ++sl) lsum[sl] = tsum[sl] + vsum[sl];
     // the four lane quarters of a wave saw different keys of the same rows
 #pragma unroll
     for (int sl = 0; sl < NSLOT; ++sl) {

@@ -122,7 +122,7 @@ __global__ __launch_bounds__(kThreads) void score_fused_kernel(
                 float m[NSLOT], lsum[NSLOT], vsum[NSLOT];
                 const uint16_t* kbase = k + (size_t)u * s.N * D;
                 const int kb = sp * fp.cs, ke = min(s.N, kb + fp.cs);
-                stats_sweep<D, NSLOT, KS>(s, kbase, kb, ke, qf, qrow, 0, NB, tiles, m, lsum, vsum);
+                stats_sweep<D, NSLOT, KS>(s, kbase, kb, ke, qf, qrow, tiles, m, lsum, vsum);
                 if (kp == 0 && lane < 16) {
 #pragma unroll
                     for (int sl = 0; sl < NSLOT; ++sl) {
