@@ -84,24 +84,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(Shape s, Rows rows, ui
     const uint16_t* knew = k_new + ((size_t)bl * s.Hkv + kvh) * D;
     const uint16_t* vnew = v_new + ((size_t)bl * s.Hkv + kvh) * D;
 
-    if (split == 0 && tid < LPR) {
-        const size_t r = rows.row(bsz + st);
-        store16(kc + r + tid * 8, load16(knew + tid * 8));
-        store16(vc + r + tid * 8, load16(vnew + tid * 8));
-    }
-
-    float qv[GMAX][8];
-#pragma unroll
-    for (int h = 0; h < GMAX; ++h) {
-        if (h < G) {
-            unpack8(load16(q + ((size_t)bl * s.H + kvh * G + h) * D + sub * 8), qv[h]);
-#pragma unroll
-            for (int e = 0; e < 8; ++e) qv[h][e] *= s.scale2;
-        } else {
-#pragma unroll
-            for (int e = 0; e < 8; ++e) qv[h][e] = 0.f;
-        }
-    }
+    float qv[GMAX][8];  // the scaled query heads, set once the first block's loads are in flight
 
     const int per = (len + nsplit - 1) / nsplit;
     const int t0 = min(split * per, len), t1 = min(t0 + per, len);
@@ -173,12 +156,34 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(Shape s, Rows rows, ui
     u32x4 ka[kUnroll], va[kUnroll], kb[kUnroll], vb[kUnroll];
     int n0 = t0 + grp;
     issue(ka, va, n0);
+    {
+        // the query's latency overlaps the first block's: wait for it (and only it) here
+        u32x4 qr[GMAX];
+#pragma unroll
+        for (int h = 0; h < GMAX; ++h) {
+            const u32x4 z = {0u, 0u, 0u, 0u};
+            qr[h] = h < G ? load16(q + ((size_t)bl * s.H + kvh * G + h) * D + sub * 8) : z;
+            settle(qr[h]);
+        }
+#pragma unroll
+        for (int h = 0; h < GMAX; ++h) {
+            unpack8(qr[h], qv[h]);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) qv[h][e] *= s.scale2;
+        }
+    }
     for (int pi = 0; pi < pairs; ++pi) {
         issue(kb, vb, n0 + S);
         consume(ka, va, n0);
         issue(ka, va, n0 + 2 * S);
         consume(kb, vb, n0 + S);
         n0 += 2 * S;
+    }
+    // the step's token into its cache slot (this launch reads it from k_new / v_new)
+    if (split == 0 && tid < LPR) {
+        const size_t r = rows.row(bsz + st);
+        store16(kc + r + tid * 8, load16(knew + tid * 8));
+        store16(vc + r + tid * 8, load16(vnew + tid * 8));
     }
 
     // merge the lane groups of the wave
@@ -302,12 +307,6 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(Shape s, Rows row
     const uint16_t* knew = k_new + ((size_t)bl * s.Hkv + kvh) * D;
     const uint16_t* vnew = v_new + ((size_t)bl * s.Hkv + kvh) * D;
 
-    if (split == 0 && tid < VCH) {
-        const size_t r = rows.row(bsz + st);
-        store16(kc + r + tid * 8, load16(knew + tid * 8));
-        store16(vc + r + tid * 8, load16(vnew + tid * 8));
-    }
-
     // B operand of S^T: query head c (zero for the padding heads), 8 dims of the lane's quarter per k-step
     bf16x8 qf[KSTEPS];
     {
@@ -427,6 +426,12 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(Shape s, Rows row
         n0 += 64;
     }
 
+    // the step's token into its cache slot (this launch reads it from k_new / v_new)
+    if (split == 0 && tid < VCH) {
+        const size_t r = rows.row(bsz + st);
+        store16(kc + r + tid * 8, load16(knew + tid * 8));
+        store16(vc + r + tid * 8, load16(vnew + tid * 8));
+    }
     // the four lane quarters summed different tokens of each head
     l_run = sum_xor32(sum_xor16(l_run));
     __syncthreads();  // every wave is done with its stage: the merge reuses it
