@@ -537,10 +537,10 @@ hipError_t launch_decode_d(const Shape& s, const Rows& rows, size_t lds_bytes, u
 int decode_splits(const Shape& s) {
     const long long units = (long long)s.B * s.L * s.Hkv;
     if (units <= 0) return 1;
-    // split a unit's tokens only while the grid would leave workgroup slots idle: 8 per CU
-    // for the VALU kernel, 4 for the matrix-core one (its occupancy); a split costs partial
-    // writes and the combine launch (at the Qwen2-VL shape, 896 units: 40.8 us unsplit
-    // against 46.3 us in two splits)
+    // split a unit's tokens only up to about 2048 workgroups for the VALU kernel (two rounds
+    // of its 4 workgroups per CU) and 1024 for the matrix-core one (one round): a split costs
+    // partial writes and the combine launch (at the Qwen2-VL shape, 896 units: 40.8 us
+    // unsplit against 46.3 us in two splits)
     long long n = (s.G >= kMfmaMinGroup ? 1024 : 2048) / units;
     if (n < 1) n = 1;
     if (n > 8) n = 8;
