@@ -349,3 +349,46 @@ def test_score_matches_oracle(lib, name, head_mode, fused):
     torch.cuda.synchronize()
     assert np.array_equal(s1[0], host(buf.s_vis)) and np.array_equal(s1[1], host(buf.s_txt))
     assert np.array_equal(s1[2], host(buf.tv_mass))
+
+
+def _ramp_inputs(cfg, direction, seed=11):
+    """Text queries all close to one direction u and keys whose component along u ramps over the
+    sequence, so every text row's logits climb (or fall) along the keys by about 30 in base-2 units:
+    the statistics sweep's running reference max moves many times and its sums hold terms far above 1
+    between moves."""
+    rng = np.random.default_rng(seed)
+    B, L, H, Hkv, D, N = cfg.batch, cfg.layers, cfg.heads_q, cfg.heads_kv, cfg.head_dim, cfg.n_tokens
+    u = rng.standard_normal(D).astype(np.float32)
+    u /= np.linalg.norm(u)
+    q = 12.0 * u + 0.2 * rng.standard_normal((B, L, H, cfg.n_text, D)).astype(np.float32)
+    a = np.linspace(-4.0, 16.0, N, dtype=np.float32)
+    if direction == "falling":
+        a = a[::-1].copy()
+    elif direction == "zigzag":
+        a = np.where(np.arange(N) % 97 < 48, a, -a)
+    k = a[:, None] * u + 0.3 * rng.standard_normal((B, L, Hkv, N, D)).astype(np.float32)
+    return f32_to_bf16_bits(q.astype(np.float32)), f32_to_bf16_bits(k.astype(np.float32))
+
+
+@pytest.mark.parametrize("fused", [False, True])
+@pytest.mark.parametrize("direction", ["rising", "falling", "zigzag"])
+@pytest.mark.parametrize("shape", ["gqa7_d128", "four_blocks"])
+def test_score_moving_max(lib, shape, direction, fused):
+    """Logits that climb along the keys: the reference max of every row moves again and again, with
+    up to 2^8-sized terms summed between moves; the scores still match the oracle."""
+    torch = _torch()
+    cfg = SCORE_SHAPES[shape]
+    log(f"score moving max {shape} {direction} fused={fused}")
+    qb, kb = _ramp_inputs(cfg, direction)
+    p = bd.problem_from(cfg)
+    buf = bd.EvictionBuffers(p, bd.make_opts(), 0, 1)
+    buf.score(dev_bf16(qb), dev_bf16(kb), bd.SCORE_ALL | (bd.SCORE_FUSED if fused else 0))
+    torch.cuda.synchronize()
+    for b in range(cfg.batch):
+        for l in range(cfg.layers):
+            r = oracle_scores(qb[b, l], kb[b, l], cfg, 0)
+            assert_close_rel("lse", host(buf.lse[b, l]), r["lse"], atol=1e-4)
+            assert_close_rel("s_txt", host(buf.s_txt[b, l]), r["s_txt"])
+            assert_close_rel("w_txt", host(buf.w_txt[b, l]), r["w_txt"])
+            assert_close_rel("tv_mass", host(buf.tv_mass[b, l]), r["tv_mass"])
+            assert_close_rel("s_vis", host(buf.s_vis[b, l]), r["s_vis"])
