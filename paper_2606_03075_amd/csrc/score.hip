@@ -134,7 +134,8 @@ __global__ __launch_bounds__(kThreads) void score_stats_text_kernel(Shape s, con
     if (lds_text) {
         // the unit's text keys go into the freed tiles after the normalisers and masses
         const size_t off = ((size_t)s.G * (s.Nt + s.Nq) * sizeof(float) + 15) & ~(size_t)15;
-        text_pass_lds<D>(s, bl, kvh, q_text, k, lse, lse2s, &tiles[0][0] + off, ws_colsum);
+        text_pass_lds<D>(s, bl, kvh, q_text, k, lse, lse2s, &tiles[0][0] + off,
+                         2LL * Geo<D>::TILE_BYTES - (long long)off, ws_colsum);
     } else {
         text_pass<D>(s, bl, kvh, q_text, k, lse, lse2s, ws_colsum);
     }
@@ -370,14 +371,16 @@ hipError_t launch_score_stats_text(const Shape& s, const RowPlan& rp, const uint
     const long long nblk = (long long)s.B * s.L * s.Hkv;
     if (nblk == 0) return hipSuccess;
     dim3 grid((unsigned)nblk), block(kThreads);
-    // the text pass stages the unit's text keys in the freed key tiles when they fit there
+    // the text pass stages the unit's text keys (in chunks of key blocks, if need be) in the
+    // freed key tiles, after the normalisers and masses, when its partials and the system
+    // keys' blocks fit there
     const long long head = ((long long)s.G * (s.Nt + s.Nq) * 4 + 15) / 16 * 16;
     if (s.D == 128) {
-        const int lds_text = head + text_lds_bytes<128>(s.G, s.Nt) <= 2LL * Geo<128>::TILE_BYTES;
+        const int lds_text = text_lds_fits<128>(s.G, s.Ns, s.Nt, 2LL * Geo<128>::TILE_BYTES - head);
         TGVKV_ROWPLAN_DISPATCH(score_stats_text_kernel, 128, rp, grid, block, 0, st, s, q_text, k, lse, ws_vm,
                                ws_colsum, ws_vmh, lds_text);
     } else {
-        const int lds_text = head + text_lds_bytes<64>(s.G, s.Nt) <= 2LL * Geo<64>::TILE_BYTES;
+        const int lds_text = text_lds_fits<64>(s.G, s.Ns, s.Nt, 2LL * Geo<64>::TILE_BYTES - head);
         TGVKV_ROWPLAN_DISPATCH(score_stats_text_kernel, 64, rp, grid, block, 0, st, s, q_text, k, lse, ws_vm,
                                ws_colsum, ws_vmh, lds_text);
     }

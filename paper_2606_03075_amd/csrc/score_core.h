@@ -610,38 +610,51 @@ __device__ void text_pass(const Shape& s, int bl, int kvh, const uint16_t* __res
     __syncthreads();
 }
 
-// LDS bytes text_pass_lds needs beyond the [G][N_t] normalisers and [G][N_q] vision
-// masses that precede it: the unit's text keys (16-row blocks, padded rows) and one
-// column-sum partial per wave and query head.
+// LDS layout of text_pass_lds in kl_bytes of 16-byte aligned LDS: the per-wave column
+// partials [4][G][TK] (TK = N_t rounded up to 16 rows), then as many 16-row blocks of
+// text keys as fit.  text_chunk_blocks gives that count; the pass needs at least the
+// system keys' blocks and one block (else it is not used).
 template <int D>
-__host__ __device__ constexpr long long text_lds_bytes(int G, int Nt) {
-    return (long long)((Nt + 15) / 16) * 16 * Geo<D>::ROWB + 4LL * G * ((Nt + 15) / 16) * 16 * (long long)sizeof(float);
+__host__ __device__ constexpr long long text_part_bytes(int G, int Nt) {
+    return ((4LL * G * ((Nt + 15) / 16) * 16 * (long long)sizeof(float)) + 15) / 16 * 16;
+}
+template <int D>
+__host__ __device__ constexpr int text_chunk_blocks(int G, int Nt, long long kl_bytes) {
+    return (int)((kl_bytes - text_part_bytes<D>(G, Nt)) / (16LL * Geo<D>::ROWB));
+}
+template <int D>
+__host__ __device__ constexpr bool text_lds_fits(int G, int Ns, int Nt, long long kl_bytes) {
+    return kl_bytes > text_part_bytes<D>(G, Nt) &&
+           text_chunk_blocks<D>(G, Nt, kl_bytes) >= ((Ns + 15) / 16 > 1 ? (Ns + 15) / 16 : 1);
 }
 
-// The text pass of text_pass with the unit's text keys staged in LDS first (one
-// round of loads by the whole workgroup), for units whose text keys fit beside the
-// normalisers in the freed key tiles.  Each wave then owns 16-row blocks of text
-// rows: it fetches a block's query fragments from global memory (the next item's
-// while the current one is used) and reads every key block it needs from LDS, so
-// the pass costs a few load latencies instead of one per (row block, key block).
-// Column sums: per (row block, key block) the 16 rows' probabilities are summed
-// across the lane groups and added to the wave's own LDS partial for those keys;
-// the four waves' partials are then added in wave order.  lse2s holds [G][N_t]
-// base-2 normalisers (the question rows' on entry); kl points at 16-byte aligned
-// LDS of text_lds_bytes<D>(G, N_t) bytes.
+// The text pass of text_pass with the unit's text keys staged in LDS (one round of
+// loads by the whole workgroup per chunk of key blocks).  Each wave owns 16-row blocks
+// of text rows: it fetches a block's query fragments from global memory (the next
+// item's while the current one is used) and reads every key block it needs from LDS,
+// so the pass costs a few load latencies per chunk instead of one per (row block, key
+// block).  When the text keys do not all fit, they are staged in chunks of key blocks
+// and each row block is revisited for every chunk up to its own keys (the causal mask
+// keeps row block rb to key blocks <= rb).  The system keys are in the first chunk.
+// Column sums: per (row block, key block) the 16 rows' probabilities are summed across
+// the lane groups and added to the wave's own LDS partial for those keys; the four
+// waves' partials are then added in wave order.  lse2s holds [G][N_t] base-2
+// normalisers (the question rows' on entry); kl points at kl_bytes of 16-byte aligned
+// LDS with text_lds_fits<D>(G, N_s, N_t, kl_bytes).
 template <int D>
 __device__ void text_pass_lds(const Shape& s, int bl, int kvh, const uint16_t* __restrict__ q_text,
                               const uint16_t* __restrict__ k, float* __restrict__ lse, float* lse2s, char* kl,
-                              float* __restrict__ ws_colsum) {
+                              long long kl_bytes, float* __restrict__ ws_colsum) {
     using GG = Geo<D>;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const size_t head0 = (size_t)bl * s.H + kvh * s.G;
     const uint16_t* kbase = k + ((size_t)bl * s.Hkv + kvh) * (size_t)s.N * D;
     const int TB = (s.Nt + 15) >> 4;
-    const int TK = TB * 16;                                       // staged key rows (last one repeated)
-    float* part = reinterpret_cast<float*>(kl + (size_t)TK * GG::ROWB);  // [4 waves][G][TK]
+    const int TK = TB * 16;                                       // key rows (the last block padded)
+    float* part = reinterpret_cast<float*>(kl);                   // [4 waves][G][TK]
+    char* kst = kl + text_part_bytes<D>(s.G, s.Nt);               // staged key blocks
+    const int KC = min(text_chunk_blocks<D>(s.G, s.Nt, kl_bytes), TB);
     const int SB = (s.Ns + 15) >> 4;
-    const int items = s.G * TB;
 
     const int koff = (lane >> 4) * 8;
     auto load_q = [&](bf16x8 (&f)[GG::KSTEPS], int g, int row) {
@@ -653,38 +666,45 @@ __device__ void text_pass_lds(const Shape& s, int bl, int kvh, const uint16_t* _
         const int it = min(item, s.G * SB - 1);
         load_q(f, it / SB, min((it % SB) * 16 + (lane & 15), s.Ns - 1));
     };
-    auto col_item_q = [&](bf16x8 (&f)[GG::KSTEPS], int item) {
-        const int it = min(item, items - 1);
-        load_q(f, it / TB, min((it % TB) * 16 + (lane & 15), s.Nt - 1));
+    // column items of a chunk starting at key block c0: row blocks rb >= c0 of every head
+    auto col_item_q = [&](bf16x8 (&f)[GG::KSTEPS], int item, int c0) {
+        const int nrb = TB - c0;
+        const int it = min(item, s.G * nrb - 1);
+        load_q(f, it / nrb, min((c0 + it % nrb) * 16 + (lane & 15), s.Nt - 1));
     };
 
-    // one round of loads: the text keys (text order: system keys, then question keys), this
-    // wave's first system-row block and its first column item; then the keys go to LDS
+    // one round of loads: key blocks [c0, c1) (text order: system keys, then question keys),
+    // with this wave's first items' query fragments; then the keys go to LDS
     constexpr int kStage = 8;  // 16-byte key loads per thread per round
     bf16x8 qs[GG::KSTEPS], qa[GG::KSTEPS], qb[GG::KSTEPS];
-    for (int c0 = 0; c0 < TK * GG::CPR; c0 += kStage * kThreads) {
-        u32x4 r[kStage];
+    auto stage = [&](int c0, int c1) {
+        const int nch = (c1 - c0) * 16 * GG::CPR;
+        for (int x0 = 0; x0 < nch; x0 += kStage * kThreads) {
+            u32x4 r[kStage];
 #pragma unroll
-        for (int i = 0; i < kStage; ++i) {
-            const int c = min(c0 + i * kThreads + tid, TK * GG::CPR - 1);
-            const int t = min(c / GG::CPR, s.Nt - 1);
-            const int pos = t < s.Ns ? t : t + s.Nv;
-            r[i] = load16(kbase + (size_t)pos * D + (c % GG::CPR) * 8);
-        }
-        if (c0 == 0) {
-            if (SB > 0) sys_item_q(qs, wave);
-            col_item_q(qa, wave);
-        }
+            for (int i = 0; i < kStage; ++i) {
+                const int c = min(x0 + i * kThreads + tid, nch - 1);
+                const int t = min(c0 * 16 + c / GG::CPR, s.Nt - 1);
+                const int pos = t < s.Ns ? t : t + s.Nv;
+                r[i] = load16(kbase + (size_t)pos * D + (c % GG::CPR) * 8);
+            }
+            if (x0 == 0) {
+                if (c0 == 0 && SB > 0) sys_item_q(qs, wave);
+                col_item_q(qa, wave, c0);
+            }
 #pragma unroll
-        for (int i = 0; i < kStage; ++i) {
-            const int c = c0 + i * kThreads + tid;
-            if (c < TK * GG::CPR) store16(kl + (c / GG::CPR) * GG::ROWB + (c % GG::CPR) * 16, r[i]);
+            for (int i = 0; i < kStage; ++i) {
+                const int c = x0 + i * kThreads + tid;
+                if (c < nch) store16(kst + (c / GG::CPR) * GG::ROWB + (c % GG::CPR) * 16, r[i]);
+            }
         }
-    }
+    };
+    stage(0, KC);
     for (int x = tid; x < 4 * s.G * TK; x += kThreads) part[x] = 0.f;
     __syncthreads();
 
-    // system rows x system keys: row normalisers (C[key][row]: a lane owns row i)
+    // system rows x system keys (all in the first chunk): row normalisers (C[key][row]: a
+    // lane owns row i)
     for (int item = wave; item < s.G * SB; item += 4) {
         const int g = item / SB, rb = item % SB;
         const int i = rb * 16 + (lane & 15);
@@ -692,7 +712,7 @@ __device__ void text_pass_lds(const Shape& s, int bl, int kvh, const uint16_t* _
         float m = kNegInf, l = 0.f;
         for (int kb = 0; kb <= rb; ++kb) {
             bf16x8 kf[GG::KSTEPS];
-            load_kfrag<D>(kf, kl, kb, lane);
+            load_kfrag<D>(kf, kst, kb, lane);
             f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(kf[ks], qs[ks], acc);
@@ -726,44 +746,56 @@ __device__ void text_pass_lds(const Shape& s, int bl, int kvh, const uint16_t* _
     }
     __syncthreads();
 
-    // all text rows x text keys (C[row][key]: a lane owns key j, rows 4*(lane/16) + jj)
-    auto consume = [&](const bf16x8 (&qf)[GG::KSTEPS], int item) {
-        const int g = item / TB, rb = item % TB;
-        float* wpart = part + ((size_t)wave * s.G + g) * TK;
-        float l2[4];
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) l2[jj] = lse2s[g * s.Nt + min(rb * 16 + (lane >> 4) * 4 + jj, s.Nt - 1)];
-        for (int kb = 0; kb <= rb; ++kb) {
-            bf16x8 kf[GG::KSTEPS];
-            load_kfrag<D>(kf, kl, kb, lane);
-            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(qf[ks], kf[ks], acc);
-            const int j = kb * 16 + (lane & 15);
-            float col = 0.f;
-#pragma unroll
-            for (int jj = 0; jj < 4; ++jj) {
-                const int ii = rb * 16 + (lane >> 4) * 4 + jj;
-                if (ii < s.Nt && j <= ii) col += fast_exp2(acc[jj] * s.scale2 - l2[jj]);
-            }
-            col = sum_xor32(sum_xor16(col));
-            if (lane < 16) wpart[j] += col;
+    // all text rows x text keys (C[row][key]: a lane owns key j, rows 4*(lane/16) + jj), one
+    // chunk of key blocks [c0, c1) at a time
+    for (int c0 = 0; c0 < TB; c0 += KC) {
+        const int c1 = min(c0 + KC, TB);
+        if (c0 > 0) {
+            stage(c0, c1);
+            __syncthreads();
         }
-    };
-    // this wave's items are wave, wave + 4, ...: two register sets, the next item's fragments
-    // fetched while the current one is used (qa already holds the first)
-    const int steps = (items + 3) / 4;
-    int item = wave;
-    for (int st = 0; st < steps; st += 2) {
-        const int nx = item + 4;
-        col_item_q(qb, nx);
-        if (item < items) consume(qa, item);
-        const int nx2 = item + 8;
-        col_item_q(qa, nx2);
-        if (nx < items) consume(qb, nx);
-        item = nx2;
+        const int nrb = TB - c0;
+        const int items = s.G * nrb;
+        auto consume = [&](const bf16x8 (&qf)[GG::KSTEPS], int item) {
+            const int g = item / nrb, rb = c0 + item % nrb;
+            float* wpart = part + ((size_t)wave * s.G + g) * TK;
+            float l2[4];
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj)
+                l2[jj] = lse2s[g * s.Nt + min(rb * 16 + (lane >> 4) * 4 + jj, s.Nt - 1)];
+            const int kend = min(rb, c1 - 1);
+            for (int kb = c0; kb <= kend; ++kb) {
+                bf16x8 kf[GG::KSTEPS];
+                load_kfrag<D>(kf, kst, kb - c0, lane);
+                f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(qf[ks], kf[ks], acc);
+                const int j = kb * 16 + (lane & 15);
+                float col = 0.f;
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) {
+                    const int ii = rb * 16 + (lane >> 4) * 4 + jj;
+                    if (ii < s.Nt && j <= ii) col += fast_exp2(acc[jj] * s.scale2 - l2[jj]);
+                }
+                col = sum_xor32(sum_xor16(col));
+                if (lane < 16) wpart[j] += col;
+            }
+        };
+        // this wave's items are wave, wave + 4, ...: two register sets, the next item's
+        // fragments fetched while the current one is used (qa already holds the first)
+        const int steps = (items + 3) / 4;
+        int item = wave;
+        for (int st = 0; st < steps; st += 2) {
+            const int nx = item + 4;
+            col_item_q(qb, nx, c0);
+            if (item < items) consume(qa, item);
+            const int nx2 = item + 8;
+            col_item_q(qa, nx2, c0);
+            if (nx < items) consume(qb, nx);
+            item = nx2;
+        }
+        __syncthreads();  // the chunk's keys are done with before the next is staged
     }
-    __syncthreads();
     for (int x = tid; x < s.G * s.Nt; x += kThreads) {
         const int g = x / s.Nt, j = x % s.Nt;
         float a = 0.f;
