@@ -26,6 +26,8 @@
 // These kernels serve phase-by-phase calls (and the vision pass restricted to
 // layers whose budget reaches past the text); score_fused.hip runs the same
 // building blocks as one persistent kernel.
+#include <algorithm>
+
 #include "score_core.h"
 
 namespace tgvkv {
@@ -229,12 +231,15 @@ __global__ __launch_bounds__(kThreads) void score_vision_kernel(Shape s, int row
                                                                 const int32_t* __restrict__ budgets,
                                                                 int vis_threshold,
                                                                 float* __restrict__ ws_part,
-                                                                float* __restrict__ ws_vm, int out_tiles) {
+                                                                float* __restrict__ ws_vm, int out_tiles,
+                                                                int vsplit) {
     constexpr int RSETS = 4 / KS;
     __shared__ __attribute__((aligned(16))) char tiles[2][Geo<D>::TILE_BYTES];
     __shared__ float red[2][RSETS][kTile];
     extern __shared__ float obuf[];  // out_tiles * kTile scores
     int bid = blockIdx.x;
+    const int sp = bid % vsplit;  // this workgroup's share of the vision keys
+    bid /= vsplit;
     const int rg = bid % rowgroups;
     bid /= rowgroups;
     const int kvh = bid % s.Hkv;
@@ -261,7 +266,10 @@ __global__ __launch_bounds__(kThreads) void score_vision_kernel(Shape s, int row
     const uint16_t* kvis = k + (((size_t)bl * s.Hkv + kvh) * (size_t)s.N + s.Ns) * D;
     float* out = ws_part + (((size_t)bl * s.Hkv + kvh) * rowgroups + rg) * (size_t)s.Nv;
     float rsum[NSLOT][4];
-    vision_sweep<D, NSLOT, KS, MASS>(s, kvis, 0, s.Nv, qf, lse2, coef, rb0, NB, tiles, red, obuf, out_tiles, out,
+    // every key's score is a sum over this workgroup's rows only, so the keys split freely
+    const int per_t = ((s.Nv + kTile - 1) / kTile + vsplit - 1) / vsplit;
+    const int vbeg = min(sp * per_t * kTile, s.Nv), vend = min(vbeg + per_t * kTile, s.Nv);
+    vision_sweep<D, NSLOT, KS, MASS>(s, kvis, vbeg, vend, qf, lse2, coef, rb0, NB, tiles, red, obuf, out_tiles, out,
                                      rsum);
     if (MASS) {
         // each row's vision mass: the sum of its probabilities over all vision keys
@@ -424,30 +432,36 @@ hipError_t launch_score_fin(const Shape& s, const float* ws_colsum, const float*
 hipError_t launch_score_vision(const Shape& s, const RowPlan& rp, const uint16_t* q_text, const uint16_t* k,
                                const float* lse, const float* w_txt, const int32_t* budgets,
                                int32_t vis_threshold, float* ws_part, float* ws_vm, hipStream_t st) {
-    const long long nblk = (long long)s.B * s.L * s.Hkv * rp.rowgroups;
+    const bool mass = ws_vm != nullptr;
+    // With few (unit, row group) workgroups the vision keys are split over several: at the
+    // Qwen2-VL shape (896 units, 2 workgroups per CU) two splits balance the last round
+    // (805 -> 740 us); at 4096 units a split only adds prologues.  The mass-collecting variant
+    // keeps one range (its row sums would need a merge).
+    const long long units = (long long)s.B * s.L * s.Hkv * rp.rowgroups;
+    const int vsplit = mass || units <= 0 ? 1 : (int)std::min<long long>(std::max<long long>(2048 / units, 1), 4);
+    const long long nblk = units * vsplit;
     if (nblk == 0 || s.Nv == 0) return hipSuccess;
     dim3 grid((unsigned)nblk), block(kThreads);
     // a unit's scores are kept in LDS and written once at the end when they fit (no global
     // store among the key loads); otherwise in bursts of kOutTiles tiles
-    const int ntiles = (s.Nv + kTile - 1) / kTile;
-    const bool mass = ws_vm != nullptr;
+    const int ntiles = ((s.Nv + kTile - 1) / kTile + vsplit - 1) / vsplit;
     const int out_tiles = (!mass && ntiles * kTile * (int)sizeof(float) <= kWholeOutBytes) ? ntiles : kOutTiles;
     const size_t obytes = (size_t)out_tiles * kTile * sizeof(float);
     if (mass) {
-        if (s.D == 128) TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 128, true, rp, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles);
-        else TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 64, true, rp, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles);
+        if (s.D == 128) TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 128, true, rp, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles, vsplit);
+        else TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 64, true, rp, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles, vsplit);
     } else if (rp.nslot == 1 && rp.ks == 1) {
         // four 16-row blocks per unit: the vision sweep runs faster with every wave holding all
         // four blocks over a quarter of each key tile (same row groups, so the same partials)
         if (s.D == 128)
             hipLaunchKernelGGL((score_vision_kernel<128, 4, 4, false>), grid, block, obytes, st, s, rp.rowgroups,
-                               q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles);
+                               q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles, vsplit);
         else
             hipLaunchKernelGGL((score_vision_kernel<64, 4, 4, false>), grid, block, obytes, st, s, rp.rowgroups,
-                               q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles);
+                               q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles, vsplit);
     } else {
-        if (s.D == 128) TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 128, false, rp, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles);
-        else TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 64, false, rp, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles);
+        if (s.D == 128) TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 128, false, rp, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles, vsplit);
+        else TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 64, false, rp, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles, vsplit);
     }
     return hipGetLastError();
 }
