@@ -237,6 +237,10 @@ tgvkv_status tgvkv_compact(const tgvkv_problem* problem, const tgvkv_opts* opts,
  * segment, then for each query head h computes
  *   out[b][l][h] = softmax_n(tau q[b][l][h] . Kc[n]) Vc[n],  n < b_l + step + 1.
  * Steps must run in order 0, 1, ... on the same cache; 0 <= step < decode_reserve.
+ * Arithmetic: logits and sums in fp32.  Up to 2 query heads per KV head the products
+ * are fp32 on the vector units; from 3 on they run on the matrix cores, with the
+ * probabilities entering P V as a high and a low bf16 part (about 16 significant
+ * bits), so results differ from the vector path in the last bits only.
  *
  * q      bf16 [B][L][heads_q][head_dim];  k_new, v_new bf16 [B][L][heads_kv][head_dim]
  * out    f32  [B][L][heads_q][head_dim]
