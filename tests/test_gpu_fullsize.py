@@ -77,16 +77,18 @@ def test_stress13b_full(lib):
     log(f"  stress13b budgets seq0: {buf.budgets[0].tolist()}")
 
 
-def test_llavanext_paged_full(lib):
+@pytest.mark.parametrize("name", ["llavanext", "qwen2vl_video"])
+def test_paged_full(lib, name):
     """The bench's paged launch configuration at full size (16-row pages, longest-first order):
     the pool gathered through the table equals the contiguous cache bit for bit, and 16 decode
-    steps with a per-sequence step vector equal the contiguous decode bit for bit."""
+    steps with a per-sequence step vector equal the contiguous decode bit for bit (one query
+    head per KV head at LLaVA-NeXT, the matrix-core decode at Qwen2-VL's seven)."""
     import torch
     from paper_2606_03075_amd import binding as bd
     from tests.test_gpu_e2e import _inputs
     from workloads import total_budget
 
-    cfg = CONFIGS["llavanext"]
+    cfg = CONFIGS[name]
     T, page = 16, 16
     t, dec, dev_t, dev_dec = _inputs(cfg, 0, T, [0, 1])
     p = bd.problem_from(cfg)
@@ -124,4 +126,4 @@ def test_llavanext_paged_full(lib):
             seg = src[base: base + Hkv * rows * D].view(Hkv, rows, D)
             got = pool_t[pages].permute(1, 0, 2, 3).reshape(Hkv, n_pg * page, D)[:, :rows]
             assert torch.equal(got, seg), bl
-    log(f"  llavanext paged: {cfg.batch * L} segments, {n_pages} pages, table width {width}")
+    log(f"  {name} paged: {cfg.batch * L} segments, {n_pages} pages, table width {width}")
