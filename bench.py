@@ -84,9 +84,10 @@ def parse():
 
 
 def source_hash(files):
-    """Hash of a kernel's sources and of the device compile flags (either changes the code)."""
+    """Hash of a kernel's sources and of the device compile flags of its main (first)
+    source (either changes the code)."""
     from paper_2606_03075_amd import build as _build
-    h = hashlib.sha256(" ".join(_build.device_flags()).encode())
+    h = hashlib.sha256(" ".join(_build.device_flags(files[0])).encode())
     for f in files:
         with open(os.path.join(ROOT, "paper_2606_03075_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
