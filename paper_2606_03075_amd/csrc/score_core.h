@@ -230,13 +230,23 @@ __device__ void stats_sweep(const Shape& s, const uint16_t* kbase, int kbeg, int
     // question row).  Every row slot is computed, also past the last row block (zero query
     // fragments, never written): with no per-slot branch the compiler interleaves one slot's
     // softmax steps with the next slot's MFMAs.  The lane keeps a reference max m per row and
-    // rescales its sums only when some slot of the wave sees a logit more than kSlack above
-    // its reference (one uniform branch per key block, rarely taken); the sums then hold terms
-    // up to 2^kSlack, far from overflow, and m + log2(sum) is the same normaliser.  The text
-    // and vision terms go to separate sums (tsum, vsum), so an all-vision tile adds once.
+    // rescales its sums only when needed (one uniform branch per key block, rarely taken), so
+    // the sums hold terms up to about 2^kSlack, far from overflow, and m + log2(sum) is the
+    // same normaliser.  An all-vision block exponentiates against the current reference
+    // first and rescales when the 4 terms of a lane sum past 2^kSlack (an overflow to inf,
+    // the first block's case, included): it needs no max of its own.  A masked block tests
+    // its largest visible logit against m + kSlack.  The text and vision terms go to
+    // separate sums (tsum, vsum), so an all-vision block adds once.
     constexpr float kSlack = 8.f;
+    constexpr float kSlackSum = 256.f;  // 2^kSlack
     auto tile = [&](const char* buf, int key0, auto pure_tag) {
         constexpr bool PURE = decltype(pure_tag)::value;
+        // sum of a slot's 4 all-vision terms against its reference max
+        auto pure_terms = [&](const f32x4& zz, float mref) {
+            const float nm = -mref;
+            return (fast_exp2(__builtin_fmaf(zz[0], s.scale2, nm)) + fast_exp2(__builtin_fmaf(zz[1], s.scale2, nm))) +
+                   (fast_exp2(__builtin_fmaf(zz[2], s.scale2, nm)) + fast_exp2(__builtin_fmaf(zz[3], s.scale2, nm)));
+        };
 #pragma unroll
         for (int kbi = 0; kbi < KBW; ++kbi) {
             const int kb = kp + kbi * KS;
@@ -244,7 +254,7 @@ __device__ void stats_sweep(const Shape& s, const uint16_t* kbase, int kbeg, int
             load_kfrag<D>(kf, buf, kb, lane);
             const int kfirst = key0 + kb * 16 + (lane >> 4) * 4;  // key of accumulator element 0
             f32x4 z[NSLOT];
-            float mx[NSLOT];
+            float mx[NSLOT];  // PURE: the slot's term sum; masked: its largest visible logit
             bool grow = false;
 #pragma unroll
             for (int sl = 0; sl < NSLOT; ++sl) {
@@ -252,8 +262,9 @@ __device__ void stats_sweep(const Shape& s, const uint16_t* kbase, int kbeg, int
 #pragma unroll
                 for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(kf[ks], qf[sl][ks], acc);
                 if (PURE) {
-                    z[sl] = acc;  // logits in MFMA units; scaled inside the exponent below
-                    mx[sl] = fmaxf(fmaxf(acc[0], acc[1]), fmaxf(acc[2], acc[3])) * s.scale2;
+                    z[sl] = acc;  // logits in MFMA units; scaled inside the exponent
+                    mx[sl] = pure_terms(acc, m[sl]);
+                    grow |= !(mx[sl] <= kSlackSum);
                 } else {
                     mx[sl] = kNegInf;
 #pragma unroll
@@ -263,30 +274,28 @@ __device__ void stats_sweep(const Shape& s, const uint16_t* kbase, int kbeg, int
                         z[sl][j] = ok ? acc[j] * s.scale2 : kNegInf;
                         mx[sl] = fmaxf(mx[sl], z[sl][j]);
                     }
+                    grow |= mx[sl] > m[sl] + kSlack;
                 }
-                grow |= mx[sl] > m[sl] + kSlack;
             }
             if (__builtin_amdgcn_ballot_w64(grow) != 0) {
 #pragma unroll
                 for (int sl = 0; sl < NSLOT; ++sl) {
-                    const float mn = fmaxf(m[sl], mx[sl]);
+                    const float bmax = PURE ? fmaxf(fmaxf(z[sl][0], z[sl][1]), fmaxf(z[sl][2], z[sl][3])) * s.scale2
+                                            : mx[sl];
+                    const float mn = fmaxf(m[sl], bmax);
                     if (mn != kNegInf) {
                         const float sc = fast_exp2(m[sl] - mn);
                         tsum[sl] *= sc;
                         vsum[sl] *= sc;
                         m[sl] = mn;
                     }
+                    if (PURE) mx[sl] = pure_terms(z[sl], m[sl]);  // the terms against the new reference
                 }
             }
 #pragma unroll
             for (int sl = 0; sl < NSLOT; ++sl) {
                 if (PURE) {
-                    const float nm = -m[sl];
-                    const float e = (fast_exp2(__builtin_fmaf(z[sl][0], s.scale2, nm)) +
-                                     fast_exp2(__builtin_fmaf(z[sl][1], s.scale2, nm))) +
-                                    (fast_exp2(__builtin_fmaf(z[sl][2], s.scale2, nm)) +
-                                     fast_exp2(__builtin_fmaf(z[sl][3], s.scale2, nm)));
-                    vsum[sl] += e;
+                    vsum[sl] += mx[sl];
                 } else {
                     const float mu = m[sl] == kNegInf ? 0.f : m[sl];  // a row with no visible key yet
 #pragma unroll
