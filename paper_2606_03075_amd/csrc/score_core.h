@@ -266,12 +266,12 @@ __device__ void stats_sweep(const Shape& s, const uint16_t* kbase, int kbeg, int
                     mx[sl] = pure_terms(acc, m[sl]);
                     grow |= !(mx[sl] <= kSlackSum);
                 } else {
+                    // a question row sees every key below vis1 and the question keys up to its own
+                    const int lim = min(kend - 1, vis1 + qrow[sl]);
                     mx[sl] = kNegInf;
 #pragma unroll
                     for (int j = 0; j < 4; ++j) {
-                        const int key = kfirst + j;
-                        const bool ok = (key < kend) & ((key < vis1) | (key - vis1 <= qrow[sl]));
-                        z[sl][j] = ok ? acc[j] * s.scale2 : kNegInf;
+                        z[sl][j] = kfirst + j <= lim ? acc[j] * s.scale2 : kNegInf;
                         mx[sl] = fmaxf(mx[sl], z[sl][j]);
                     }
                     grow |= mx[sl] > m[sl] + kSlack;
