@@ -279,6 +279,21 @@ def ingest_mfma_counters(csv_path, workload):
     print(json.dumps(rec))
 
 
+def mfma_summary(c, launch_ms):
+    """What one scoring kernel's matrix-core counters say at a measured launch time: the
+    issued MFMA rate against the dense bf16 peak and the busy fraction (busy cycles are
+    summed over the SIMDs, GPU-active cycles over the XCDs)."""
+    issued = c["mfma_instrs"] * MFMA_FLOPS / (launch_ms * 1e-3) / 1e12
+    return {
+        "mfma_instrs_per_launch": int(c["mfma_instrs"]),
+        "issued_tflops": round(issued, 1),
+        "issued_frac_of_peak": round(issued / BF16_PEAK_TFLOPS, 4),
+        "mfma_busy_frac": round(c["mfma_busy_cycles"] / (SIMDS / XCDS * c["gpu_active_cycles"]), 4),
+        "valu_instrs_per_mfma": round(c["valu_instrs"] / max(c["mfma_instrs"], 1), 2),
+        "trans_instrs_per_launch": int(c["trans_instrs"]),
+    }
+
+
 def mfma_for(kernel, workload):
     """Committed matrix-core counters of a scoring kernel, if they match the current source."""
     try:
@@ -478,16 +493,7 @@ def main():
         c = mfma_for(kname, ckey) if kname != "score" else None
         ent = {"avg_launch_ms": round(ms, 4), "counters": None}
         if c is not None:
-            issued = c["mfma_instrs"] * MFMA_FLOPS / (ms * 1e-3) / 1e12
-            ent["counters"] = {
-                "mfma_instrs_per_launch": int(c["mfma_instrs"]),
-                "issued_tflops": round(issued, 1),
-                "issued_frac_of_peak": round(issued / BF16_PEAK_TFLOPS, 4),
-                # busy cycles are summed over the SIMDs; active cycles over the XCDs
-                "mfma_busy_frac": round(c["mfma_busy_cycles"] / (SIMDS / XCDS * c["gpu_active_cycles"]), 4),
-                "valu_instrs_per_mfma": round(c["valu_instrs"] / max(c["mfma_instrs"], 1), 2),
-                "trans_instrs_per_launch": int(c["trans_instrs"]),
-            }
+            ent["counters"] = mfma_summary(c, ms)
         per_kernel[kname] = ent
     scoring_mfma = None
     if score_ms > 0:
