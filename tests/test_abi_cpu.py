@@ -34,7 +34,8 @@ def lib():
 
 
 def declared_functions():
-    text = open(os.path.join(ROOT, "include", "tgvkv.h")).read()
+    with open(os.path.join(ROOT, "include", "tgvkv.h")) as f:
+        text = f.read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(tgvkv_[a-z_]+)\s*\(", text)))
 

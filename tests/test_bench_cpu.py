@@ -24,6 +24,11 @@ def _write_csv(path, rows):
             w.writerow(r)
 
 
+def _load(path):
+    with open(path) as f:
+        return json.load(f)
+
+
 def _row(kernel, counter, value, t0=0, t1=1000):
     return {"Kernel_Name": kernel, "Counter_Name": counter, "Counter_Value": value, "Start_Timestamp": t0,
             "End_Timestamp": t1}
@@ -49,7 +54,7 @@ def test_hbm_counters_scale_by_the_copy(tmp_path, monkeypatch):
     _write_csv(cf, [_row("copy", "FETCH_SIZE", bench.COPY_BYTES // 2048), _row("fill", "FETCH_SIZE", 3)])
     _write_csv(cw, [_row("copy", "WRITE_SIZE", bench.COPY_BYTES // 1024)])
     bench.ingest_counters(str(fetch), str(write), str(cf), str(cw), workload="w", decode_steps=7)
-    rec = json.load(open(bench.COUNTERS))["w"]
+    rec = _load(bench.COUNTERS)["w"]
     assert rec["score_text"]["fetch_bytes"] == pytest.approx(1000 * 2048)
     assert rec["score_text"]["write_bytes"] == pytest.approx(10 * 1024)
     assert rec["decode"]["bytes_per_launch"] == pytest.approx(200 * 2048 + 4 * 1024)  # mean over dispatches
@@ -73,7 +78,7 @@ def test_mfma_counters_and_their_reading(tmp_path, monkeypatch):
     path = tmp_path / "p.csv"
     _write_csv(path, rows)
     bench.ingest_mfma_counters(str(path), "w")
-    rec = json.load(open(bench.MFMA_COUNTERS))["w"]["score_vision"]
+    rec = _load(bench.MFMA_COUNTERS)["w"]["score_vision"]
     assert rec["mfma_instrs"] == 1000 and rec["pmc_run_launch_ns"] == 2000
     assert bench.mfma_for("score_vision", "w") == rec
     summ = bench.mfma_summary(rec, launch_ms=0.002)
