@@ -315,6 +315,14 @@ SCORE_SHAPES = {
                                  n_qst=61),
     "four_blocks_gqa_d64": custom_config(batch=1, layers=2, heads_q=8, heads_kv=4, head_dim=64, n_sys=3, n_vis=201,
                                          n_qst=29),
+    # three 16-row blocks per KV head (two slots over two key parts)
+    "three_blocks": custom_config(batch=1, layers=2, heads_q=4, heads_kv=4, head_dim=128, n_sys=11, n_vis=180,
+                                  n_qst=40),
+    # twelve 16-row blocks per KV head (four slots per wave)
+    "twelve_blocks_gqa4": custom_config(batch=1, layers=2, heads_q=8, heads_kv=2, head_dim=128, n_sys=6, n_vis=260,
+                                        n_qst=45),
+    "twelve_blocks_gqa4_d64": custom_config(batch=1, layers=2, heads_q=8, heads_kv=2, head_dim=64, n_sys=2,
+                                            n_vis=190, n_qst=37),
 }
 
 
@@ -372,7 +380,7 @@ def _ramp_inputs(cfg, direction, seed=11):
 
 @pytest.mark.parametrize("fused", [False, True])
 @pytest.mark.parametrize("direction", ["rising", "falling", "zigzag"])
-@pytest.mark.parametrize("shape", ["gqa7_d128", "four_blocks"])
+@pytest.mark.parametrize("shape", ["gqa7_d128", "twelve_blocks_gqa4", "four_blocks"])
 def test_score_moving_max(lib, shape, direction, fused):
     """Logits that climb along the keys: the reference max of every row moves again and again, with
     up to 2^8-sized terms summed between moves; the scores still match the oracle."""
