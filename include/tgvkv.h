@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define TGVKV_ABI_VERSION 5
+#define TGVKV_ABI_VERSION 6
 
 typedef enum tgvkv_status {
     TGVKV_OK = 0,
@@ -133,7 +133,9 @@ enum { TGVKV_CALL_SCORE = 0, TGVKV_CALL_DECODE = 1 };
  * s_vis   f32  [B][L][g][n_vis]      out
  * budgets_or_null  int32 [B][L]: if given, the VISION phase skips every layer
  *                  whose budget leaves no room for vision tokens (budget <=
- *                  |forced U T|); s_vis of skipped layers is left untouched.
+ *                  |forced U T|, or <= |forced| with opts.joint_rank: the
+ *                  vision threshold of tgvkv_sizes); s_vis of skipped layers is
+ *                  left untouched.
  * phases  any non-empty OR of STATS, TEXT, VISION, optionally with FUSED; or
  *         exactly TEXT|VISION|LSE_IN (see TGVKV_SCORE_LSE_IN).
  *         Phases must run in the order STATS, TEXT, VISION, with the same
@@ -337,6 +339,21 @@ tgvkv_status tgvkv_decode_attn_paged(const tgvkv_problem* problem, const tgvkv_o
                                      const int32_t* steps, const void* q, const void* k_new, const void* v_new,
                                      float* out, void* workspace, size_t workspace_bytes,
                                      const int32_t* unit_order_or_null, hipStream_t stream);
+
+/* tgvkv_sizes -- host-only sizes that follow from the problem and options (no HIP call).
+ * With the total_budget given to tgvkv_budget:
+ *   *kept_out              K, the tokens each sequence keeps over its layers: B_tot, or
+ *                          L*(N_t + F_v) + V_tot with vision_only (App. B.3).  One
+ *                          sequence's tgvkv_select output holds g * K positions, and its
+ *                          compacted cache K + L * decode_reserve rows per KV head;
+ *   *vision_threshold_out  a layer's vision scores are needed, and tgvkv_score given
+ *                          budgets computes them, only when its budget exceeds this:
+ *                          |forced U T| (Eq. (10) takes text first), or |forced| with
+ *                          opts.joint_rank.
+ * Either output may be NULL.  TGVKV_E_INVAL for a negative total_budget,
+ * TGVKV_E_CAPACITY above what tgvkv_budget accepts. */
+tgvkv_status tgvkv_sizes(const tgvkv_problem* problem, const tgvkv_opts* opts, int64_t total_budget,
+                         int64_t* kept_out, int32_t* vision_threshold_out);
 
 /* Workspace bytes needed by tgvkv_score (which = TGVKV_CALL_SCORE) or
  * tgvkv_decode_attn / tgvkv_decode_attn_paged (TGVKV_CALL_DECODE); 0 for an invalid problem. */

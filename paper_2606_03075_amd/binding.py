@@ -22,9 +22,10 @@ SCORE_STATS, SCORE_TEXT, SCORE_VISION, SCORE_ALL, SCORE_FUSED = 1, 2, 4, 7, 8
 SCORE_LSE_IN = 16  # lse holds the text rows' normalisers from the caller's prefill: K is read once
 CALL_SCORE, CALL_DECODE = 0, 1
 
+ABI_VERSION = 6  # TGVKV_ABI_VERSION of the library this binding marshals for
 EXPORTS = ("tgvkv_score", "tgvkv_budget", "tgvkv_select", "tgvkv_compact", "tgvkv_decode_attn",
            "tgvkv_page_plan", "tgvkv_page_table", "tgvkv_compact_paged", "tgvkv_decode_attn_paged",
-           "tgvkv_workspace_size", "tgvkv_status_string", "tgvkv_abi_version")
+           "tgvkv_sizes", "tgvkv_workspace_size", "tgvkv_status_string", "tgvkv_abi_version")
 
 
 class TgvkvProblem(ctypes.Structure):
@@ -70,6 +71,7 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.tgvkv_compact_paged.argtypes = [P, O, vp, vp, vp, vp, vp, i64, vp, i32, i32, vp, vp, i64, vp, vp]
     lib.tgvkv_decode_attn_paged.argtypes = [P, O, vp, vp, i64, i32, vp, i32, vp, i32, vp, vp, vp, vp, vp, vp, sz,
                                             vp, vp]
+    lib.tgvkv_sizes.argtypes = [P, O, i64, vp, vp]
     lib.tgvkv_workspace_size.argtypes = [P, O, i32]
     lib.tgvkv_workspace_size.restype = sz
     lib.tgvkv_status_string.argtypes = [ctypes.c_int]
@@ -77,8 +79,11 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.tgvkv_abi_version.argtypes = []
     for name in ("tgvkv_score", "tgvkv_budget", "tgvkv_select", "tgvkv_compact", "tgvkv_decode_attn",
                  "tgvkv_page_plan", "tgvkv_page_table", "tgvkv_compact_paged", "tgvkv_decode_attn_paged",
-                 "tgvkv_abi_version"):
+                 "tgvkv_sizes", "tgvkv_abi_version"):
         getattr(lib, name).restype = ctypes.c_int32
+    if lib.tgvkv_abi_version() != ABI_VERSION:
+        raise RuntimeError(f"{p} has ABI {lib.tgvkv_abi_version()}, this binding needs {ABI_VERSION}; "
+                           "rebuild it with __graft_entry__.build()")
     if path is None:
         _lib = lib
     return lib
@@ -106,37 +111,18 @@ def make_opts(sm_scale: float = 0.0, head_mode: int = 0, n_sink: int = 0, n_rece
                      int(vision_rank), int(bool(joint_rank)))
 
 
-def forced_or_text_count(problem, opts) -> int:
-    """|forced U T|: the text tokens plus the forced positions (first n_sink, last n_recent) that are vision."""
-    p, o = problem, opts
-    N = p.n_sys + p.n_vis + p.n_qst
-    n_sink = o.n_sink if o is not None else 0
-    n_recent = o.n_recent if o is not None else 0
-    fs = min(n_sink, N)
-    fr = max(N - n_recent, fs)
-    v0, v1 = p.n_sys, p.n_sys + p.n_vis
-    fv = max(0, min(fs, v1) - v0) + max(0, v1 - max(fr, v0))
-    return p.n_sys + p.n_qst + fv
-
-
-def forced_count(problem, opts) -> int:
-    """|forced|: the first n_sink and the last n_recent positions."""
-    N = problem.n_sys + problem.n_vis + problem.n_qst
-    n_sink = opts.n_sink if opts is not None else 0
-    n_recent = opts.n_recent if opts is not None else 0
-    fs = min(n_sink, N)
-    fr = max(N - n_recent, fs)
-    return fs + (N - fr)
+def tgvkv_sizes(problem, opts, total_budget: int = 0):
+    """(K, vision threshold) from tgvkv_sizes: the tokens one sequence keeps for a total_budget
+    given to tgvkv_budget, and the budget a layer must exceed to need vision scores."""
+    kept, thr = ctypes.c_int64(0), ctypes.c_int32(0)
+    _check("tgvkv_sizes", load_library().tgvkv_sizes(ctypes.byref(problem), _opts_ref(opts), int(total_budget),
+                                                     ctypes.byref(kept), ctypes.byref(thr)))
+    return kept.value, thr.value
 
 
 def kept_per_sequence(problem, opts, total_budget: int) -> int:
-    """Tokens one sequence keeps for a total_budget given to tgvkv_budget (its idx / cache sizing).
-
-    With vision-only eviction every layer also keeps its text and forced vision positions.
-    """
-    if opts is not None and opts.vision_only:
-        return int(total_budget) + problem.layers * forced_or_text_count(problem, opts)
-    return int(total_budget)
+    """Tokens one sequence keeps for a total_budget given to tgvkv_budget (its idx / cache sizing)."""
+    return tgvkv_sizes(problem, opts, total_budget)[0]
 
 
 def status_string(status: int) -> str:
@@ -378,9 +364,7 @@ class EvictionBuffers:
     def forced_or_text(self) -> int:
         """A layer needs vision scores only when its budget exceeds this: |forced U T| with TPR,
         |forced| when text and vision are ranked jointly."""
-        if self.opts is not None and self.opts.joint_rank:
-            return forced_count(self.problem, self.opts)
-        return forced_or_text_count(self.problem, self.opts)
+        return tgvkv_sizes(self.problem, self.opts, self.total_budget)[1]
 
     def schedule(self) -> str:
         """'two_step': text statistics and text scores, budgets, then vision scores only for the

@@ -383,6 +383,18 @@ tgvkv_status tgvkv_page_plan(const tgvkv_problem* problem, const tgvkv_opts* opt
     return TGVKV_OK;
 }
 
+tgvkv_status tgvkv_sizes(const tgvkv_problem* problem, const tgvkv_opts* opts, int64_t total_budget,
+                         int64_t* kept_out, int32_t* vision_threshold_out) {
+    Shape s;
+    tgvkv_status st = make_shape(problem, opts, &s);
+    if (st != TGVKV_OK) return st;
+    if (total_budget < 0) return TGVKV_E_INVAL;
+    if (total_budget > budget_capacity(s)) return TGVKV_E_CAPACITY;
+    if (kept_out != nullptr) *kept_out = kept_per_sequence(s, total_budget);
+    if (vision_threshold_out != nullptr) *vision_threshold_out = vision_threshold(s);
+    return TGVKV_OK;
+}
+
 tgvkv_status tgvkv_page_table(const tgvkv_problem* problem, const tgvkv_opts* opts, const int32_t* budgets,
                               int64_t total_budget, int32_t decode_reserve, int32_t page_size,
                               const int32_t* free_pages, int64_t n_free, int32_t* block_table, int32_t max_pages,

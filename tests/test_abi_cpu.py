@@ -45,7 +45,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(bd.EXPORTS) <= set(names) and len(names) == len(bd.EXPORTS), names
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.tgvkv_abi_version() == 5
+    assert lib.tgvkv_abi_version() == bd.ABI_VERSION == 6
     for st in (0, -1, -2, -3, -4, -5):
         assert lib.tgvkv_status_string(st)
     assert lib.tgvkv_status_string(7) == b"unknown status"
@@ -218,6 +218,46 @@ def test_paged_validation_before_any_launch(lib):
                                        fake, big, None, s) == -1
     assert lib.tgvkv_decode_attn_paged(ok, None, fake, fake, 64, 8, fake, 0, fake, 4, fake, fake, fake, fake, fake,
                                        fake, big, None, s) == -1
+
+
+@pytest.mark.parametrize("shape", [(3, 40, 5), (0, 30, 4), (6, 0, 9), (2, 7, 0)])
+@pytest.mark.parametrize("forced", [(0, 0), (4, 1), (50, 50)])
+def test_sizes_follow_the_oracle(lib, shape, forced):
+    """K and the vision threshold from tgvkv_sizes against the oracle's budgets and forced positions."""
+    import numpy as np
+    import oracle.tgvkv_oracle as O
+    ns, nv, nq = shape
+    L, N, nt = 3, ns + nv + nq, ns + nq
+    prob = P(layers=L, n_sys=ns, n_vis=nv, n_qst=nq)
+    n_forced = len(O.forced_positions(N, *forced))
+    nfv = O.forced_vision_count(ns, nv, nq, *forced)
+    masses = np.array([0.2, 0.5, 0.3])
+    for total in sorted({0, 1, L * N // 4, L * N}):
+        o = bd.make_opts(n_sink=forced[0], n_recent=forced[1])
+        assert bd.tgvkv_sizes(prob, o, total) == (total, nt + nfv)
+        o = bd.make_opts(n_sink=forced[0], n_recent=forced[1], joint_rank=True)
+        assert bd.tgvkv_sizes(prob, o, total) == (total, n_forced)
+    vo = bd.make_opts(n_sink=forced[0], n_recent=forced[1], vision_only=True)
+    cap = L * (nv - nfv)
+    for vtot in sorted({v for v in (0, 1, cap) if v <= cap}):
+        kept = int(O.vision_only_budgets(masses, vtot, nt, nv, nfv).sum())
+        assert bd.tgvkv_sizes(prob, vo, vtot) == (kept, nt + nfv)
+    with pytest.raises(bd.TgvkvError):
+        bd.tgvkv_sizes(prob, vo, cap + 1)
+
+
+def test_sizes_reject_bad_arguments(lib):
+    kept, thr = ctypes.c_int64(-7), ctypes.c_int32(-7)
+    ok = ctypes.byref(P())  # L = 2, N = 48
+    assert lib.tgvkv_sizes(ok, None, -1, ctypes.byref(kept), ctypes.byref(thr)) == -1
+    assert lib.tgvkv_sizes(ok, None, 2 * 48 + 1, ctypes.byref(kept), ctypes.byref(thr)) == -4
+    assert lib.tgvkv_sizes(ctypes.byref(P(heads_q=3)), None, 0, ctypes.byref(kept), ctypes.byref(thr)) == -1
+    assert lib.tgvkv_sizes(None, None, 0, ctypes.byref(kept), ctypes.byref(thr)) == -1
+    assert (kept.value, thr.value) == (-7, -7)
+    assert lib.tgvkv_sizes(ok, None, 10, None, None) == 0
+    assert lib.tgvkv_sizes(ok, None, 10, ctypes.byref(kept), None) == 0 and kept.value == 10
+    with pytest.raises(bd.TgvkvError):
+        bd.tgvkv_sizes(P(), None, -1)
 
 
 def test_empty_batch_is_a_no_op(lib):
