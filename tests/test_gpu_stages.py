@@ -121,7 +121,9 @@ def test_budget_kernel_vision_only_exact(lib, L, ns, nv, nq, n_sink, n_recent):
 # ----------------------------------------------------------------------------- selection
 @pytest.mark.parametrize("rank", ["tpr", "joint_twr", "joint_sum"])
 @pytest.mark.parametrize("head_mode", [0, 1])
-@pytest.mark.parametrize("shape", [(3, 40, 5), (0, 30, 4), (8, 144, 16), (35, 576, 40), (2, 0, 9), (16, 1300, 48)])
+# the last shape is longer than the kernel's LDS key buffer (12288 keys): keys are re-read from memory
+@pytest.mark.parametrize("shape", [(3, 40, 5), (0, 30, 4), (8, 144, 16), (35, 576, 40), (2, 0, 9), (16, 1300, 48),
+                                   (16, 13000, 48)])
 @pytest.mark.parametrize("forced", [(0, 0), (4, 1)])
 def test_select_kernel_exact(lib, head_mode, shape, forced, rank):
     torch = _torch()
