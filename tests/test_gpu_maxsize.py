@@ -102,3 +102,20 @@ def test_max_sequence(lib):
     for st in range(steps):
         err = np.abs(outs[st][0, 0] - ref[st]).max()
         assert err <= DECODE_ATOL, (st, err)
+
+
+@pytest.mark.parametrize("shape", [
+    # one query head, 16384 text rows (8000 system + 8384 question), 100 vision tokens
+    dict(heads_q=1, heads_kv=1, head_dim=64, n_sys=8000, n_vis=100, n_qst=8384),
+    # 16 query heads per KV head, 1024 text rows each
+    dict(heads_q=16, heads_kv=1, head_dim=128, n_sys=24, n_vis=500, n_qst=1000),
+])
+def test_max_text_rows(lib, shape):
+    """16384 text rows per KV head (query heads x text tokens), the library's limit: the
+    row normalisers of a KV head's text rows fill the text pass's LDS buffer."""
+    from tests.test_gpu_e2e import run_and_check
+    cfg = custom_config(name="maxtext", batch=1, layers=2, **shape)
+    assert cfg.heads_q // cfg.heads_kv * cfg.n_text == 16384
+    # a budget inside the text (top text tokens), then one that reaches into the vision tokens
+    for rho in (0.3, 0.998):
+        run_and_check(cfg, rho, steps=2, seed=5)
