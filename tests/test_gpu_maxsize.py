@@ -119,3 +119,12 @@ def test_max_text_rows(lib, shape):
     # a budget inside the text (top text tokens), then one that reaches into the vision tokens
     for rho in (0.3, 0.998):
         run_and_check(cfg, rho, steps=2, seed=5)
+
+
+def test_max_layers(lib):
+    """512 layers (the library's limit) end to end: budgets shared over every layer, decode's
+    longest-first dispatch over 1024 (sequence, layer) segments."""
+    from tests.test_gpu_e2e import run_and_check
+    cfg = custom_config(name="maxlayers", batch=2, layers=512, heads_q=2, heads_kv=1, head_dim=64, n_sys=3,
+                        n_vis=30, n_qst=4)
+    run_and_check(cfg, 0.2, steps=2, seed=9)

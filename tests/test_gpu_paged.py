@@ -167,6 +167,17 @@ def test_paged_llava15(lib):
     _paged_matches_contiguous(cfg, 0.05, 16, steps=8, seed=0)
 
 
+def test_paged_table_width_limit(lib):
+    """A segment of 4096 one-row pages, the widest table the library takes (its page ids are
+    staged in LDS): every token kept (N = 4094) plus 2 decode steps."""
+    import torch
+    cfg = custom_config(name="wide", batch=1, layers=1, heads_q=2, heads_kv=1, head_dim=64, n_sys=10, n_vis=4070,
+                        n_qst=14)
+    width, _ = bd.page_plan(bd.problem_from(cfg), None, cfg.n_tokens, 2, 1)
+    assert width == 4096
+    _paged_matches_contiguous(cfg, 1.0, 1, steps=2, seed=6)
+
+
 # ----------------------------------------------------------------------------- continuous batching
 def _oracle_cache(t, cfg, tot, b, gpu_idx, io, budgets, L):
     """Per layer: oracle retained rows (K, V per KV head) where the GPU's set matches the oracle's."""
