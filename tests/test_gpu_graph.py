@@ -65,3 +65,37 @@ def test_decode_graph_replays(lib, heads_q, heads_kv):
     buf.decode(T - 1, dq[T - 1], dk[T - 1], dv[T - 1])
     torch.cuda.synchronize()
     assert torch.equal(buf.out, eager[T - 1])
+
+
+@pytest.mark.parametrize("schedule", ["two_step", "fused"])
+def test_eviction_graph_replays(lib, schedule):
+    """The whole eviction pass (scores, budgets, vision scores where needed, selection,
+    compaction) captured once and replayed: every output equals the eager pass bit for bit."""
+    import torch
+    cfg = custom_config(name="graphev", batch=2, layers=4, heads_q=8, heads_kv=2, head_dim=128, n_sys=6,
+                        n_vis=300, n_qst=21)
+    log(f"graph eviction {schedule}")
+    t = make_prefill_tensors(cfg, seed=8)
+    q, k, v = (dev_bf16(t[n]) for n in ("q_text", "k", "v"))
+    buf = bd.EvictionBuffers(bd.problem_from(cfg), None, total_budget(0.1, cfg.n_tokens, cfg.layers), 2)
+    names = ("lse", "s_txt", "w_txt", "tv_mass", "s_vis", "budgets", "idx_offsets", "seg_offsets", "unit_order",
+             "idx", "kc", "vc")
+    # the decode-reserve slots of the cache are not written by the pass: zero them on both sides
+    buf.kc.zero_()
+    buf.vc.zero_()
+    buf.evict(q, k, v, schedule=schedule)
+    torch.cuda.synchronize()
+    eager = {n: getattr(buf, n).clone() for n in names}
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        buf.evict(q, k, v, schedule=schedule)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for n in ("s_vis", "idx", "kc", "vc"):
+            getattr(buf, n).zero_()
+        buf.score(q, k, bd.SCORE_STATS)  # eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for n in names:
+            assert torch.equal(getattr(buf, n), eager[n]), f"replay {rep}: {n}"
