@@ -259,8 +259,13 @@ __device__ void stats_sweep(const Shape& s, const uint16_t* kbase, int kbeg, int
 #pragma unroll
             for (int sl = 0; sl < NSLOT; ++sl) {
                 f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+                // With 6 slots (2 waves per SIMD) a wave issuing its MFMAs goes first, the other
+                // wave's softmax fills in: 763-780 against 819-821 us per launch at the
+                // Qwen2-VL shape; at 4 slots it changed nothing, and the vision sweep lost.
+                if (NSLOT >= 6 && KS == 1) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
                 for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(kf[ks], qf[sl][ks], acc);
+                if (NSLOT >= 6 && KS == 1) __builtin_amdgcn_s_setprio(0);
                 if (PURE) {
                     z[sl] = acc;  // logits in MFMA units; scaled inside the exponent
                     mx[sl] = pure_terms(acc, m[sl]);
