@@ -39,6 +39,15 @@ def _positions(n_sys, n_vis, n_qst):
     return list(range(n_sys)) + [n_sys + n_vis + i for i in range(n_qst)]
 
 
+def _first_and_last(n, n_first, n_last):
+    """App. A.2 spelled out by hand: positions 0..n_first-1 and n-n_last..n-1, clipped to [0, n)."""
+    out = set()
+    for p in range(n):
+        if p < n_first or p >= n - n_last:
+            out.add(p)
+    return out
+
+
 # ----------------------------------------------------------------------------- softmax rows
 def check_softmax_rows(O, seed=0):
     """Rows of Eq. (2) restricted to text queries: sums, causal zeros, library softmax."""
@@ -297,7 +306,7 @@ def check_tpr(O, seed=6):
         sv = rng.integers(0, 4, size=nv).astype(float) / 4
         st = rng.integers(0, 4, size=n_text).astype(float) / 4
         n_sink, n_recent = (0, 0) if rng.random() < 0.5 else (int(rng.integers(0, 5)), int(rng.integers(0, 3)))
-        forced = set(O.forced_positions(N, n_sink, n_recent).tolist())
+        forced = _first_and_last(N, n_sink, n_recent)
         for b in range(0, N + 1):
             I = O.tpr_select(sv, st, b, ns, nv, nq, n_sink, n_recent)
             I = list(I)
@@ -457,7 +466,7 @@ def check_variants(O, seed=9):
         b = int(rng.integers(0, n + 1))
         keep = O.joint_select(sv, st, b, ns, nv, nq, fs, fr, scale)
         assert len(keep) == b and np.all(np.diff(keep) > 0)
-        forced = set(O.forced_positions(n, fs, fr).tolist())
+        forced = _first_and_last(n, fs, fr)
         score = {}
         for i, p_ in enumerate(_positions(ns, nv, nq)):
             score[p_] = st[i]
@@ -474,6 +483,89 @@ def check_variants(O, seed=9):
     assert list(O.tpr_select([5.0, 0.0], [1.0, 1.0], 1, 1, 2, 1)) == [0]
 
 
+# ----------------------------------------------------------------------------- forced tokens
+def _vision_blind_layer(rng, H, H_kv, d, ns, nv, nq, blind):
+    """One layer's q/k whose question rows put exactly zero float64 mass on vision keys if blind.
+
+    Every key is +-c u for one unit direction u and every question query is +c u, so a
+    question row's logits are +c^2/sqrt(d) on text keys and -c^2/sqrt(d) on vision keys.
+    With c^2/sqrt(d) = 400 the vision probabilities are exp(-800) relative to the text ones,
+    which is 0 in float64.  System rows never see vision keys (causal mask).  A layer that is
+    not blind gets random keys, so its mass is positive.
+    """
+    N, n_text = ns + nv + nq, ns + nq
+    u = np.zeros(d)
+    u[0] = 1.0
+    c = math.sqrt(400.0 * math.sqrt(d))
+    if not blind:
+        return rng.standard_normal((H, n_text, d)), rng.standard_normal((H_kv, N, d))
+    k = np.tile(c * u, (H_kv, N, 1))
+    k[:, ns:ns + nv] = -c * u
+    q = np.tile(c * u, (H, n_text, 1))
+    return q, k
+
+
+def check_forced(O, seed=10):
+    """App. A.2 keeps the first 4 and the last 1 tokens: closed forms, and the per-layer floor of TVB.
+
+    The floor: with forced tokens every layer first gets F = min(|forced|, B_tot // L, N) of
+    the budget and the rest R = B_tot - L*F is shared by mass, so masses (m, 0, 0, 0) give
+    budgets (F + R, F, F, F) and the three zero-mass layers keep exactly the forced positions.
+    """
+    # closed forms of the forced set
+    assert list(O.forced_positions(10, 4, 1)) == [0, 1, 2, 3, 9]
+    assert list(O.forced_positions(10, 4, 0)) == [0, 1, 2, 3]
+    assert list(O.forced_positions(10, 0, 1)) == [9]
+    assert list(O.forced_positions(10, 0, 3)) == [7, 8, 9]
+    assert list(O.forced_positions(10, 0, 0)) == []
+    assert list(O.forced_positions(5, 4, 1)) == [0, 1, 2, 3, 4]       # n_sink + n_recent == N
+    assert list(O.forced_positions(4, 4, 1)) == [0, 1, 2, 3]          # overlap: the last token is a sink
+    assert list(O.forced_positions(3, 4, 2)) == [0, 1, 2]             # both larger than N
+    assert list(O.forced_positions(1, 0, 1)) == [0]
+    assert list(O.forced_positions(0, 4, 1)) == []
+    for n in range(0, 12):
+        for a in range(0, 6):
+            for r in range(0, 4):
+                f = O.forced_positions(n, a, r)
+                assert set(f.tolist()) == _first_and_last(n, a, r) and list(f) == sorted(f), (n, a, r)
+    # the forced set is what a budget of |forced| keeps, whatever the scores
+    ns, nv, nq = 3, 12, 5
+    st = np.linspace(1.0, 0.0, ns + nq)
+    sv = np.linspace(0.0, 1.0, nv)
+    assert list(O.tpr_select(sv, st, 5, ns, nv, nq, 4, 1)) == [0, 1, 2, 3, ns + nv + nq - 1]
+    assert list(O.joint_select(sv, st, 5, ns, nv, nq, 4, 1)) == [0, 1, 2, 3, ns + nv + nq - 1]
+    # whole sequence: layer 0 sees vision, layers 1..3 put zero mass on it
+    rng = np.random.default_rng(seed)
+    H, H_kv, d, L = 4, 2, 16, 4
+    N = ns + nv + nq
+    q, k = [], []
+    for l in range(L):
+        ql, kl = _vision_blind_layer(rng, H, H_kv, d, ns, nv, nq, blind=l > 0)
+        q.append(ql)
+        k.append(kl)
+    for tot in (24, 30, 35):
+        scores, b, idx = O.evict_sequence(q, k, ns, nv, nq, tot, n_sink=4, n_recent=1)
+        assert scores[0]["tv_mass"] > 0.0
+        for l in range(1, L):
+            assert scores[l]["tv_mass"] == 0.0
+        F = min(5, tot // L, N)
+        assert list(b) == [F + tot - L * F, F, F, F], (tot, list(b))
+        for l in range(1, L):
+            assert list(idx[l][0]) == [0, 1, 2, 3, N - 1]
+        assert {0, 1, 2, 3, N - 1} <= set(idx[0][0].tolist())
+    # past the cap N the dominant layer stops at N and the rest is shared evenly, lower layers first
+    scores, b, idx = O.evict_sequence(q, k, ns, nv, nq, 37, n_sink=4, n_recent=1)
+    assert list(b) == [N, 5 + 1, 5 + 1, 5]
+    # a budget below L*|forced| floors at B_tot // L and keeps the first forced positions
+    scores, b, idx = O.evict_sequence(q, k, ns, nv, nq, 13, n_sink=4, n_recent=1)
+    assert list(b) == [3 + 1, 3, 3, 3]
+    for l in range(1, L):
+        assert list(idx[l][0]) == [0, 1, 2]
+    # without forced tokens the same masses give everything to layer 0
+    scores, b, idx = O.evict_sequence(q, k, ns, nv, nq, 18, n_sink=0, n_recent=0)
+    assert list(b) == [18, 0, 0, 0]
+
+
 ALL_CHECKS = [
     check_softmax_rows,
     check_mass_split,
@@ -486,4 +578,5 @@ ALL_CHECKS = [
     check_compact_and_decode,
     check_vision_only,
     check_variants,
+    check_forced,
 ]

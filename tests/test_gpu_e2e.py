@@ -223,7 +223,7 @@ def test_vision_only_small(lib, head_mode, forced):
     cfg = custom_config(batch=2, layers=4, heads_q=8, heads_kv=4, head_dim=128, n_sys=6, n_vis=230, n_qst=21)
     for rho in (0.0, 0.05, 0.3, 1.0):
         run_and_check(cfg, rho, head_mode, forced, steps=3, seed=5, vision_only=True)
-    # no system text: the sink is a vision token and becomes each layer's floor
+    # no system text: the forced sink is a vision token, kept beside the vision budget like the text
     cfg = custom_config(name="nos", batch=1, layers=3, heads_q=4, heads_kv=4, head_dim=64, n_sys=0, n_vis=90,
                         n_qst=17)
     run_and_check(cfg, 0.1, head_mode, forced, steps=2, seed=6, vision_only=True)

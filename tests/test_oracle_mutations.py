@@ -15,7 +15,7 @@ from tests import oracle_pins as pins
 _orig = {name: getattr(O, name) for name in
          ("text_row_softmax", "text_scores", "text_weights", "vision_scores", "tv_mass",
           "head_average", "layer_budgets", "tpr_select", "decode_attention", "vision_only_budgets",
-          "budget_masses", "score_slice", "joint_select")}
+          "budget_masses", "score_slice", "joint_select", "forced_positions", "evict_sequence")}
 
 
 def _softmax_mask_off_by_one(q_text, k, n_sys, n_vis, n_qst, sm_scale):
@@ -165,6 +165,30 @@ def _joint_without_scale(s_vis, s_txt, budget, n_sys, n_vis, n_qst, n_sink=0, n_
     return _orig["joint_select"](s_vis, s_txt, budget, n_sys, n_vis, n_qst, n_sink, n_recent, 1.0)
 
 
+def _forced_drops_recent(n_tokens, n_sink, n_recent):
+    # forgets the last n_recent tokens of App. A.2
+    return _orig["forced_positions"](n_tokens, n_sink, 0)
+
+
+def _forced_one_recent_too_many(n_tokens, n_sink, n_recent):
+    # keeps n_recent + 1 trailing tokens
+    return _orig["forced_positions"](n_tokens, n_sink, n_recent + 1 if n_recent > 0 else 0)
+
+
+def _evict_sequence_no_floor(*args, **kwargs):
+    # hands TVB no per-layer floor for the forced tokens
+    real = O.layer_budgets
+
+    def no_floor(masses, total_budget, n_tokens, n_floor=0, return_detail=False):
+        return real(masses, total_budget, n_tokens, 0, return_detail)
+
+    O.layer_budgets = no_floor
+    try:
+        return _orig["evict_sequence"](*args, **kwargs)
+    finally:
+        O.layer_budgets = real
+
+
 MUTANTS = {
     "softmax_mask_off_by_one": ("text_row_softmax", _softmax_mask_off_by_one),
     "softmax_wrong_kv_head": ("text_row_softmax", _softmax_wrong_kv_head),
@@ -189,6 +213,9 @@ MUTANTS = {
     "attention_sum_still_weighted": ("score_slice", _attention_sum_still_weighted),
     "joint_ties_to_higher_position": ("joint_select", _joint_ties_to_higher_position),
     "joint_without_scale": ("joint_select", _joint_without_scale),
+    "forced_drops_recent": ("forced_positions", _forced_drops_recent),
+    "forced_one_recent_too_many": ("forced_positions", _forced_one_recent_too_many),
+    "evict_sequence_no_floor": ("evict_sequence", _evict_sequence_no_floor),
 }
 
 
