@@ -75,11 +75,9 @@ def parse():
                     help="turn a rocprofv3 --pmc run of this bench with SQ_INSTS_MFMA SQ_VALU_MFMA_BUSY_CYCLES "
                          "GRBM_GUI_ACTIVE SQ_INSTS_VALU SQ_INSTS_VALU_TRANS_F32 into profiles/mfma_counters.json "
                          "(matrix-core work per launch of each scoring kernel)")
-    ap.add_argument("--schedule", default="auto", choices=("auto", "two_step", "phases", "fused", "fused_text",
-                                                           "lse_in"),
+    ap.add_argument("--schedule", default="auto", choices=("auto", "two_step", "phases", "lse_in"),
                     help="scoring schedule: vision scores after the budgets only for layers that need them "
-                         "(auto, two_step), one launch per phase for every layer (phases), or the persistent "
-                         "fused kernel (fused, fused_text)")
+                         "(auto, two_step), or one launch per phase for every layer (phases)")
     return ap.parse_args()
 
 
@@ -480,7 +478,7 @@ def main():
     H, Hkv, D, Nq, Nv = cfg.heads_q, cfg.heads_kv, cfg.head_dim, cfg.n_qst, cfg.n_vis
     budgets = buf.budgets.cpu().numpy()
     thr = buf.forced_or_text()
-    vis_layers = int((budgets > thr).sum()) if sched in ("two_step", "fused_text") else B * L
+    vis_layers = int((budgets > thr).sum()) if sched == "two_step" else B * L
     kept = buf.kept  # tokens each sequence keeps
     k_bytes = B * L * Hkv * N * D * 2
     q_bytes = B * L * H * cfg.n_text * D * 2

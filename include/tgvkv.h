@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define TGVKV_ABI_VERSION 6
+#define TGVKV_ABI_VERSION 7
 
 typedef enum tgvkv_status {
     TGVKV_OK = 0,
@@ -99,8 +99,6 @@ enum {
     TGVKV_SCORE_TEXT   = 2,  /* text scores s^T, weights w~, per-layer text->vision mass      */
     TGVKV_SCORE_VISION = 4,  /* text-weighted vision scores s^V                               */
     TGVKV_SCORE_ALL    = 7,
-    TGVKV_SCORE_FUSED  = 8,  /* with ALL or STATS|TEXT: one persistent launch instead of one
-                                per phase (needs budgets_or_null == NULL)                     */
     TGVKV_SCORE_LSE_IN = 16  /* with exactly TEXT|VISION: lse is an input holding every text
                                 row's normaliser, as a prefill attention kernel returns it;
                                 the statistics sweep is skipped, the vision sweep also gives
@@ -136,16 +134,12 @@ enum { TGVKV_CALL_SCORE = 0, TGVKV_CALL_DECODE = 1 };
  *                  |forced U T|, or <= |forced| with opts.joint_rank: the
  *                  vision threshold of tgvkv_sizes); s_vis of skipped layers is
  *                  left untouched.
- * phases  any non-empty OR of STATS, TEXT, VISION, optionally with FUSED; or
- *         exactly TEXT|VISION|LSE_IN (see TGVKV_SCORE_LSE_IN).
+ * phases  any non-empty OR of STATS, TEXT, VISION; or exactly TEXT|VISION|LSE_IN
+ *         (see TGVKV_SCORE_LSE_IN).
  *         Phases must run in the order STATS, TEXT, VISION, with the same
  *         workspace and outputs; a later phase reads what the earlier ones left
  *         there.  Pointers of phases not requested may be NULL (lse is needed by
- *         all three, w_txt by VISION).  FUSED (with ALL or STATS|TEXT, no budgets)
- *         runs the phases as one persistent kernel whose workgroups take key
- *         splits in ticket order; it is bit-for-bit a different summation order
- *         of the same quantities and is slower on gfx950 than the per-phase
- *         kernels, so it is never chosen implicitly.
+ *         all three, w_txt by VISION).
  * workspace / workspace_bytes  >= tgvkv_workspace_size(p, o, TGVKV_CALL_SCORE).
  */
 tgvkv_status tgvkv_score(const tgvkv_problem* problem, const tgvkv_opts* opts, int32_t phases,

@@ -18,11 +18,11 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libtgvkv.so")
 
 TGVKV_OK, TGVKV_E_INVAL, TGVKV_E_UNSUPPORTED, TGVKV_E_WORKSPACE, TGVKV_E_CAPACITY, TGVKV_E_HIP = 0, -1, -2, -3, -4, -5
-SCORE_STATS, SCORE_TEXT, SCORE_VISION, SCORE_ALL, SCORE_FUSED = 1, 2, 4, 7, 8
+SCORE_STATS, SCORE_TEXT, SCORE_VISION, SCORE_ALL = 1, 2, 4, 7
 SCORE_LSE_IN = 16  # lse holds the text rows' normalisers from the caller's prefill: K is read once
 CALL_SCORE, CALL_DECODE = 0, 1
 
-ABI_VERSION = 6  # TGVKV_ABI_VERSION of the library this binding marshals for
+ABI_VERSION = 7  # TGVKV_ABI_VERSION of the library this binding marshals for
 EXPORTS = ("tgvkv_score", "tgvkv_budget", "tgvkv_select", "tgvkv_compact", "tgvkv_decode_attn",
            "tgvkv_page_plan", "tgvkv_page_table", "tgvkv_compact_paged", "tgvkv_decode_attn_paged",
            "tgvkv_sizes", "tgvkv_workspace_size", "tgvkv_status_string", "tgvkv_abi_version")
@@ -375,27 +375,14 @@ class EvictionBuffers:
         """Score, budget, select and (unless compact=False, e.g. for a paged cache) compact.
 
         schedule: 'auto' (= 'two_step'), 'two_step', 'phases' (every scoring phase as its own
-        launch, vision scores for every layer), 'fused' (one persistent scoring launch),
-        'fused_text' (persistent text pass, then vision scores where needed) or 'lse_in' (self.lse
+        launch, vision scores for every layer) or 'lse_in' (self.lse
         already holds every text row's normaliser from the caller's prefill: text and vision
         scores and the TV mass in one K pass, then the budgets).  marks(name) is called after
         each stage (for event timing).
         """
         mark = marks if marks is not None else (lambda name: None)
         sched = self.schedule() if schedule == "auto" else schedule
-        if sched == "fused":
-            self.score(q_text, k, SCORE_ALL | SCORE_FUSED, stream=stream)
-            mark("score")
-            self.budget(stream)
-            mark("budget")
-        elif sched == "fused_text":
-            self.score(q_text, k, SCORE_STATS | SCORE_TEXT | SCORE_FUSED, stream=stream)
-            mark("score_text")
-            self.budget(stream)
-            mark("budget")
-            self.score(q_text, k, SCORE_VISION, budgets=self.budgets, stream=stream)
-            mark("score_vision")
-        elif sched == "two_step":
+        if sched == "two_step":
             self.score(q_text, k, SCORE_STATS | SCORE_TEXT, stream=stream)
             mark("score_text")
             self.budget(stream)

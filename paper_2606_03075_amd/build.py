@@ -18,7 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build", "tgvkv")
 LIB = os.path.join(PKG, "libtgvkv.so")
 
-HIP_SOURCES = ["score.hip", "score_fused.hip", "budget.hip", "select.hip", "compact.hip", "decode.hip", "pages.hip"]
+HIP_SOURCES = ["score.hip", "budget.hip", "select.hip", "compact.hip", "decode.hip", "pages.hip"]
 CXX_SOURCES = ["api.cpp"]
 ARCH = "gfx950"
 
@@ -35,7 +35,7 @@ def common_flags():
 
 
 # Sources whose kernels run with the IEEE mode bit off (see device_flags).
-NO_IEEE_SOURCES = ("score.hip", "score_fused.hip")
+NO_IEEE_SOURCES = ("score.hip",)
 
 
 def device_flags(src=None):

@@ -117,8 +117,6 @@ struct ScoreWs {
     float* colsum;
     float* vmh;
     float* part;
-    float* part_stats;  // fused path: per-split row statistics
-    int* sync;          // fused path: ticket, error word and completion counters
     size_t bytes;
 };
 
@@ -135,16 +133,6 @@ ScoreWs score_workspace(const Shape& s, const RowPlan& rp, void* base) {
     off = align_up(off + sizeof(float) * bl * s.H);
     w.part = reinterpret_cast<float*>(b ? b + off : nullptr);
     off = align_up(off + sizeof(float) * bl * s.Hkv * (size_t)std::max(rp.rowgroups, 1) * s.Nv);
-    w.part_stats = nullptr;
-    w.sync = nullptr;
-    if (tgvkv::fused_eligible(s, rp)) {
-        const tgvkv::FusedPlan fp = tgvkv::plan_fused(s, true);
-        const size_t rows = (size_t)s.G * ((s.Nq + 15) / 16) * 16;
-        w.part_stats = reinterpret_cast<float*>(b ? b + off : nullptr);
-        off = align_up(off + sizeof(float) * bl * s.Hkv * (size_t)fp.sa * rows * 3);
-        w.sync = reinterpret_cast<int*>(b ? b + off : nullptr);
-        off = align_up(off + sizeof(int) * (size_t)tgvkv::fused_sync_words(s));
-    }
     w.bytes = off;
     return w;
 }
@@ -219,13 +207,9 @@ tgvkv_status tgvkv_score(const tgvkv_problem* problem, const tgvkv_opts* opts, i
     Shape s;
     tgvkv_status st = make_shape(problem, opts, &s);
     if (st != TGVKV_OK) return st;
-    const bool want_fused = (phases & TGVKV_SCORE_FUSED) != 0;
     const bool lse_in = (phases & TGVKV_SCORE_LSE_IN) != 0;
-    phases &= ~(TGVKV_SCORE_FUSED | TGVKV_SCORE_LSE_IN);
+    phases &= ~TGVKV_SCORE_LSE_IN;
     if (phases < 1 || phases > TGVKV_SCORE_ALL) return TGVKV_E_INVAL;
-    if (want_fused && (lse_in || budgets_or_null != nullptr ||
-                       (phases != TGVKV_SCORE_ALL && phases != (TGVKV_SCORE_STATS | TGVKV_SCORE_TEXT))))
-        return TGVKV_E_INVAL;
     // given normalisers: text and vision scores and the TV mass in one pass, for every layer
     if (lse_in && (phases != (TGVKV_SCORE_TEXT | TGVKV_SCORE_VISION) || budgets_or_null != nullptr))
         return TGVKV_E_INVAL;
@@ -247,14 +231,6 @@ tgvkv_status tgvkv_score(const tgvkv_problem* problem, const tgvkv_opts* opts, i
     const uint16_t* q = static_cast<const uint16_t*>(q_text);
     const uint16_t* kk = static_cast<const uint16_t*>(k);
     const int32_t vthr = vision_threshold(s);
-
-    // One persistent kernel when asked for and the shape allows it (one row group per unit).
-    if (want_fused && w.sync != nullptr) {
-        tgvkv::FusedPlan fp = tgvkv::plan_fused(s, (phases & TGVKV_SCORE_VISION) != 0);
-        if (const char* lag = std::getenv("TGVKV_FUSED_LAG")) fp.lag = std::max(0, std::atoi(lag));
-        tgvkv::FusedPtrs fptr{q, kk, lse, s_txt, w_txt, tv_mass, s_vis, w.part_stats, w.colsum, w.vmh, w.part, w.sync};
-        return hip_status(tgvkv::launch_score_fused(s, rp, fp, fptr, stream));
-    }
 
     hipError_t e = hipSuccess;
     if (lse_in) {

@@ -24,8 +24,7 @@
 //                 is read once.
 //
 // These kernels serve phase-by-phase calls (and the vision pass restricted to
-// layers whose budget reaches past the text); score_fused.hip runs the same
-// building blocks as one persistent kernel.
+// layers whose budget reaches past the text).
 #include <algorithm>
 
 #include "score_core.h"

@@ -1,6 +1,4 @@
-// Device building blocks of the TWR / TVB scoring passes, shared by the
-// phase-by-phase kernels (score.hip) and the fused persistent kernel
-// (score_fused.hip).
+// Device building blocks of the TWR / TVB scoring passes (kernels in score.hip).
 //
 // A "unit" is one (sequence b, layer l, KV head) slice: bl = b * L + l.  Its
 // question rows (query heads sharing the KV head x question tokens) are cut into

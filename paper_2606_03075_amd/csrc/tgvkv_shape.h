@@ -27,30 +27,6 @@ struct RowPlan {
 
 RowPlan plan_question_rows(const Shape& s);
 
-// Persistent fused scoring: items are key splits of (sequence, layer, KV head)
-// units; A items sweep all keys for statistics, B items sweep vision keys.
-struct FusedPlan {
-    int sa, sb;        // statistics / vision splits per unit
-    int cs, cv;        // keys per statistics split, vision keys per vision split
-    int lag;           // layers by which a layer's A items precede its B items (0: pick at launch)
-    int nA, nB, nbl;   // items per layer, (sequence, layer) count
-    long long total;   // tickets
-};
-
-struct FusedPtrs {
-    const uint16_t* q_text;
-    const uint16_t* k;
-    float *lse, *s_txt, *w_txt, *tv_mass, *s_vis;
-    float *part_stats, *ws_colsum, *ws_vmh, *ws_part;
-    int* sync;
-};
-
-long long fused_sync_words(const Shape& s);
-bool fused_eligible(const Shape& s, const RowPlan& rp);
-FusedPlan plan_fused(const Shape& s, bool with_vision);
-hipError_t launch_score_fused(const Shape& s, const RowPlan& rp, const FusedPlan& fp, const FusedPtrs& p,
-                              hipStream_t st);
-
 // Score phases.
 hipError_t launch_score_stats(const Shape& s, const RowPlan& rp, const uint16_t* q_text,
                               const uint16_t* k, float* lse, float* ws_vm, hipStream_t st);

@@ -45,7 +45,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(bd.EXPORTS) <= set(names) and len(names) == len(bd.EXPORTS), names
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.tgvkv_abi_version() == bd.ABI_VERSION == 6
+    assert lib.tgvkv_abi_version() == bd.ABI_VERSION == 7
     for st in (0, -1, -2, -3, -4, -5):
         assert lib.tgvkv_status_string(st)
     assert lib.tgvkv_status_string(7) == b"unknown status"
@@ -94,7 +94,7 @@ def test_validation_before_any_launch(lib):
     assert lib.tgvkv_score(ok, None, 8 | 4, fake, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
     assert lib.tgvkv_score(ok, None, 8 | 1, fake, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
     assert lib.tgvkv_score(ok, None, 8 | 7, fake, fake, fake, fake, fake, fake, fake, fake, fake, big, s) == -1
-    # normalisers from the caller: only with exactly TEXT|VISION, no budgets, not fused
+    # normalisers from the caller: only with exactly TEXT|VISION, no budgets
     assert lib.tgvkv_score(ok, None, 16, fake, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
     assert lib.tgvkv_score(ok, None, 16 | 7, fake, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
     assert lib.tgvkv_score(ok, None, 16 | 2, fake, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1

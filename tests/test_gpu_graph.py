@@ -67,7 +67,7 @@ def test_decode_graph_replays(lib, heads_q, heads_kv):
     assert torch.equal(buf.out, eager[T - 1])
 
 
-@pytest.mark.parametrize("schedule", ["two_step", "fused"])
+@pytest.mark.parametrize("schedule", ["two_step", "phases"])
 def test_eviction_graph_replays(lib, schedule):
     """The whole eviction pass (scores, budgets, vision scores where needed, selection,
     compaction) captured once and replayed: every output equals the eager pass bit for bit."""

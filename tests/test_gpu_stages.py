@@ -328,14 +328,13 @@ SCORE_SHAPES = {
 }
 
 
-@pytest.mark.parametrize("fused", [False, True])
 @pytest.mark.parametrize("name", sorted(SCORE_SHAPES))
 @pytest.mark.parametrize("head_mode", [0, 1])
-def test_score_matches_oracle(lib, name, head_mode, fused):
+def test_score_matches_oracle(lib, name, head_mode):
     torch = _torch()
     cfg = SCORE_SHAPES[name]
-    log(f"score {name} mode={head_mode} fused={fused}")
-    phases = bd.SCORE_ALL | (bd.SCORE_FUSED if fused else 0)
+    log(f"score {name} mode={head_mode}")
+    phases = bd.SCORE_ALL
     t = make_prefill_tensors(cfg, seed=3, names=("q_text", "k"))
     p = bd.problem_from(cfg)
     o = bd.make_opts(head_mode=head_mode)
@@ -380,19 +379,18 @@ def _ramp_inputs(cfg, direction, seed=11):
     return f32_to_bf16_bits(q.astype(np.float32)), f32_to_bf16_bits(k.astype(np.float32))
 
 
-@pytest.mark.parametrize("fused", [False, True])
 @pytest.mark.parametrize("direction", ["rising", "falling", "zigzag"])
 @pytest.mark.parametrize("shape", ["gqa7_d128", "twelve_blocks_gqa4", "four_blocks"])
-def test_score_moving_max(lib, shape, direction, fused):
+def test_score_moving_max(lib, shape, direction):
     """Logits that climb along the keys: the reference max of every row moves again and again, with
     up to 2^8-sized terms summed between moves; the scores still match the oracle."""
     torch = _torch()
     cfg = SCORE_SHAPES[shape]
-    log(f"score moving max {shape} {direction} fused={fused}")
+    log(f"score moving max {shape} {direction}")
     qb, kb = _ramp_inputs(cfg, direction)
     p = bd.problem_from(cfg)
     buf = bd.EvictionBuffers(p, bd.make_opts(), 0, 1)
-    buf.score(dev_bf16(qb), dev_bf16(kb), bd.SCORE_ALL | (bd.SCORE_FUSED if fused else 0))
+    buf.score(dev_bf16(qb), dev_bf16(kb), bd.SCORE_ALL)
     torch.cuda.synchronize()
     for b in range(cfg.batch):
         for l in range(cfg.layers):
