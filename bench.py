@@ -62,6 +62,17 @@ def parse():
     ap.add_argument("--page-size", type=int, default=16, help="rows per page of the paged cache")
     ap.add_argument("--decode-steps", type=int, default=None)
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--tv-gap", type=float, default=None,
+                    help="draw the question-row queries with the per-layer depth profile of this strength "
+                         "(default: the workload's i.i.d. text queries)")
+    ap.add_argument("--no-depth-profile", action="store_true",
+                    help="skip the extra run of the same workload with the depth profile (tv_gap 6)")
+    ap.add_argument("--no-flush-mall", dest="flush_mall", action="store_false",
+                    help="do not flush the MALL before timed passes (by default every timed pass starts after a "
+                         "512 MB read of an unrelated buffer, so the MALL holds none of its inputs and no dirty "
+                         "lines; passes after a 512 MB write, and back-to-back passes, are timed separately)")
+    ap.add_argument("--no-ceilings", action="store_true",
+                    help="skip the in-run read / copy / matrix-core ceiling measurements")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target length of the oracle sample")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -330,6 +341,56 @@ def mfma_for(kernel, workload):
     return rec
 
 
+FLUSH_BYTES = 512 << 20       # read (or written) before a timed pass so the 256 MB MALL holds none of its inputs
+CEILING_BYTES = 1 << 30       # read / copy ceiling stream
+CEILING_MFMA_WG = 512         # 2 waves per SIMD on all 1024 SIMDs
+CEILING_MFMA_ITERS = 20000
+
+
+def measure_ceilings(bd, reps=5):
+    """The chip's achievable rates, measured in this process (HIP events on the launch stream):
+    a 1 GiB non-temporal read stream and a 1 GiB copy (the access pattern of the key sweeps,
+    compaction and decode), and back-to-back dense bf16 MFMAs on every SIMD."""
+    import torch
+    stream = torch.cuda.current_stream()
+    src = torch.empty(CEILING_BYTES, dtype=torch.uint8, device="cuda")
+    src.fill_(1)
+    dst = torch.empty_like(src)
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    out = torch.empty(CEILING_MFMA_WG * 256, dtype=torch.float32, device="cuda")
+
+    def timed(fn):
+        fn()  # warm-up launch
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        best = None
+        for _ in range(reps):
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1)
+            best = ms if best is None else min(best, ms)
+        return best
+
+    read_ms = timed(lambda: bd.tgvkv_ceiling_read(src, sink))
+    copy_ms = timed(lambda: bd.tgvkv_ceiling_copy(src, dst))
+    flops = [0]
+
+    def mfma():
+        flops[0] = bd.tgvkv_ceiling_mfma(CEILING_MFMA_WG, CEILING_MFMA_ITERS, out)
+
+    mfma_ms = timed(mfma)
+    del src, dst
+    return {
+        "read_gbs": round(CEILING_BYTES / (read_ms * 1e-3) / 1e9, 1),
+        "copy_gbs": round(2 * CEILING_BYTES / (copy_ms * 1e-3) / 1e9, 1),
+        "mfma_bf16_tflops": round(flops[0] / (mfma_ms * 1e-3) / 1e12, 1),
+        "how": f"best of {reps}: 1 GiB read and 1 GiB copy with 16-byte non-temporal loads (copy counts read "
+               f"+ write bytes); {CEILING_MFMA_WG} workgroups x 4 waves x {CEILING_MFMA_ITERS} rounds of 8 "
+               f"independent v_mfma_f32_16x16x32_bf16",
+    }
+
+
 def main():
     args = parse()
     if args.ingest_mfma_counters:
@@ -354,13 +415,17 @@ def main():
     import torch
 
     from paper_2606_03075_amd import binding as bd
-    from workloads import CONFIGS, make_decode_tensors, make_prefill_tensors, total_budget
+    from workloads import CONFIGS, DEPTH_PROFILE_TV_GAP, depth_profile, make_decode_tensors, make_prefill_tensors, \
+        total_budget
+    from workloads.gen import gen_qtext_slice, f32_to_bf16_bits
 
     bd.load_library()
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     cfg = CONFIGS[args.workload]
+    if args.tv_gap is not None:
+        cfg = depth_profile(cfg, args.tv_gap)
     rho = args.rho if args.rho is not None else cfg.rhos[0]
     T = cfg.decode_steps if args.decode_steps is None else args.decode_steps
     B, L, N = cfg.batch, cfg.layers, cfg.n_tokens
@@ -370,7 +435,7 @@ def main():
     t0 = time.perf_counter()
     t = make_prefill_tensors(cfg, seed=args.seed)
     dec = make_decode_tensors(cfg, seed=args.seed, steps=max(T, 1))
-    log(f"[bench] generated {cfg.name} inputs in {time.perf_counter() - t0:.1f} s")
+    log(f"[bench] generated {cfg.name} inputs (tv_gap {cfg.tv_gap:g}) in {time.perf_counter() - t0:.1f} s")
 
     def dev(x):
         return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).cuda()
@@ -387,11 +452,16 @@ def main():
     stream = torch.cuda.current_stream()
     schedule = args.schedule
     if args.lse_from_prefill:
+        schedule = "lse_in"
+
+    def prefill_normalisers():
         # what a prefill attention kernel returns for the text rows (their row log-sum-exp),
         # produced here, outside the timed region, by the library's own statistics sweep
         buf.score(q_d, k_d, bd.SCORE_STATS | bd.SCORE_TEXT)
         torch.cuda.synchronize()
-        schedule = "lse_in"
+
+    if args.lse_from_prefill:
+        prefill_normalisers()
 
     paged = args.cache == "paged"
     if paged:
@@ -403,8 +473,19 @@ def main():
         used = torch.zeros((1,), dtype=torch.int64, device="cuda")
         steps_d = torch.arange(max(T, 1), dtype=torch.int32, device="cuda")[:, None].repeat(1, B).contiguous()
         log(f"[bench] paged cache: {n_pages} pages of {args.page_size} rows, table width {width}")
+    flush_buf = None
+    if args.flush_mall:
+        flush_buf = torch.ones(FLUSH_BYTES // 4, dtype=torch.float32, device="cuda")
+        flush_sum = torch.empty((), dtype=torch.float32, device="cuda")
+    flush = "read" if args.flush_mall else None
 
-    def one_step(events=None):
+    def do_flush():
+        if flush == "read":
+            torch.sum(flush_buf, out=flush_sum)  # 512 MB of clean lines replace whatever the MALL held
+        elif flush == "write":
+            flush_buf.zero_()  # 512 MB of dirty lines, as a prefill that just wrote the cache leaves it
+
+    def one_step(events=None, decode=True):
         names = []
 
         def mark(name):
@@ -414,6 +495,7 @@ def main():
                 ev.record(stream)
                 events.append((name, ev))
 
+        do_flush()  # outside the timed intervals
         mark("start")
         sched = buf.evict(q_d, k_d, v_d, schedule=schedule, marks=mark, compact=not paged)
         if paged:
@@ -422,7 +504,7 @@ def main():
             bd.tgvkv_compact_paged(p, opts, k_d, v_d, buf.idx, buf.budgets, buf.idx_offsets, tot, table,
                                    args.page_size, pool.k_pool, pool.v_pool, unit_order=buf.unit_order)
             mark("compact")
-        for s_ in range(T):
+        for s_ in range(T if decode else 0):
             mark("decode_gap")  # launch gap before the step: in the step time, not in the kernel's
             if paged:
                 pool.decode(p, opts, table, buf.budgets, max(T, 1), steps_d[s_], dq[s_], dk[s_], dv[s_], buf.out,
@@ -432,76 +514,126 @@ def main():
             mark("decode")
         return sched
 
-    for _ in range(args.warmup):
-        sched = one_step()
-    torch.cuda.synchronize()
-    timed = [[] for _ in range(args.steps)]
-    w0 = time.perf_counter()
-    for k in range(args.steps):
-        sched = one_step(timed[k])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - w0
-    decode_graph_us = None if paged else decode_in_graph(buf, dq, dk, dv, T, args.steps)
-
-    stage_ms = {}
-    dec_ms = 0.0
-    dec_gap_ms = 0.0
-    step_ms = 0.0
-    evict_per_step, decode_launch_us = [], []  # spread over the timed steps / launches
-    for evs in timed:
-        ev_step = 0.0
-        for (n0, e0), (n1, e1) in zip(evs[:-1], evs[1:]):
-            raw = e0.elapsed_time(e1)
-            ms = raw / args.steps
-            if n1 == "decode":
-                dec_ms += ms / max(T, 1)
-                decode_launch_us.append(raw * 1e3)
-            elif n1 == "decode_gap":
-                dec_gap_ms += ms / max(T, 1)
-            else:
-                stage_ms[n1] = stage_ms.get(n1, 0.0) + ms
-                ev_step += raw
-        evict_per_step.append(ev_step)
-        step_ms += evs[0][1].elapsed_time(evs[-1][1]) / args.steps
-    evict_ms = sum(stage_ms.values())
+    def run(n_warm, n_timed, decode=True):
+        """n_warm untimed steps, then n_timed steps with events; returns per-stage mean times."""
+        for _ in range(n_warm):
+            one_step(decode=decode)
+        torch.cuda.synchronize()
+        timed = [[] for _ in range(n_timed)]
+        w0 = time.perf_counter()
+        sched = None
+        for k in range(n_timed):
+            sched = one_step(timed[k], decode=decode)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - w0
+        stage_ms, dec_ms, dec_gap_ms, step_ms = {}, 0.0, 0.0, 0.0
+        evict_per_step, decode_launch_us = [], []
+        for evs in timed:
+            ev_step = 0.0
+            for (n0, e0), (n1, e1) in zip(evs[:-1], evs[1:]):
+                raw = e0.elapsed_time(e1)
+                ms = raw / n_timed
+                if n1 == "decode":
+                    dec_ms += ms / max(T, 1)
+                    decode_launch_us.append(raw * 1e3)
+                elif n1 == "decode_gap":
+                    dec_gap_ms += ms / max(T, 1)
+                else:
+                    stage_ms[n1] = stage_ms.get(n1, 0.0) + ms
+                    ev_step += raw
+            evict_per_step.append(ev_step)
+            step_ms += evs[0][1].elapsed_time(evs[-1][1]) / n_timed
+        return {"sched": sched, "stage_ms": stage_ms, "evict_ms": sum(stage_ms.values()), "dec_ms": dec_ms,
+                "dec_gap_ms": dec_gap_ms, "step_ms": step_ms, "wall": wall, "evict_per_step": evict_per_step,
+                "decode_launch_us": decode_launch_us}
 
     def spread(xs, nd):
         if not xs:
             return None
         q = np.percentile(np.asarray(xs, np.float64), [10, 50, 90])
         return {"p10": round(float(q[0]), nd), "median": round(float(q[1]), nd), "p90": round(float(q[2]), nd)}
+
+    thr = buf.forced_or_text()
+
+    def vision_layers(sched):
+        budgets = buf.budgets.cpu().numpy()
+        return int((budgets > thr).sum()) if sched == "two_step" else B * L
+
+    # ---- the timed steps: each pass starts after a 512 MB read of an unrelated buffer (cold: the
+    # MALL holds none of its inputs and nothing dirty), and is followed by every decode step
+    main_run = run(args.warmup, args.steps)
+    sched = main_run["sched"]
+    stage_ms, dec_ms, evict_ms = main_run["stage_ms"], main_run["dec_ms"], main_run["evict_ms"]
+    vis_layers = vision_layers(sched)
+    decode_graph_us = None if paged else decode_in_graph(buf, dq, dk, dv, T, args.steps)
+    # ---- the eviction pass after a 512 MB write (the MALL full of dirty lines, whose write-back
+    # then competes with the pass's reads), and back to back with no flush and no decode in
+    # between (warm: what the previous pass left in the MALL and L2, its compaction's writes
+    # included)
+    after_write_ms = warm_ms = None
+    if args.flush_mall:
+        flush = "write"
+        after_write_ms = run(args.warmup, args.steps, decode=False)["evict_ms"]
+        flush = None
+        warm_ms = run(args.warmup, args.steps, decode=False)["evict_ms"]
+        flush = "read"
+    ceilings = None if args.no_ceilings else measure_ceilings(bd)
     tokens_per_s = B * N / (evict_ms * 1e-3)
 
     # algorithmic bytes per launch: what the method must move, each once (K and the text
     # queries for scoring, the retained K/V read and written for compaction, the pruned
-    # cache plus new tokens for a decode step), not what an implementation re-reads
+    # cache plus new tokens for a decode step); score_vision's key bytes are the second
+    # sweep over K, traffic of this implementation rather than of the method
     H, Hkv, D, Nq, Nv = cfg.heads_q, cfg.heads_kv, cfg.head_dim, cfg.n_qst, cfg.n_vis
-    budgets = buf.budgets.cpu().numpy()
-    thr = buf.forced_or_text()
-    vis_layers = int((budgets > thr).sum()) if sched == "two_step" else B * L
     kept = buf.kept  # tokens each sequence keeps
     k_bytes = B * L * Hkv * N * D * 2
     q_bytes = B * L * H * cfg.n_text * D * 2
+    compact_bytes = 4 * B * kept * Hkv * D * 2
     alg = {
         "score": k_bytes + q_bytes,
         "score_text": k_bytes + q_bytes,
         "score_stats": k_bytes + B * L * H * Nq * D * 2,
         "score_vision": vis_layers * (Hkv * Nv * D * 2 + H * Nq * D * 2),
-        "compact": 4 * B * kept * Hkv * D * 2,
+        "compact": compact_bytes,
         "decode": (B * kept + B * L * (T + 1) / 2.0) * Hkv * D * 4 + B * L * (H * D * 2 + 2 * Hkv * D * 2 + H * D * 4),
     }
+    kinds = {k: "algorithmic" for k in alg}
+    kinds["score_vision"] = "implementation: the second sweep over the vision keys (re-read)"
+
+    def achieved_peak(kname):
+        if ceilings is None:
+            return None
+        return ceilings["copy_gbs"] if kname == "compact" else ceilings["read_gbs"]
+
     roofs = {}
     for kname in ("score", "score_text", "score_stats", "score_vision", "compact", "decode"):
         ms = dec_ms if kname == "decode" else stage_ms.get(kname, 0.0)
         if ms <= 0:
             continue
         gbs = alg[kname] / (ms * 1e-3) / 1e9
+        ap = achieved_peak(kname)
         roofs[kname] = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                         "frac": round(gbs / HBM_PEAK_GBS, 4),
                         "traffic": traffic_for(kname, counter_key(cfg.name, args.vision_only, args.cache), T),
-                        "kernel": kname, "alg_bytes_per_launch": int(alg[kname]), "avg_launch_ms": round(ms, 4),
-                        "ms_per_step": round(ms * (T if kname == "decode" else 1), 4)}
+                        "kernel": kname, "alg_bytes_per_launch": int(alg[kname]), "bytes_kind": kinds[kname],
+                        "avg_launch_ms": round(ms, 4),
+                        "ms_per_step": round(ms * (T if kname == "decode" else 1), 4),
+                        "achieved_peak": ap, "frac_of_achieved": round(gbs / ap, 4) if ap else None}
     dominant = max(roofs, key=lambda k: roofs[k]["ms_per_step"])
+    # the whole eviction pass against what the method must move once: K and the text queries,
+    # and the retained K/V read and written by compaction
+    pass_bytes = k_bytes + q_bytes + compact_bytes
+
+    def pass_roof(ms):
+        gbs = pass_bytes / (ms * 1e-3) / 1e9
+        ap = ceilings["read_gbs"] if ceilings else None
+        return {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(gbs / HBM_PEAK_GBS, 4), "alg_bytes": int(pass_bytes),
+                "alg_bytes_are": "K + text-row queries once, plus the retained K/V read and written",
+                "evict_ms": round(ms, 4), "roof_ms": round(pass_bytes / (HBM_PEAK_GBS * 1e9) * 1e3, 4),
+                "roof_tokens_per_s": round(B * N / (pass_bytes / (HBM_PEAK_GBS * 1e9)), 1),
+                "achieved_peak": ap, "frac_of_achieved": round(gbs / ap, 4) if ap else None}
+
     # scoring's algorithmic matrix work: one QK^T over the logits every text row can see
     # (system row i sees i + 1 keys, question row i sees the system and vision keys and i + 1
     # question keys), 2 * head_dim flops each; the implementation's second sweep is not counted
@@ -523,10 +655,14 @@ def main():
     scoring_mfma = None
     if score_ms > 0:
         tf = score_flops / (score_ms * 1e-3) / 1e12
+        mp = ceilings["mfma_bf16_tflops"] if ceilings else None
         scoring_mfma = {"alg_flops": int(score_flops), "score_ms": round(score_ms, 4), "alg_tflops": round(tf, 1),
                         "peak_tflops": BF16_PEAK_TFLOPS, "alg_frac_of_peak": round(tf / BF16_PEAK_TFLOPS, 4),
+                        "achieved_peak_tflops": mp, "alg_frac_of_achieved": round(tf / mp, 4) if mp else None,
                         "kernels": per_kernel}
 
+    recipe = (f"text queries and keys i.i.d. N(0,1)" if cfg.tv_gap == 0 else
+              f"depth profile: question-row vision logits shifted per layer (tv_gap {cfg.tv_gap:g})")
     line = {
         "metric": METRIC,
         "value": round(tokens_per_s, 1),
@@ -534,7 +670,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(step_ms, 4),
+        "ms_per_step": round(main_run["step_ms"], 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -545,27 +681,62 @@ def main():
                                f"{' of vision tokens (all text kept)' if args.vision_only else ''}"
                                f"{', text-row normalisers from the prefill' if args.lse_from_prefill else ''}"
                                f", {T} decode steps"
-                               f"{f', paged cache ({args.page_size}-row pages)' if paged else ''}",
+                               f"{f', paged cache ({args.page_size}-row pages)' if paged else ''}; {recipe}; "
+                               f"vision noise {cfg.vis_sigma:g}{', sink on token 0' if cfg.sink else ''}"
+                               f"{f', {cfg.frames} frames' if cfg.frames else ''}",
                    "batch": B, "layers": L, "heads_q": H, "heads_kv": Hkv, "head_dim": D,
                    "n_sys": cfg.n_sys, "n_vis": Nv, "n_qst": Nq, "retention": rho, "total_budget_per_seq": tot,
+                   "tv_gap": cfg.tv_gap, "vision_noise": cfg.vis_sigma,
                    "vision_only": bool(args.vision_only),
                    "normalisers_from_prefill": bool(args.lse_from_prefill),
                    "budget_rule": args.budget_rule, "vision_rank": args.vision_rank, "tpr": not args.no_tpr,
                    "decode_steps": T, "vision_scored_layers": vis_layers, "schedule": sched,
-                   "cache": args.cache, "page_size": args.page_size if paged else None},
+                   "cache": args.cache, "page_size": args.page_size if paged else None,
+                   "mall_before_each_pass": "512 MB read of an unrelated buffer" if args.flush_mall else
+                   "what the previous step's decode left"},
         "evict_ms": round(evict_ms, 4),
-        "evict_ms_spread": spread(evict_per_step, 4),
-        "decode_launch_us_spread": spread(decode_launch_us, 2),
+        "evict_ms_spread": spread(main_run["evict_per_step"], 4),
+        "evict_ms_after_write": round(after_write_ms, 4) if after_write_ms is not None else None,
+        "evict_ms_warm": round(warm_ms, 4) if warm_ms is not None else None,
+        "evict_roofline": pass_roof(evict_ms),
+        "decode_launch_us_spread": spread(main_run["decode_launch_us"], 2),
         "decode_us_per_step": round(dec_ms * 1e3, 2),
-        "decode_us_per_step_with_launch_gaps": round((dec_ms + dec_gap_ms) * 1e3, 2),
+        "decode_us_per_step_with_launch_gaps": round((dec_ms + main_run["dec_gap_ms"]) * 1e3, 2),
         "decode_us_per_step_graph": decode_graph_us,
         "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},
         "schedule": sched,
         "scoring_mfma": scoring_mfma,
         "roofline": roofs[dominant],
         "roofline_kernels": roofs,
-        "wall_ms_per_step": round(wall / args.steps * 1e3, 3),
+        "ceilings": ceilings,
+        "wall_ms_per_step": round(main_run["wall"] / args.steps * 1e3, 3),
     }
+
+    # ---- the same workload with the depth profile of the text-to-vision attention (only the
+    # question-row queries change), as a labelled variant beside the i.i.d. headline
+    if not args.no_depth_profile and cfg.tv_gap == 0 and not args.vision_only and not args.no_tpr \
+            and args.budget_rule == "tv":
+        dcfg = depth_profile(cfg)
+        t1 = time.perf_counter()
+        qd = np.stack([np.stack([f32_to_bf16_bits(gen_qtext_slice(dcfg, args.seed, b, l)) for l in range(L)])
+                       for b in range(B)])
+        q_d.copy_(dev(qd))
+        del qd
+        if args.lse_from_prefill:
+            prefill_normalisers()
+        log(f"[bench] depth-profile queries in {time.perf_counter() - t1:.1f} s")
+        dp = run(args.warmup, args.steps)
+        dvl = vision_layers(dp["sched"])
+        line["depth_profile"] = {
+            "tv_gap": DEPTH_PROFILE_TV_GAP,
+            "value": round(B * N / (dp["evict_ms"] * 1e-3), 1), "unit": "tokens/s",
+            "evict_ms": round(dp["evict_ms"], 4), "evict_ms_spread": spread(dp["evict_per_step"], 4),
+            "evict_roofline": pass_roof(dp["evict_ms"]),
+            "decode_us_per_step": round(dp["dec_ms"] * 1e3, 2),
+            "stage_ms": {k: round(v, 4) for k, v in dp["stage_ms"].items()},
+            "vision_scored_layers": dvl,
+            "budgets_seq0": buf.budgets[0].tolist(),
+        }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(cfg, t, dec, tot, args.cpu_seconds, args.vision_only, opts)
     print(json.dumps(line), flush=True)

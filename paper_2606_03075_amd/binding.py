@@ -26,6 +26,8 @@ ABI_VERSION = 7  # TGVKV_ABI_VERSION of the library this binding marshals for
 EXPORTS = ("tgvkv_score", "tgvkv_budget", "tgvkv_select", "tgvkv_compact", "tgvkv_decode_attn",
            "tgvkv_page_plan", "tgvkv_page_table", "tgvkv_compact_paged", "tgvkv_decode_attn_paged",
            "tgvkv_sizes", "tgvkv_workspace_size", "tgvkv_status_string", "tgvkv_abi_version")
+# measurement kernels (include/tgvkv_ceiling.h): the chip's achievable stream and matrix-core rates
+CEILING_EXPORTS = ("tgvkv_ceiling_read", "tgvkv_ceiling_copy", "tgvkv_ceiling_mfma", "tgvkv_ceiling_mfma_flops")
 
 
 class TgvkvProblem(ctypes.Structure):
@@ -77,9 +79,15 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.tgvkv_status_string.argtypes = [ctypes.c_int]
     lib.tgvkv_status_string.restype = ctypes.c_char_p
     lib.tgvkv_abi_version.argtypes = []
+    lib.tgvkv_ceiling_read.argtypes = [vp, i64, vp, vp]
+    lib.tgvkv_ceiling_copy.argtypes = [vp, vp, i64, vp]
+    lib.tgvkv_ceiling_mfma.argtypes = [i32, i32, vp, vp]
+    lib.tgvkv_ceiling_mfma_flops.argtypes = [i32, i32]
+    lib.tgvkv_ceiling_mfma_flops.restype = ctypes.c_longlong
     for name in ("tgvkv_score", "tgvkv_budget", "tgvkv_select", "tgvkv_compact", "tgvkv_decode_attn",
                  "tgvkv_page_plan", "tgvkv_page_table", "tgvkv_compact_paged", "tgvkv_decode_attn_paged",
-                 "tgvkv_sizes", "tgvkv_abi_version"):
+                 "tgvkv_sizes", "tgvkv_abi_version", "tgvkv_ceiling_read", "tgvkv_ceiling_copy",
+                 "tgvkv_ceiling_mfma"):
         getattr(lib, name).restype = ctypes.c_int32
     if lib.tgvkv_abi_version() != ABI_VERSION:
         raise RuntimeError(f"{p} has ABI {lib.tgvkv_abi_version()}, this binding needs {ABI_VERSION}; "
@@ -233,6 +241,39 @@ def tgvkv_decode_attn(problem, opts, kc, vc, budgets, seg_offsets, decode_reserv
                                           _ptr(workspace, None, "workspace"), ws_bytes,
                                           _ptr(unit_order, (torch.int32,), "unit_order"), _stream(stream))
     _check("tgvkv_decode_attn", st)
+
+
+# --------------------------------------------------------------------------- measurement kernels
+def _ceiling_check(fn: str, status: int):
+    if status != 0:
+        raise RuntimeError(f"{fn} failed: status {status}")
+
+
+def tgvkv_ceiling_read(src, sink, stream=None):
+    """One non-temporal 16-byte read stream over the bytes of src (a contiguous device tensor)."""
+    import torch
+    _ceiling_check("tgvkv_ceiling_read", load_library().tgvkv_ceiling_read(
+        _ptr(src, None, "src"), src.numel() * src.element_size(), _ptr(sink, (torch.int32,), "sink"),
+        _stream(stream)))
+
+
+def tgvkv_ceiling_copy(src, dst, stream=None):
+    """Copy src to dst (same byte size) with the read stream's loads and non-temporal stores."""
+    nbytes = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() != nbytes:
+        raise ValueError("src and dst must have the same byte size")
+    _ceiling_check("tgvkv_ceiling_copy", load_library().tgvkv_ceiling_copy(
+        _ptr(src, None, "src"), _ptr(dst, None, "dst"), nbytes, _stream(stream)))
+
+
+def tgvkv_ceiling_mfma(workgroups, iters, out, stream=None):
+    """Back-to-back dense bf16 MFMAs; returns the launch's flops (out: float32 [workgroups * 256])."""
+    if out.numel() < workgroups * 256:
+        raise ValueError("out must hold workgroups * 256 floats")
+    lib = load_library()
+    _ceiling_check("tgvkv_ceiling_mfma", lib.tgvkv_ceiling_mfma(int(workgroups), int(iters),
+                                                                _ptr(out, _f32(), "out"), _stream(stream)))
+    return int(lib.tgvkv_ceiling_mfma_flops(int(workgroups), int(iters)))
 
 
 # --------------------------------------------------------------------------- paged cache

@@ -18,7 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build", "tgvkv")
 LIB = os.path.join(PKG, "libtgvkv.so")
 
-HIP_SOURCES = ["score.hip", "budget.hip", "select.hip", "compact.hip", "decode.hip", "pages.hip"]
+HIP_SOURCES = ["score.hip", "budget.hip", "select.hip", "compact.hip", "decode.hip", "pages.hip", "ceiling.hip"]
 CXX_SOURCES = ["api.cpp"]
 ARCH = "gfx950"
 

@@ -33,17 +33,21 @@ def lib():
     return bd.load_library()
 
 
-def declared_functions():
-    with open(os.path.join(ROOT, "include", "tgvkv.h")) as f:
+def declared_functions(header="tgvkv.h"):
+    with open(os.path.join(ROOT, "include", header)) as f:
         text = f.read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(tgvkv_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(tgvkv_[a-z0-9_]+)\s*\(", text)))
 
 
 def test_exports_every_declared_symbol(lib):
+    headers = sorted(f for f in os.listdir(os.path.join(ROOT, "include")) if f.endswith(".h"))
+    assert headers == ["tgvkv.h", "tgvkv_ceiling.h"], headers
     names = declared_functions()
     assert set(bd.EXPORTS) <= set(names) and len(names) == len(bd.EXPORTS), names
-    for n in names:
+    ceiling = declared_functions("tgvkv_ceiling.h")
+    assert sorted(ceiling) == sorted(bd.CEILING_EXPORTS), ceiling
+    for n in names + ceiling:
         assert hasattr(lib, n), n
     assert lib.tgvkv_abi_version() == bd.ABI_VERSION == 7
     for st in (0, -1, -2, -3, -4, -5):
@@ -279,3 +283,24 @@ def test_empty_batch_is_a_no_op(lib):
 def test_binding_fails_loudly_without_library(tmp_path):
     with pytest.raises(RuntimeError):
         bd.load_library(str(tmp_path / "missing.so"))
+
+
+@pytest.mark.skipif(_gpu(), reason="fake pointers are used only where no GPU exists")
+def test_ceiling_validation_before_any_launch(lib):
+    fake = ctypes.c_void_p(0x10000)
+    odd = ctypes.c_void_p(0x10008)
+    s = ctypes.c_void_p(0)
+    assert lib.tgvkv_ceiling_read(None, 16, fake, s) == -1
+    assert lib.tgvkv_ceiling_read(fake, 0, fake, s) == -1
+    assert lib.tgvkv_ceiling_read(fake, 24, fake, s) == -1       # not a multiple of 16
+    assert lib.tgvkv_ceiling_read(odd, 16, fake, s) == -1        # not 16-byte aligned
+    assert lib.tgvkv_ceiling_read(fake, 16, None, s) == -1
+    assert lib.tgvkv_ceiling_copy(fake, None, 16, s) == -1
+    assert lib.tgvkv_ceiling_copy(fake, odd, 16, s) == -1
+    assert lib.tgvkv_ceiling_copy(fake, fake, -16, s) == -1
+    assert lib.tgvkv_ceiling_mfma(0, 10, fake, s) == -1
+    assert lib.tgvkv_ceiling_mfma(4, 0, fake, s) == -1
+    assert lib.tgvkv_ceiling_mfma(4, 10, None, s) == -1
+    # 4 waves per workgroup, 8 MFMAs of 16 x 16 x 32 (2 flops each) per round
+    assert lib.tgvkv_ceiling_mfma_flops(3, 5) == 3 * 4 * 5 * 8 * 2 * 16 * 16 * 32
+    assert lib.tgvkv_ceiling_mfma_flops(0, 5) == 0

@@ -12,7 +12,7 @@ import pytest
 
 from tests.gpu_util import log
 from tests.test_gpu_e2e import run_and_check
-from workloads.configs import CONFIGS
+from workloads.configs import CONFIGS, depth_profile
 
 pytestmark = pytest.mark.gpu
 
@@ -35,9 +35,12 @@ def _properties(buf, cfg):
                 assert np.isin(sel, text).all()
 
 
-def test_llavanext_full(lib):
-    """batch 4 x 32 layers x 32 heads, 35 + 2880 + 64 tokens, 5 % retention, 128 decode steps."""
-    cfg = CONFIGS["llavanext"]
+@pytest.mark.parametrize("recipe", ["iid", "depth"])
+def test_llavanext_full(lib, recipe):
+    """batch 4 x 32 layers x 32 heads, 35 + 2880 + 64 tokens, 5 % retention, 128 decode steps; i.i.d.
+    text queries (every layer's budget passes N_t) and the depth profile (budgets spread over an
+    order of magnitude, a third of the layers keep text only), both as the benchmark runs them."""
+    cfg = CONFIGS["llavanext"] if recipe == "iid" else depth_profile(CONFIGS["llavanext"])
     buf = run_and_check(cfg, cfg.rhos[0], steps=cfg.decode_steps, seed=0, check_seqs=range(cfg.batch),
                         decode_seqs=[0])
     _properties(buf, cfg)
@@ -52,14 +55,19 @@ def test_qwen2vl_video_full(lib, rho):
     _properties(buf, cfg)
 
 
-def test_stress13b_full(lib):
+@pytest.mark.parametrize("recipe", ["iid", "depth"])
+def test_stress13b_full(lib, recipe):
     """batch 16 x 40 layers x 40 heads, 35 + 2880 + 256 tokens, 5 % retention, 256 decode steps.
+
+    With i.i.d. text queries every layer's budget (158 or 159) is below N_t = 291, so every layer
+    takes the text-top-k case of Eq. (10); with the depth profile the shallowest layers keep all
+    text plus vision tokens.
 
     Sequences 0 and 15 are generated and checked against the oracle (every layer); the other
     sequences of the batch repeat them (even ones sequence 0, odd ones sequence 15), so the
     device runs the full-size batch, and sequences holding the same data must agree exactly.
     """
-    cfg = CONFIGS["stress13b"]
+    cfg = CONFIGS["stress13b"] if recipe == "iid" else depth_profile(CONFIGS["stress13b"])
     buf = run_and_check(cfg, cfg.rhos[0], steps=cfg.decode_steps, seed=0, check_seqs=[0, 15], decode_seqs=[0],
                         gen_seqs=[0, 15])
     _properties(buf, cfg)

@@ -5,7 +5,7 @@ import torch
 
 from workloads import (CONFIGS, bf16_bits_to_f32, f32_to_bf16_bits, gen_k_slice, gen_qtext_slice,
                        make_decode_tensors, make_prefill_tensors, total_budget)
-from workloads.configs import custom_config
+from workloads.configs import custom_config, depth_profile
 
 
 def test_bf16_rounding_matches_torch():
@@ -65,3 +65,15 @@ def test_total_budget():
     assert total_budget(0.05, 3171, 40) == 6342
     assert total_budget(0.05, 651, 32) == 1042 and total_budget(0.2, 651, 32) == 4166
     assert total_budget(0.5, 3, 1) == 2   # halves round away from zero
+
+
+def test_depth_profile_changes_only_question_queries():
+    """The model shapes draw i.i.d. text queries; the depth profile shifts only the question rows."""
+    for name in ("llava15", "llavanext", "qwen2vl_video", "stress13b"):
+        assert CONFIGS[name].tv_gap == 0.0
+    cfg = custom_config(batch=1, layers=4, heads_q=4, heads_kv=2, head_dim=64, n_sys=3, n_vis=40, n_qst=6)
+    dp = depth_profile(cfg)
+    for l in range(4):
+        q0, q1 = gen_qtext_slice(cfg, 3, 0, l), gen_qtext_slice(dp, 3, 0, l)
+        assert np.array_equal(q0[:, :3], q1[:, :3]) and not np.array_equal(q0[:, 3:], q1[:, 3:])
+        assert np.array_equal(gen_k_slice(cfg, 3, 0, l), gen_k_slice(dp, 3, 0, l))

@@ -7,7 +7,7 @@ arithmetic (no attention, scores, budgets or selection), only the random
 recipes and the shapes.
 """
 
-from .configs import WorkloadConfig, CONFIGS, get_config, custom_config  # noqa: F401
+from .configs import WorkloadConfig, CONFIGS, DEPTH_PROFILE_TV_GAP, get_config, custom_config, depth_profile  # noqa: F401
 from .gen import (  # noqa: F401
     bf16_bits_to_f32,
     f32_to_bf16_bits,

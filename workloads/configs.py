@@ -58,18 +58,31 @@ CONFIGS = {
                            rhos=(0.10, 0.50, 1.0), decode_steps=1, fp32_data=True),
     # LLaVA-1.5-7B: 32 layers, 32 MHA heads, 35 + 576 + 40 tokens.
     "llava15": WorkloadConfig("llava15", 1, 32, 32, 32, 128, 35, 576, 40, vis_sigma=0.3,
-                              rhos=(0.05, 0.10, 0.20), decode_steps=64, tv_gap=6.0),
+                              rhos=(0.05, 0.10, 0.20), decode_steps=64),
     # LLaVA-NeXT-7B with 5 image tiles: batch 4, 35 + 2880 + 64 tokens.
     "llavanext": WorkloadConfig("llavanext", 4, 32, 32, 32, 128, 35, 2880, 64, vis_sigma=0.25,
-                                rhos=(0.05,), decode_steps=128, tv_gap=6.0),
+                                rhos=(0.05,), decode_steps=128),
     # Qwen2-VL-7B GQA video: 28 layers, 28 query heads over 4 KV heads, 16 frames x 512.
     "qwen2vl_video": WorkloadConfig("qwen2vl_video", 8, 28, 28, 4, 128, 16, 8192, 48,
                                     vis_sigma=0.3, frames=16, frame_alpha=0.1,
-                                    rhos=(0.05, 0.10), decode_steps=128, tv_gap=6.0),
+                                    rhos=(0.05, 0.10), decode_steps=128),
     # 13B-class stress: 40 layers, 40 heads, batch 16, 35 + 2880 + 256 tokens.
     "stress13b": WorkloadConfig("stress13b", 16, 40, 40, 40, 128, 35, 2880, 256, vis_sigma=0.3,
-                                rhos=(0.05,), decode_steps=256, tv_gap=6.0),
+                                rhos=(0.05,), decode_steps=256),
 }
+
+# The model shapes above draw their text queries i.i.d. N(0, 1) (tv_gap 0).  The depth
+# profile is a named variant of any of them: question-row queries shifted per layer so that
+# shallow layers attend to the image and middle layers hardly at all (see gen), which makes
+# TVB's layer budgets spread out over an order of magnitude.
+DEPTH_PROFILE_TV_GAP = 6.0
+
+
+def depth_profile(cfg: "WorkloadConfig", tv_gap: float = DEPTH_PROFILE_TV_GAP) -> "WorkloadConfig":
+    """The same workload with the per-layer text-to-vision depth profile (only the question-row
+    queries change; keys, values and decode inputs are the same draws)."""
+    return dataclasses.replace(cfg, tv_gap=float(tv_gap))
+
 
 # Ordered as the configs are listed: tiny first, then the four model shapes.
 CONFIG_ORDER = ("tiny", "llava15", "llavanext", "qwen2vl_video", "stress13b")
