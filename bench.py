@@ -481,7 +481,7 @@ def main():
 
     def do_flush():
         if flush == "read":
-            torch.sum(flush_buf, out=flush_sum)  # 512 MB of clean lines replace whatever the MALL held
+            torch.sum(flush_buf, dim=0, out=flush_sum)  # 512 MB of clean lines replace whatever the MALL held
         elif flush == "write":
             flush_buf.zero_()  # 512 MB of dirty lines, as a prefill that just wrote the cache leaves it
 
