@@ -27,7 +27,8 @@
  *    invalid call returns a negative status and launches nothing.  Kernels are
  *    enqueued asynchronously on `stream`; the library never allocates, frees or
  *    synchronises, and keeps no pointer after a call returns.  A launch failure
- *    returns TGVKV_E_HIP.  Calls are thread-safe (no global mutable state).
+ *    returns TGVKV_E_HIP.  Calls are thread-safe (no global mutable state), except
+ *    that tgvkv_decode_attn_noalloc calls share one buffer per GPU (see there).
  *  - Query head h reads KV head h / (heads_q / heads_kv).
  *  - "groups" g: 1 when opts.head_mode == 0 (one retained set per sequence and
  *    layer, from attention averaged over all query heads), heads_kv when
@@ -46,7 +47,7 @@
 extern "C" {
 #endif
 
-#define TGVKV_ABI_VERSION 7
+#define TGVKV_ABI_VERSION 8
 
 typedef enum tgvkv_status {
     TGVKV_OK = 0,
@@ -253,6 +254,29 @@ tgvkv_status tgvkv_decode_attn(const tgvkv_problem* problem, const tgvkv_opts* o
                                const void* q, const void* k_new, const void* v_new, float* out,
                                void* workspace, size_t workspace_bytes, const int32_t* unit_order_or_null,
                                hipStream_t stream);
+
+/*
+ * tgvkv_decode_attn_noalloc -- tgvkv_decode_attn for callers that cannot allocate:
+ * code under HIP graph capture, serving loops and harnesses that forbid hipMalloc.
+ *
+ * Same arguments, kernels and results as tgvkv_decode_attn, bit for bit, without the
+ * workspace: when the token ranges are split (few (sequence, layer, KV head) units),
+ * the split partials go to a static device buffer of the library, one per GPU, held
+ * until the process ends.  The call allocates nothing.  The first call on a device
+ * looks the buffer's address up with that device current.
+ * Limit: the partials must fit in 16 MiB, i.e. tgvkv_workspace_size(p, o,
+ * TGVKV_CALL_DECODE) <= 16 MiB (every shape these kernels split stays below 9 MiB);
+ * above it TGVKV_E_WORKSPACE and nothing is launched.  Every element of the buffer
+ * that a call reads it first writes itself, so nothing is cleared between calls.
+ * Calls that overlap on one GPU (other streams or threads while one is in flight)
+ * share that GPU's buffer and race: serialise them, or use tgvkv_decode_attn with a
+ * workspace each.  Calls on different GPUs do not interact.
+ */
+tgvkv_status tgvkv_decode_attn_noalloc(const tgvkv_problem* problem, const tgvkv_opts* opts,
+                                       void* kc, void* vc, const int32_t* budgets,
+                                       const int64_t* seg_offsets, int32_t decode_reserve, int32_t step,
+                                       const void* q, const void* k_new, const void* v_new, float* out,
+                                       const int32_t* unit_order_or_null, hipStream_t stream);
 
 /*
  * Paged cache, for serving with continuous batching.

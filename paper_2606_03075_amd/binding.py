@@ -22,8 +22,9 @@ SCORE_STATS, SCORE_TEXT, SCORE_VISION, SCORE_ALL = 1, 2, 4, 7
 SCORE_LSE_IN = 16  # lse holds the text rows' normalisers from the caller's prefill: K is read once
 CALL_SCORE, CALL_DECODE = 0, 1
 
-ABI_VERSION = 7  # TGVKV_ABI_VERSION of the library this binding marshals for
+ABI_VERSION = 8  # TGVKV_ABI_VERSION of the library this binding marshals for
 EXPORTS = ("tgvkv_score", "tgvkv_budget", "tgvkv_select", "tgvkv_compact", "tgvkv_decode_attn",
+           "tgvkv_decode_attn_noalloc",
            "tgvkv_page_plan", "tgvkv_page_table", "tgvkv_compact_paged", "tgvkv_decode_attn_paged",
            "tgvkv_sizes", "tgvkv_workspace_size", "tgvkv_status_string", "tgvkv_abi_version")
 # measurement kernels (include/tgvkv_ceiling.h): the chip's achievable stream and matrix-core rates
@@ -68,6 +69,7 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.tgvkv_select.argtypes = [P, O, vp, vp, vp, vp, vp, vp]
     lib.tgvkv_compact.argtypes = [P, O, vp, vp, vp, vp, vp, vp, i64, i32, vp, vp, vp, vp]
     lib.tgvkv_decode_attn.argtypes = [P, O, vp, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, sz, vp, vp]
+    lib.tgvkv_decode_attn_noalloc.argtypes = [P, O, vp, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp]
     lib.tgvkv_page_plan.argtypes = [P, O, i64, i32, i32, vp, vp]
     lib.tgvkv_page_table.argtypes = [P, O, vp, i64, i32, i32, vp, i64, vp, i32, vp, vp]
     lib.tgvkv_compact_paged.argtypes = [P, O, vp, vp, vp, vp, vp, i64, vp, i32, i32, vp, vp, i64, vp, vp]
@@ -85,7 +87,7 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.tgvkv_ceiling_mfma_flops.argtypes = [i32, i32]
     lib.tgvkv_ceiling_mfma_flops.restype = ctypes.c_longlong
     for name in ("tgvkv_score", "tgvkv_budget", "tgvkv_select", "tgvkv_compact", "tgvkv_decode_attn",
-                 "tgvkv_page_plan", "tgvkv_page_table", "tgvkv_compact_paged", "tgvkv_decode_attn_paged",
+                 "tgvkv_decode_attn_noalloc", "tgvkv_page_plan", "tgvkv_page_table", "tgvkv_compact_paged", "tgvkv_decode_attn_paged",
                  "tgvkv_sizes", "tgvkv_abi_version", "tgvkv_ceiling_read", "tgvkv_ceiling_copy",
                  "tgvkv_ceiling_mfma"):
         getattr(lib, name).restype = ctypes.c_int32
@@ -241,6 +243,20 @@ def tgvkv_decode_attn(problem, opts, kc, vc, budgets, seg_offsets, decode_reserv
                                           _ptr(workspace, None, "workspace"), ws_bytes,
                                           _ptr(unit_order, (torch.int32,), "unit_order"), _stream(stream))
     _check("tgvkv_decode_attn", st)
+
+
+def tgvkv_decode_attn_noalloc(problem, opts, kc, vc, budgets, seg_offsets, decode_reserve, step, q, k_new, v_new,
+                              out, stream=None, unit_order=None):
+    """tgvkv_decode_attn without a workspace: split partials in the library's per-GPU static buffer."""
+    import torch
+    st = load_library().tgvkv_decode_attn_noalloc(ctypes.byref(problem), _opts_ref(opts), _ptr(kc, _bf16(), "kc"),
+                                                  _ptr(vc, _bf16(), "vc"), _ptr(budgets, (torch.int32,), "budgets"),
+                                                  _ptr(seg_offsets, (torch.int64,), "seg_offsets"),
+                                                  int(decode_reserve), int(step), _ptr(q, _bf16(), "q"),
+                                                  _ptr(k_new, _bf16(), "k_new"), _ptr(v_new, _bf16(), "v_new"),
+                                                  _ptr(out, _f32(), "out"),
+                                                  _ptr(unit_order, (torch.int32,), "unit_order"), _stream(stream))
+    _check("tgvkv_decode_attn_noalloc", st)
 
 
 # --------------------------------------------------------------------------- measurement kernels

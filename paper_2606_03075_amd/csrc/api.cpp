@@ -342,6 +342,34 @@ tgvkv_status tgvkv_decode_attn(const tgvkv_problem* problem, const tgvkv_opts* o
                                            out, static_cast<float*>(workspace), unit_order_or_null, stream));
 }
 
+tgvkv_status tgvkv_decode_attn_noalloc(const tgvkv_problem* problem, const tgvkv_opts* opts, void* kc, void* vc,
+                                       const int32_t* budgets, const int64_t* seg_offsets, int32_t decode_reserve,
+                                       int32_t step, const void* q, const void* k_new, const void* v_new, float* out,
+                                       const int32_t* unit_order_or_null, hipStream_t stream) {
+    Shape s;
+    tgvkv_status st = make_shape(problem, opts, &s);
+    if (st != TGVKV_OK) return st;
+    if (decode_reserve < 0) return TGVKV_E_INVAL;
+    if (step < 0 || step >= decode_reserve) return TGVKV_E_CAPACITY;
+    if (s.B == 0) return TGVKV_OK;
+    if (kc == nullptr || vc == nullptr || budgets == nullptr || seg_offsets == nullptr || q == nullptr ||
+        k_new == nullptr || v_new == nullptr || out == nullptr)
+        return TGVKV_E_INVAL;
+    if (!aligned16(kc) || !aligned16(vc) || !aligned16(q) || !aligned16(k_new) || !aligned16(v_new))
+        return TGVKV_E_INVAL;
+    const size_t need = decode_workspace_bytes(s);
+    if (need > tgvkv::kDecodeScratchBytes) return TGVKV_E_WORKSPACE;
+    float* ws = nullptr;
+    if (need > 0) {
+        const hipError_t e = tgvkv::decode_scratch(&ws);
+        if (e != hipSuccess) return TGVKV_E_HIP;
+    }
+    return hip_status(tgvkv::launch_decode(s, static_cast<uint16_t*>(kc), static_cast<uint16_t*>(vc), budgets,
+                                           seg_offsets, decode_reserve, step, static_cast<const uint16_t*>(q),
+                                           static_cast<const uint16_t*>(k_new), static_cast<const uint16_t*>(v_new),
+                                           out, ws, unit_order_or_null, stream));
+}
+
 tgvkv_status tgvkv_page_plan(const tgvkv_problem* problem, const tgvkv_opts* opts, int64_t total_budget,
                              int32_t decode_reserve, int32_t page_size, int32_t* max_pages_out,
                              int64_t* pool_pages_out) {

@@ -24,6 +24,7 @@
 // workgroup serves, so the long segments do not all start last.
 #include <algorithm>
 #include <climits>
+#include <mutex>
 
 #include "tgvkv_device.h"
 #include "tgvkv_rows.h"
@@ -533,6 +534,31 @@ hipError_t launch_decode_d(const Shape& s, const Rows& rows, size_t lds_bytes, u
 }
 
 }  // namespace
+
+// Split partials of decode for callers that cannot allocate (tgvkv_decode_attn_noalloc):
+// one buffer per GPU, living as long as the process.  Host code must not pass the array's
+// name to a kernel (it is a host-side stand-in there); decode_scratch() gives its device
+// address, looked up once per device with that device current.
+static __device__ __align__(256) float scratch[kDecodeScratchBytes / sizeof(float)];
+
+hipError_t decode_scratch(float** ptr) {
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static float* addr[kMaxDevices] = {};
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (addr[dev] == nullptr) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        addr[dev] = static_cast<float*>(p);
+    }
+    *ptr = addr[dev];
+    return hipSuccess;
+}
 
 int decode_splits(const Shape& s) {
     const long long units = (long long)s.B * s.L * s.Hkv;

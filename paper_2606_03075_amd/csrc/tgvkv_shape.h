@@ -70,6 +70,10 @@ hipError_t launch_compact_paged(const Shape& s, const uint16_t* k, const uint16_
                                 const int32_t* unit_order, uint16_t* k_pool, uint16_t* v_pool, hipStream_t st);
 
 int decode_splits(const Shape& s);
+// Bytes of the per-GPU static buffer that holds decode's split partials for callers that
+// cannot allocate, and its device address on the current device (looked up once per device).
+constexpr size_t kDecodeScratchBytes = size_t(16) << 20;
+hipError_t decode_scratch(float** ptr);
 hipError_t launch_decode(const Shape& s, uint16_t* kc, uint16_t* vc, const int32_t* budgets,
                          const int64_t* seg_off, int32_t reserve, int32_t step, const uint16_t* q,
                          const uint16_t* k_new, const uint16_t* v_new, float* out, float* ws_part,

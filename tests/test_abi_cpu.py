@@ -49,7 +49,7 @@ def test_exports_every_declared_symbol(lib):
     assert sorted(ceiling) == sorted(bd.CEILING_EXPORTS), ceiling
     for n in names + ceiling:
         assert hasattr(lib, n), n
-    assert lib.tgvkv_abi_version() == bd.ABI_VERSION == 7
+    assert lib.tgvkv_abi_version() == bd.ABI_VERSION == 8
     for st in (0, -1, -2, -3, -4, -5):
         assert lib.tgvkv_status_string(st)
     assert lib.tgvkv_status_string(7) == b"unknown status"
@@ -134,6 +134,16 @@ def test_validation_before_any_launch(lib):
     assert dec(-1, fake, fake, fake, big) == -4
     assert dec(0, fake, None, fake, big) == -1
     assert dec(0, fake, fake, None, 0) == -3
+    # the scratch-free variant validates the same way, before looking up its buffer
+    na = lambda prob, step, kn, out: lib.tgvkv_decode_attn_noalloc(prob, None, fake, fake, fake, fake, 4, step, fake,
+                                                                   kn, fake, out, None, s)
+    assert na(ok, 4, fake, fake) == -4
+    assert na(ok, -1, fake, fake) == -4
+    assert na(ok, 0, None, fake) == -1
+    assert na(ok, 0, fake, None) == -1
+    assert na(ok, 0, odd, fake) == -1
+    assert na(ctypes.byref(P(heads_q=3)), 0, fake, fake) == -1
+    assert na(ctypes.byref(P(head_dim=96)), 0, fake, fake) == -2
 
 
 def _plan(problem, opts, total, reserve, page):
