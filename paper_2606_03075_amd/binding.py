@@ -15,7 +15,8 @@ import os
 from typing import Optional
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libtgvkv.so")
+# TGVKV_LIBRARY names another build of the same ABI (e.g. the host-sanitized one of build.py)
+LIB_PATH = os.environ.get("TGVKV_LIBRARY") or os.path.join(_HERE, "libtgvkv.so")
 
 TGVKV_OK, TGVKV_E_INVAL, TGVKV_E_UNSUPPORTED, TGVKV_E_WORKSPACE, TGVKV_E_CAPACITY, TGVKV_E_HIP = 0, -1, -2, -3, -4, -5
 SCORE_STATS, SCORE_TEXT, SCORE_VISION, SCORE_ALL = 1, 2, 4, 7

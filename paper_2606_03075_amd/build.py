@@ -87,5 +87,36 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
     return LIB
 
 
+SAN_BUILD = os.path.join(ROOT, "_build", "tgvkv_san")
+SAN_LIB = os.path.join(SAN_BUILD, "libtgvkv_san.so")
+SAN_FLAGS = ["-fsanitize=address,undefined", "-fno-sanitize-recover=undefined", "-fno-omit-frame-pointer", "-g"]
+
+
+def build_sanitized(verbose: bool = False) -> str:
+    """A host-sanitized copy of the library for CPU tests of the C ABI: api.cpp (argument
+    validation, workspace layout, launch set-up) built by g++ with AddressSanitizer and
+    UndefinedBehaviorSanitizer, linked with the unsanitized device objects of build().
+    Load it with libasan / libubsan preloaded (the Python interpreter is not instrumented).
+    Returns the library path (under _build/, never shipped)."""
+    os.makedirs(SAN_BUILD, exist_ok=True)
+    dev_objs = [os.path.join(BUILD, os.path.splitext(src)[0] + ".o") for src in HIP_SOURCES]
+    if not all(os.path.exists(o) for o in dev_objs):
+        build(verbose)
+    obj = os.path.join(SAN_BUILD, "api_san.o")
+    cmd = ["g++", "-O1", "-fPIC", "-std=c++17", "-Wall", "-D__HIP_PLATFORM_AMD__", f"-I{INCLUDE}", f"-I{CSRC}",
+           "-I/opt/rocm/include"] + SAN_FLAGS + ["-c", os.path.join(CSRC, "api.cpp"), "-o", obj]
+    for c in (cmd, ["g++", "-shared", "-o", SAN_LIB, obj] + dev_objs + SAN_FLAGS[:1] +
+              ["-L/opt/rocm/lib", "-lamdhip64", "-Wl,-rpath,/opt/rocm/lib"]):
+        if verbose:
+            print(" ".join(c), flush=True)
+        r = subprocess.run(c, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"sanitized build failed\n{r.stdout}\n{r.stderr}")
+    return SAN_LIB
+
+
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    if "--sanitize" in sys.argv:
+        print(build_sanitized(verbose="-v" in sys.argv))
+    else:
+        print(build(verbose="-v" in sys.argv))
