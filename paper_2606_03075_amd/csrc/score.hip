@@ -80,13 +80,19 @@ __global__ __launch_bounds__(kThreads) void score_stats_kernel(Shape s, int rowg
 // the text pass through LDS.  The row statistics are bit-identical to
 // score_stats'; the text pass stages the unit's text keys in the freed tiles
 // when they fit (a different summation order of the same column sums).
+// Row plans whose statistics+text kernel has text mode 2 (text_pass_qregs): with four row
+// slots per wave the sweep sets the kernel's register count, and the pass fits beside it;
+// with fewer slots it would cost occupancy, with six it would spill.
+template <int NSLOT, int KS>
+constexpr bool kQregsText = NSLOT == 4 && KS == 1;
+
 template <int D, int NSLOT, int KS>
 __global__ __launch_bounds__(kThreads) void score_stats_text_kernel(Shape s, const uint16_t* __restrict__ q_text,
                                                                     const uint16_t* __restrict__ k,
                                                                     float* __restrict__ lse,
                                                                     float* __restrict__ ws_vm,
                                                                     float* __restrict__ ws_colsum,
-                                                                    float* __restrict__ ws_vmh, int lds_text) {
+                                                                    float* __restrict__ ws_vmh, int text_mode) {
     constexpr int RSETS = 4 / KS;
     __shared__ __attribute__((aligned(16))) char tiles[2][Geo<D>::TILE_BYTES];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -104,8 +110,10 @@ __global__ __launch_bounds__(kThreads) void score_stats_text_kernel(Shape s, con
     const uint16_t* kbase = k + ((size_t)bl * s.Hkv + kvh) * (size_t)s.N * D;
     stats_sweep<D, NSLOT, KS>(s, kbase, 0, s.N, qf, qrow, tiles, m, lsum, vsum);
 
-    // the key tiles are free now: [G][N_t] normalisers (base 2), then [G][N_q] vision masses
-    float* lse2s = reinterpret_cast<float*>(&tiles[0][0]);
+    // [G][N_t] normalisers (base 2), then [G][N_q] vision masses: in the dynamic LDS area
+    // (text mode 2, whose text pass streams keys through the tiles), else in the freed tiles
+    extern __shared__ float tarea[];
+    float* lse2s = text_mode == 2 ? tarea : reinterpret_cast<float*>(&tiles[0][0]);
     float* vms = lse2s + (size_t)s.G * s.Nt;
     if (kp == 0 && lane < 16) {
 #pragma unroll
@@ -132,7 +140,15 @@ __global__ __launch_bounds__(kThreads) void score_stats_text_kernel(Shape s, con
         for (int off = 32; off > 0; off >>= 1) a += shfl_xor(a, off);
         if ((tid & 63) == 0) ws_vmh[head0 + g] = a;
     }
-    if (lds_text) {
+    if constexpr (kQregsText<NSLOT, KS>) {
+        if (text_mode == 2) {
+            // the question rows' fragments are still in registers: only text keys are loaded
+            text_pass_qregs<D, NSLOT, KS>(s, bl, kvh, q_text, k, lse, qf, lse2s, vms + (size_t)s.G * s.Nq, tiles,
+                                          ws_colsum);
+            return;
+        }
+    }
+    if (text_mode == 1) {
         // the unit's text keys go into the freed tiles after the normalisers and masses
         const size_t off = ((size_t)s.G * (s.Nt + s.Nq) * sizeof(float) + 15) & ~(size_t)15;
         text_pass_lds<D>(s, bl, kvh, q_text, k, lse, lse2s, &tiles[0][0] + off,
@@ -247,13 +263,16 @@ __global__ __launch_bounds__(kThreads) void score_vision_kernel(Shape s, int row
     const int NB = s.G * QB;
     const int rb0 = rg * RSETS * NSLOT;
 
-    // the row loads are issued before the budget test so that their latencies overlap
+    // a layer whose budget leaves no room for vision tokens needs no scores: its workgroups
+    // leave before loading anything (at the 13B stress shape with i.i.d. text queries every
+    // layer is such a layer, and loading the rows first cost 0.27 ms of a launch that computes
+    // nothing)
+    if (budgets != nullptr && budgets[bl] <= vis_threshold) return;
     bf16x8 qf[NSLOT][Geo<D>::KSTEPS];
     int qrow[NSLOT];
     load_qrows<D, NSLOT, KS, false>(s, q_text, bl, kvh, rb0, qf, qrow);
     float lse2[NSLOT][4], coef[NSLOT][4];
     load_row_coefs<NSLOT, KS, false>(s, bl, kvh, rb0, lse, w_txt, lse2, coef);
-    if (budgets != nullptr && budgets[bl] <= vis_threshold) return;
     settle_qrows<D, NSLOT>(qf);
 #pragma unroll
     for (int sl = 0; sl < NSLOT; ++sl)
@@ -378,18 +397,26 @@ hipError_t launch_score_stats_text(const Shape& s, const RowPlan& rp, const uint
     const long long nblk = (long long)s.B * s.L * s.Hkv;
     if (nblk == 0) return hipSuccess;
     dim3 grid((unsigned)nblk), block(kThreads);
-    // the text pass stages the unit's text keys (in chunks of key blocks, if need be) in the
-    // freed key tiles, after the normalisers and masses, when its partials and the system
-    // keys' blocks fit there
+    // Text mode 2 (the question rows' fragments reused from the sweep, the system keys staged
+    // in the tiles, the question keys streamed through them) needs the normalisers, masses and
+    // column partials in a dynamic LDS area that leaves the kernel's occupancy as it is.
+    // Otherwise mode 1 stages the unit's text keys (in chunks of key blocks, if need be) in
+    // the freed key tiles, after the normalisers and masses, when its partials and the system
+    // keys' blocks fit there; else mode 0 reads them from memory.
+    const long long tile_bytes = 2LL * kTile * (2 * s.D + 16);
+    const long long area = text_area_floats(s.G, s.Nt, s.Nq) * (long long)sizeof(float);
+    const int occupancy = rp.nslot == 1 ? 4 : rp.nslot == 2 ? 3 : (rp.nslot == 4 && s.D == 64) ? 3 : 2;
+    const bool qregs = rp.nslot == 4 && rp.ks == 1 && s.Ns <= 2 * kTile && area <= 163840 / occupancy - tile_bytes;
     const long long head = ((long long)s.G * (s.Nt + s.Nq) * 4 + 15) / 16 * 16;
+    const size_t dyn = qregs ? (size_t)area : 0;
     if (s.D == 128) {
-        const int lds_text = text_lds_fits<128>(s.G, s.Ns, s.Nt, 2LL * Geo<128>::TILE_BYTES - head);
-        TGVKV_ROWPLAN_DISPATCH(score_stats_text_kernel, 128, rp, grid, block, 0, st, s, q_text, k, lse, ws_vm,
-                               ws_colsum, ws_vmh, lds_text);
+        const int mode = qregs ? 2 : text_lds_fits<128>(s.G, s.Ns, s.Nt, tile_bytes - head) ? 1 : 0;
+        TGVKV_ROWPLAN_DISPATCH(score_stats_text_kernel, 128, rp, grid, block, dyn, st, s, q_text, k, lse, ws_vm,
+                               ws_colsum, ws_vmh, mode);
     } else {
-        const int lds_text = text_lds_fits<64>(s.G, s.Ns, s.Nt, 2LL * Geo<64>::TILE_BYTES - head);
-        TGVKV_ROWPLAN_DISPATCH(score_stats_text_kernel, 64, rp, grid, block, 0, st, s, q_text, k, lse, ws_vm,
-                               ws_colsum, ws_vmh, lds_text);
+        const int mode = qregs ? 2 : text_lds_fits<64>(s.G, s.Ns, s.Nt, tile_bytes - head) ? 1 : 0;
+        TGVKV_ROWPLAN_DISPATCH(score_stats_text_kernel, 64, rp, grid, block, dyn, st, s, q_text, k, lse, ws_vm,
+                               ws_colsum, ws_vmh, mode);
     }
     return hipGetLastError();
 }

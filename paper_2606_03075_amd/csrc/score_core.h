@@ -818,6 +818,225 @@ __device__ void text_pass_lds(const Shape& s, int bl, int kvh, const uint16_t* _
     __syncthreads();
 }
 
+// LDS of text_pass_qregs outside the key tiles, in floats: [G][N_t] normalisers (base 2),
+// [G][N_q] vision masses, then the per-wave column partials [4][G][TK] (TK = N_t rounded up
+// to 16 rows).
+__host__ __device__ constexpr long long text_area_floats(int G, int Nt, int Nq) {
+    return (long long)G * Nt + (long long)G * Nq + 4LL * G * ((Nt + 15) / 16) * 16;
+}
+
+// The text pass of a unit whose question rows are held in registers by the statistics
+// sweep (qf, the sweep's row plan; rb0 = 0).  The question rows' text->text probabilities
+// are recomputed from those fragments: against the system keys, staged once in the key
+// tiles, and against the question keys, streamed through the tile pipeline, so that the
+// pass loads no question-row fragment and only the text keys.  The system rows (which see
+// only system keys) load their fragments: first their normalisers, then their column
+// sums.  Column sums go to per-wave LDS partials, which are then added in wave order.
+// lse2s [G][N_t] holds the question rows' normalisers (base 2) on entry; part is
+// 4*G*TK floats of LDS; the two key tiles must hold the system keys (N_s <= 2 * kTile).
+template <int D, int NSLOT, int KS>
+__device__ void text_pass_qregs(const Shape& s, int bl, int kvh, const uint16_t* __restrict__ q_text,
+                                const uint16_t* __restrict__ k, float* __restrict__ lse,
+                                const bf16x8 (&qf)[NSLOT][Geo<D>::KSTEPS], float* lse2s, float* part,
+                                char (*tiles)[Geo<D>::TILE_BYTES], float* __restrict__ ws_colsum) {
+    using GG = Geo<D>;
+    constexpr int RSETS = 4 / KS;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int rs = wave % RSETS, kp = wave / RSETS;
+    const size_t head0 = (size_t)bl * s.H + kvh * s.G;
+    const uint16_t* kbase = k + ((size_t)bl * s.Hkv + kvh) * (size_t)s.N * D;
+    const int QB = (s.Nq + 15) >> 4;
+    const int NB = s.G * QB;
+    const int TK = ((s.Nt + 15) >> 4) * 16;
+    const int SB = (s.Ns + 15) >> 4;
+    const int koff = (lane >> 4) * 8;
+    char* sysk = &tiles[0][0];  // the system keys' 16-row blocks, ROWB bytes a row
+
+    // per slot: its head, its first question row, and the normalisers of this lane's
+    // accumulator rows 4*(lane/16) + j in C[row][key] (+inf for rows past N_q: p = 0)
+    int gsl[NSLOT], q0s[NSLOT];
+    bool sok[NSLOT];
+    float l2r[NSLOT][4];
+#pragma unroll
+    for (int sl = 0; sl < NSLOT; ++sl) {
+        const int rb = rs + sl * RSETS;
+        sok[sl] = rb < NB;
+        gsl[sl] = sok[sl] ? rb / QB : 0;
+        q0s[sl] = (rb % QB) * 16;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int qi = q0s[sl] + (lane >> 4) * 4 + j;
+            l2r[sl][j] = (sok[sl] && qi < s.Nq) ? lse2s[gsl[sl] * s.Nt + s.Ns + qi] : __builtin_inff();
+        }
+    }
+    // adds a 16-key block's column sums (lane: key lane % 16, 4 rows each) of head g to this
+    // wave's partial at text index t0 + lane % 16, for the block's first kn keys
+    auto flush = [&](float col, int g, int t0, int kn) {
+        col = sum_xor32(sum_xor16(col));
+        if (lane < min(kn, 16)) part[((size_t)wave * s.G + g) * TK + t0 + lane] += col;
+    };
+    // question rows x one 16-key block kf of text keys, of which the first kn are keys; c0:
+    // the block's first question-key index (causal: keys of later question tokens are masked),
+    // kSysBlock for system keys (visible to every question row); t0: the block's text index
+    constexpr int kSysBlock = -(1 << 30);
+    auto qrow_block = [&](const bf16x8 (&kf)[GG::KSTEPS], int c0, int t0, int kn) {
+        float colacc = 0.f;
+        int gcur = -1;
+#pragma unroll
+        for (int sl = 0; sl < NSLOT; ++sl) {
+            // wave-uniform: a slot past the last block, or whose rows all precede the block
+            if (!sok[sl] || c0 > q0s[sl] + 15) continue;
+            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(qf[sl][ks], kf[ks], acc);
+            const bool full = c0 + 15 <= q0s[sl];  // every key of the block precedes every row
+            float col = 0.f;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const float p = fast_exp2(acc[j] * s.scale2 - l2r[sl][j]);
+                const bool vis = full || c0 + (lane & 15) <= q0s[sl] + (lane >> 4) * 4 + j;
+                col += vis ? p : 0.f;
+            }
+            if (gsl[sl] != gcur) {
+                if (gcur >= 0) flush(colacc, gcur, t0, kn);
+                colacc = 0.f;
+                gcur = gsl[sl];
+            }
+            colacc += col;
+        }
+        if (gcur >= 0) flush(colacc, gcur, t0, kn);
+    };
+
+    // 1. the system keys into the tiles (every load of a round issued before its stores);
+    //    the partials zeroed
+    {
+        constexpr int kStage = 8;
+        const int nch = SB * 16 * GG::CPR;
+        for (int x0 = 0; x0 < nch; x0 += kStage * kThreads) {
+            u32x4 r[kStage];
+#pragma unroll
+            for (int i = 0; i < kStage; ++i) {
+                const int c = min(x0 + i * kThreads + tid, nch - 1);
+                r[i] = load16(kbase + (size_t)min(c / GG::CPR, s.Ns - 1) * D + (c % GG::CPR) * 8);
+            }
+#pragma unroll
+            for (int i = 0; i < kStage; ++i) {
+                const int c = x0 + i * kThreads + tid;
+                if (c < nch) store16(sysk + (c / GG::CPR) * GG::ROWB + (c % GG::CPR) * 16, r[i]);
+            }
+        }
+        for (int x = tid; x < 4 * s.G * TK; x += kThreads) part[x] = 0.f;
+    }
+    __syncthreads();
+
+    // 2. system rows x system keys: the system rows' normalisers (C[key][row]: a lane owns row i)
+    auto load_q = [&](bf16x8 (&f)[GG::KSTEPS], int g, int row) {
+        const uint16_t* src = q_text + ((head0 + g) * s.Nt + row) * D + koff;
+#pragma unroll
+        for (int ks = 0; ks < GG::KSTEPS; ++ks) f[ks] = as_bf16x8(load16(src + ks * 32));
+    };
+    for (int item = wave; item < s.G * SB; item += 4) {
+        const int g = item / SB, rb = item % SB;
+        const int i = rb * 16 + (lane & 15);
+        bf16x8 qs[GG::KSTEPS];
+        load_q(qs, g, min(i, s.Ns - 1));
+        float m = kNegInf, l = 0.f;
+        for (int kb = 0; kb <= rb; ++kb) {
+            bf16x8 kf[GG::KSTEPS];
+            load_kfrag<D>(kf, sysk, kb, lane);
+            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(kf[ks], qs[ks], acc);
+            float z[4];
+            float mx = kNegInf;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int key = kb * 16 + (lane >> 4) * 4 + j;
+                z[j] = (key <= i && key < s.Ns) ? acc[j] * s.scale2 : kNegInf;
+                mx = fmaxf(mx, z[j]);
+            }
+            if (mx > m) {
+                l *= fast_exp2(m - mx);
+                m = mx;
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (z[j] != kNegInf) l += fast_exp2(z[j] - m);
+        }
+        float dummy = 0.f;
+#pragma unroll
+        for (int off = 16; off < 64; off <<= 1) {
+            const float m2 = shfl_xor(m, off), l2 = shfl_xor(l, off), d2 = shfl_xor(dummy, off);
+            merge_stats(m, l, dummy, m2, l2, d2);
+        }
+        if (lane < 16 && i < s.Ns) {
+            const float L2 = m + log2f(l);
+            lse2s[g * s.Nt + i] = L2;
+            lse[(head0 + g) * s.Nt + i] = L2 * kLn2;
+        }
+    }
+    __syncthreads();
+
+    // 3. column sums over the system keys: system rows (C[row][key]: a lane owns key j), then
+    //    question rows from their registers (key blocks dealt over the key parts)
+    for (int item = wave; item < s.G * SB; item += 4) {
+        const int g = item / SB, rb = item % SB;
+        bf16x8 qs[GG::KSTEPS];
+        load_q(qs, g, min(rb * 16 + (lane & 15), s.Ns - 1));
+        float l2[4];
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) l2[jj] = lse2s[g * s.Nt + min(rb * 16 + (lane >> 4) * 4 + jj, s.Ns - 1)];
+        for (int kb = 0; kb <= rb; ++kb) {
+            bf16x8 kf[GG::KSTEPS];
+            load_kfrag<D>(kf, sysk, kb, lane);
+            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(qs[ks], kf[ks], acc);
+            const int j = kb * 16 + (lane & 15);
+            float col = 0.f;
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+                const int ii = rb * 16 + (lane >> 4) * 4 + jj;
+                if (ii < s.Ns && j <= ii) col += fast_exp2(acc[jj] * s.scale2 - l2[jj]);
+            }
+            flush(col, g, kb * 16, s.Ns - kb * 16);
+        }
+    }
+    for (int kb = kp; kb < SB; kb += KS) {
+        bf16x8 kf[GG::KSTEPS];
+        load_kfrag<D>(kf, sysk, kb, lane);
+        qrow_block(kf, kSysBlock, kb * 16, s.Ns - kb * 16);
+    }
+    __syncthreads();  // the tiles are free for the question keys
+
+    // 4. question rows x question keys, through the tile pipeline
+    const int qbeg = s.Ns + s.Nv;
+    tile_pipeline<D, 2>(
+        kbase, qbeg, s.N, tiles,
+        [&](const char* buf, int key0, int) {
+#pragma unroll
+            for (int kb = 0; kb < kTile / 16; ++kb) {
+                if (kb % KS != kp) continue;
+                const int c0 = key0 - qbeg + kb * 16;
+                if (c0 >= s.Nq) continue;  // the last tile's clamped keys
+                bf16x8 kf[GG::KSTEPS];
+                load_kfrag<D>(kf, buf, kb, lane);
+                qrow_block(kf, c0, s.Ns + c0, s.Nq - c0);
+            }
+        },
+        [](int, int) {});
+    __syncthreads();
+
+    // 5. the four waves' partials, in wave order
+    for (int x = tid; x < s.G * s.Nt; x += kThreads) {
+        const int g = x / s.Nt, j = x % s.Nt;
+        float a = 0.f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) a += part[((size_t)w * s.G + g) * TK + j];
+        ws_colsum[(head0 + g) * s.Nt + j] = a;
+    }
+}
+
 // Column sums of the text->text probabilities for one 16-key block kb of query
 // head g of a unit, by one wave, with every text row's normaliser given (natural
 // log, lse [.., N_t] of the head): the items of a unit are independent, so each

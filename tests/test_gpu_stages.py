@@ -325,6 +325,15 @@ SCORE_SHAPES = {
                                         n_qst=45),
     "twelve_blocks_gqa4_d64": custom_config(batch=1, layers=2, heads_q=8, heads_kv=2, head_dim=64, n_sys=2,
                                             n_vis=190, n_qst=37),
+    # sixteen 16-row blocks of one head (the 13B stress shape's row plan, text pass fed from the
+    # sweep's registers): causal question-key blocks skipped, full and diagonal
+    "sixteen_blocks_long_question": custom_config(batch=1, layers=2, heads_q=2, heads_kv=2, head_dim=128, n_sys=35,
+                                                  n_vis=150, n_qst=250),
+    # seven system-key blocks staged for that text pass; and one past its limit of 128 system keys
+    "ten_blocks_long_system": custom_config(batch=1, layers=2, heads_q=3, heads_kv=3, head_dim=128, n_sys=100,
+                                            n_vis=90, n_qst=150),
+    "ten_blocks_system_past_limit": custom_config(batch=1, layers=1, heads_q=2, heads_kv=2, head_dim=128,
+                                                  n_sys=140, n_vis=50, n_qst=150),
 }
 
 
@@ -380,7 +389,7 @@ def _ramp_inputs(cfg, direction, seed=11):
 
 
 @pytest.mark.parametrize("direction", ["rising", "falling", "zigzag"])
-@pytest.mark.parametrize("shape", ["gqa7_d128", "twelve_blocks_gqa4", "four_blocks"])
+@pytest.mark.parametrize("shape", ["gqa7_d128", "twelve_blocks_gqa4", "four_blocks", "sixteen_blocks_long_question"])
 def test_score_moving_max(lib, shape, direction):
     """Logits that climb along the keys: the reference max of every row moves again and again, with
     up to 2^8-sized terms summed between moves; the scores still match the oracle."""
