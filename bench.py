@@ -112,10 +112,12 @@ KERNEL_SOURCES = {
 }
 
 
-def counter_key(workload, vision_only=False, cache="contiguous"):
-    """Key of a workload's counters in profiles/hbm_counters.json (the eviction mode and the cache
-    layout change the bytes)."""
-    return workload + (":vision_only" if vision_only else "") + (":paged" if cache == "paged" else "")
+def counter_key(workload, vision_only=False, cache="contiguous", rho=None):
+    """Key of a workload's counters in profiles/hbm_counters.json (the eviction mode, the cache
+    layout and a retention other than the workload's first change the bytes)."""
+    from workloads import CONFIGS
+    rho_tag = "" if rho is None or rho == CONFIGS[workload].rhos[0] else f"@rho{rho:g}"
+    return workload + rho_tag + (":vision_only" if vision_only else "") + (":paged" if cache == "paged" else "")
 
 
 def traffic_for(kernel, workload, decode_steps=None):
@@ -214,6 +216,8 @@ COPY_BYTES = 1 << 30
 # text pass, the kernel the two-step schedule runs for that stage)
 KERNEL_NAMES = {"score_text": "score_stats_text_kernel", "score_stats": "score_stats_kernel",
                 "score_vision": "score_vision_kernel", "compact": "compact_kernel", "decode": "decode_kernel"}
+# rocprofv3 names of the kernels behind each bench stage (decode runs on the vector or the matrix cores)
+KERNEL_MATCH = {"decode": ("decode_kernel<", "decode_mfma_kernel<")}
 
 
 def calibrate_copy():
@@ -256,8 +260,9 @@ def ingest_counters(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, worklo
                             "fetch_scale": scale_f, "write_scale": scale_w}}
     rec = {}
     for key, kname in KERNEL_NAMES.items():
-        fk = [v for n, v in fetch.items() if kname in n]
-        wk = [v for n, v in write.items() if kname in n]
+        pats = KERNEL_MATCH.get(key, (kname,))
+        fk = [v for n, v in fetch.items() if any(p in n for p in pats)]
+        wk = [v for n, v in write.items() if any(p in n for p in pats)]
         if not fk or not wk:
             continue
         fb, wb = max(fk) * scale_f, max(wk) * scale_w
@@ -394,12 +399,14 @@ def measure_ceilings(bd, reps=5):
 def main():
     args = parse()
     if args.ingest_mfma_counters:
-        ingest_mfma_counters(args.ingest_mfma_counters, counter_key(args.workload, args.vision_only, args.cache))
+        ingest_mfma_counters(args.ingest_mfma_counters,
+                             counter_key(args.workload, args.vision_only, args.cache, args.rho))
         return
     if args.ingest_counters:
         from workloads import CONFIGS
         T = CONFIGS[args.workload].decode_steps if args.decode_steps is None else args.decode_steps
-        ingest_counters(*args.ingest_counters, workload=counter_key(args.workload, args.vision_only, args.cache),
+        ingest_counters(*args.ingest_counters,
+                        workload=counter_key(args.workload, args.vision_only, args.cache, args.rho),
                         decode_steps=T)
         return
     if args.calibrate_copy:
@@ -614,7 +621,7 @@ def main():
         ap = achieved_peak(kname)
         roofs[kname] = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                         "frac": round(gbs / HBM_PEAK_GBS, 4),
-                        "traffic": traffic_for(kname, counter_key(cfg.name, args.vision_only, args.cache), T),
+                        "traffic": traffic_for(kname, counter_key(cfg.name, args.vision_only, args.cache, rho), T),
                         "kernel": kname, "alg_bytes_per_launch": int(alg[kname]), "bytes_kind": kinds[kname],
                         "avg_launch_ms": round(ms, 4),
                         "ms_per_step": round(ms * (T if kname == "decode" else 1), 4),
@@ -641,7 +648,7 @@ def main():
     logits = Ns * (Ns + 1) / 2 + Nq * (Ns + Nv) + Nq * (Nq + 1) / 2
     score_flops = 2.0 * B * L * H * D * logits
     score_ms = sum(v for k, v in stage_ms.items() if k in ("score",) + SCORE_KERNELS)
-    ckey = counter_key(cfg.name, args.vision_only, args.cache)
+    ckey = counter_key(cfg.name, args.vision_only, args.cache, rho)
     per_kernel = {}
     for kname in SCORE_KERNELS + ("score",):
         ms = stage_ms.get(kname, 0.0)
