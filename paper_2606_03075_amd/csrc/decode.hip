@@ -563,11 +563,11 @@ hipError_t decode_scratch(float** ptr) {
 int decode_splits(const Shape& s) {
     const long long units = (long long)s.B * s.L * s.Hkv;
     if (units <= 0) return 1;
-    // split a unit's tokens only up to about 2048 workgroups for the VALU kernel (two rounds
-    // of its 4 workgroups per CU) and 1024 for the matrix-core one (one round): a split costs
-    // partial writes and the combine launch (at the Qwen2-VL shape, 896 units: 40.8 us
-    // unsplit against 46.3 us in two splits)
-    long long n = (s.G >= kMfmaMinGroup ? 1024 : 2048) / units;
+    // split a unit's tokens only up to about 1024 workgroups (one round of 4 workgroups per
+    // CU): a split costs partial writes and the combine launch (at the Qwen2-VL shape, 896
+    // units: 40.8 us unsplit against 46.3 us in two splits; at the LLaVA-1.5 shape, 1024 units
+    // at 5 %: 10.0 us per step replayed from a HIP graph unsplit against 17.2 us in two splits)
+    long long n = 1024 / units;
     if (n < 1) n = 1;
     if (n > 8) n = 8;
     return (int)n;

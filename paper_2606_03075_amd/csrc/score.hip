@@ -363,7 +363,7 @@ RowPlan plan_question_rows(const Shape& s) {
     RowPlan rp;
     if (NB <= 1) { rp.nslot = 1; rp.ks = 4; }
     else if (NB == 2) { rp.nslot = 1; rp.ks = 2; }
-    else if (NB == 3) { rp.nslot = 2; rp.ks = 2; }
+    else if (NB == 3) { rp.nslot = 1; rp.ks = 1; }  // the vision sweep runs these as (2, 2)
     else if (NB <= 4) { rp.nslot = 1; rp.ks = 1; }
     else if (NB <= 8) { rp.nslot = 2; rp.ks = 1; }
     else if (NB <= 16) { rp.nslot = 4; rp.ks = 1; }
@@ -476,6 +476,14 @@ hipError_t launch_score_vision(const Shape& s, const RowPlan& rp, const uint16_t
     if (mass) {
         if (s.D == 128) TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 128, true, rp, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles, vsplit);
         else TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 64, true, rp, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles, vsplit);
+    } else if (rp.nslot == 1 && rp.ks == 1 && (s.G * ((s.Nq + 15) / 16)) == 3) {
+        // three 16-row blocks per unit: two slots over half of each key tile (same row groups);
+        // at the LLaVA-1.5 shape 43 us against 46-48 us for the four-slot shape below
+        const RowPlan r2{2, 2, rp.rowgroups};
+        if (s.D == 128)
+            TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 128, false, r2, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles, vsplit);
+        else
+            TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 64, false, r2, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles, vsplit);
     } else if (rp.nslot == 1 && rp.ks == 1) {
         // four 16-row blocks per unit: the vision sweep runs faster with every wave holding all
         // four blocks over a quarter of each key tile (same row groups, so the same partials)
