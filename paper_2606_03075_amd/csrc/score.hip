@@ -86,13 +86,14 @@ __global__ __launch_bounds__(kThreads) void score_stats_kernel(Shape s, int rowg
 template <int NSLOT, int KS>
 constexpr bool kQregsText = NSLOT == 4 && KS == 1;
 
+// With four row slots the kernel is held to 168 registers, 3 waves per SIMD: it then spills
+// 96 bytes a lane, all outside the sweep's tile loops (at its phase changes and in the text
+// pass), and at the 13B stress shape it took 6.84 ms against 7.21-7.25 ms at 2 waves per SIMD.
 template <int D, int NSLOT, int KS>
-__global__ __launch_bounds__(kThreads) void score_stats_text_kernel(Shape s, const uint16_t* __restrict__ q_text,
-                                                                    const uint16_t* __restrict__ k,
-                                                                    float* __restrict__ lse,
-                                                                    float* __restrict__ ws_vm,
-                                                                    float* __restrict__ ws_colsum,
-                                                                    float* __restrict__ ws_vmh, int text_mode) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NSLOT == 4 ? 3 : 1))) void
+score_stats_text_kernel(Shape s, const uint16_t* __restrict__ q_text, const uint16_t* __restrict__ k,
+                        float* __restrict__ lse, float* __restrict__ ws_vm, float* __restrict__ ws_colsum,
+                        float* __restrict__ ws_vmh, int text_mode) {
     constexpr int RSETS = 4 / KS;
     __shared__ __attribute__((aligned(16))) char tiles[2][Geo<D>::TILE_BYTES];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -405,7 +406,7 @@ hipError_t launch_score_stats_text(const Shape& s, const RowPlan& rp, const uint
     // keys' blocks fit there; else mode 0 reads them from memory.
     const long long tile_bytes = 2LL * kTile * (2 * s.D + 16);
     const long long area = text_area_floats(s.G, s.Nt, s.Nq) * (long long)sizeof(float);
-    const int occupancy = rp.nslot == 1 ? 4 : rp.nslot == 2 ? 3 : (rp.nslot == 4 && s.D == 64) ? 3 : 2;
+    const int occupancy = rp.nslot == 1 ? 4 : rp.nslot == 2 ? 3 : rp.nslot == 4 ? 3 : 2;
     const bool qregs = rp.nslot == 4 && rp.ks == 1 && s.Ns <= 2 * kTile && area <= 163840 / occupancy - tile_bytes;
     const long long head = ((long long)s.G * (s.Nt + s.Nq) * 4 + 15) / 16 * 16;
     const size_t dyn = qregs ? (size_t)area : 0;
