@@ -112,12 +112,13 @@ KERNEL_SOURCES = {
 }
 
 
-def counter_key(workload, vision_only=False, cache="contiguous", rho=None):
-    """Key of a workload's counters in profiles/hbm_counters.json (the eviction mode, the cache
-    layout and a retention other than the workload's first change the bytes)."""
+def counter_key(workload, vision_only=False, cache="contiguous", rho=None, lse_in=False):
+    """Key of a workload's counters in profiles/hbm_counters.json (the eviction mode, the scoring
+    schedule, the cache layout and a retention other than the workload's first change the bytes)."""
     from workloads import CONFIGS
     rho_tag = "" if rho is None or rho == CONFIGS[workload].rhos[0] else f"@rho{rho:g}"
-    return workload + rho_tag + (":vision_only" if vision_only else "") + (":paged" if cache == "paged" else "")
+    return (workload + rho_tag + (":vision_only" if vision_only else "") + (":lse_in" if lse_in else "")
+            + (":paged" if cache == "paged" else ""))
 
 
 def traffic_for(kernel, workload, decode_steps=None):
@@ -400,13 +401,14 @@ def main():
     args = parse()
     if args.ingest_mfma_counters:
         ingest_mfma_counters(args.ingest_mfma_counters,
-                             counter_key(args.workload, args.vision_only, args.cache, args.rho))
+                             counter_key(args.workload, args.vision_only, args.cache, args.rho,
+                                         args.lse_from_prefill))
         return
     if args.ingest_counters:
         from workloads import CONFIGS
         T = CONFIGS[args.workload].decode_steps if args.decode_steps is None else args.decode_steps
         ingest_counters(*args.ingest_counters,
-                        workload=counter_key(args.workload, args.vision_only, args.cache, args.rho),
+                        workload=counter_key(args.workload, args.vision_only, args.cache, args.rho, args.lse_from_prefill),
                         decode_steps=T)
         return
     if args.calibrate_copy:
@@ -492,6 +494,8 @@ def main():
         elif flush == "write":
             flush_buf.zero_()  # 512 MB of dirty lines, as a prefill that just wrote the cache leaves it
 
+    sched_now = [schedule]  # the schedule one_step runs (the one-sweep variant below switches it)
+
     def one_step(events=None, decode=True):
         names = []
 
@@ -504,7 +508,7 @@ def main():
 
         do_flush()  # outside the timed intervals
         mark("start")
-        sched = buf.evict(q_d, k_d, v_d, schedule=schedule, marks=mark, compact=not paged)
+        sched = buf.evict(q_d, k_d, v_d, schedule=sched_now[0], marks=mark, compact=not paged)
         if paged:
             bd.tgvkv_page_table(p, opts, buf.budgets, tot, max(T, 1), args.page_size, free_ids, table, used)
             mark("pages")
@@ -621,7 +625,8 @@ def main():
         ap = achieved_peak(kname)
         roofs[kname] = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                         "frac": round(gbs / HBM_PEAK_GBS, 4),
-                        "traffic": traffic_for(kname, counter_key(cfg.name, args.vision_only, args.cache, rho), T),
+                        "traffic": traffic_for(kname, counter_key(cfg.name, args.vision_only, args.cache, rho,
+                                                                   args.lse_from_prefill), T),
                         "kernel": kname, "alg_bytes_per_launch": int(alg[kname]), "bytes_kind": kinds[kname],
                         "avg_launch_ms": round(ms, 4),
                         "ms_per_step": round(ms * (T if kname == "decode" else 1), 4),
@@ -648,7 +653,7 @@ def main():
     logits = Ns * (Ns + 1) / 2 + Nq * (Ns + Nv) + Nq * (Nq + 1) / 2
     score_flops = 2.0 * B * L * H * D * logits
     score_ms = sum(v for k, v in stage_ms.items() if k in ("score",) + SCORE_KERNELS)
-    ckey = counter_key(cfg.name, args.vision_only, args.cache, rho)
+    ckey = counter_key(cfg.name, args.vision_only, args.cache, rho, args.lse_from_prefill)
     per_kernel = {}
     for kname in SCORE_KERNELS + ("score",):
         ms = stage_ms.get(kname, 0.0)
@@ -718,6 +723,22 @@ def main():
         "ceilings": ceilings,
         "wall_ms_per_step": round(main_run["wall"] / args.steps * 1e3, 3),
     }
+
+    # ---- the same inputs with every text row's normaliser taken from the prefill (one K sweep:
+    # text and vision scores and the TV mass in one pass, then the budgets), as a labelled variant
+    if sched == "two_step" and not args.no_depth_profile:
+        prefill_normalisers()
+        sched_now[0] = "lse_in"
+        lp = run(args.warmup, args.steps, decode=False)
+        sched_now[0] = schedule
+        line["normalisers_from_prefill"] = {
+            "value": round(B * N / (lp["evict_ms"] * 1e-3), 1), "unit": "tokens/s",
+            "evict_ms": round(lp["evict_ms"], 4), "evict_ms_spread": spread(lp["evict_per_step"], 4),
+            "evict_roofline": pass_roof(lp["evict_ms"]),
+            "stage_ms": {k: round(v, 4) for k, v in lp["stage_ms"].items()},
+            "note": "the text rows' log-sum-exp is given (as a prefill attention kernel returns it), "
+                    "produced outside the timed region by the library's own statistics sweep",
+        }
 
     # ---- the same workload with the depth profile of the text-to-vision attention (only the
     # question-row queries change), as a labelled variant beside the i.i.d. headline

@@ -125,8 +125,8 @@ ScoreWs score_workspace(const Shape& s, const RowPlan& rp, void* base) {
     size_t off = 0;
     ScoreWs w;
     char* b = static_cast<char*>(base);
-    w.vm = reinterpret_cast<float*>(b ? b + off : nullptr);
-    off = align_up(off + sizeof(float) * bl * s.H * s.Nq);
+    w.vm = reinterpret_cast<float*>(b ? b + off : nullptr);  // [vision splits][B*L*H][N_q] row masses
+    off = align_up(off + sizeof(float) * bl * s.H * s.Nq * (size_t)tgvkv::vision_splits(s, rp));
     w.colsum = reinterpret_cast<float*>(b ? b + off : nullptr);
     off = align_up(off + sizeof(float) * bl * s.H * s.Nt);
     w.vmh = reinterpret_cast<float*>(b ? b + off : nullptr);
@@ -239,7 +239,7 @@ tgvkv_status tgvkv_score(const tgvkv_problem* problem, const tgvkv_opts* opts, i
         if (e == hipSuccess)
             e = tgvkv::launch_score_vision(s, rp, q, kk, lse, w_txt, nullptr, vthr, w.part, w.vm, stream);
         if (e == hipSuccess) e = tgvkv::launch_score_vis_reduce(s, rp, w.part, nullptr, vthr, s_vis, stream);
-        if (e == hipSuccess) e = tgvkv::launch_score_mass(s, w.vm, w.vmh, tv_mass, stream);
+        if (e == hipSuccess) e = tgvkv::launch_score_mass(s, rp, w.vm, w.vmh, tv_mass, stream);
         return hip_status(e);
     }
     const bool both = (phases & TGVKV_SCORE_STATS) && (phases & TGVKV_SCORE_TEXT);

@@ -219,14 +219,23 @@ __global__ __launch_bounds__(kThreads) void score_fin_kernel(Shape s, const floa
 
 // Layer TV mass (Eq. (5)-(6)) from per-row vision masses, in the same order as the
 // two-sweep path: per head over question rows, then the mean over heads.
+// ws_vm holds one row-mass partial per share of the vision keys ([vsplit][B*L*H][N_q]); a
+// row's shares are added first, in share order.
 __global__ __launch_bounds__(kThreads) void score_mass_kernel(Shape s, const float* __restrict__ ws_vm,
                                                               float* __restrict__ ws_vmh,
-                                                              float* __restrict__ tv_mass) {
+                                                              float* __restrict__ tv_mass, int vsplit) {
     const int bl = blockIdx.x;
+    const size_t share = (size_t)s.B * s.L * s.H * s.Nq;
     for (int h = threadIdx.x; h < s.H; h += kThreads) {
         float a = 0.f;
-        if (s.Nv > 0)  // with no vision keys the vision sweep does not run and every mass is 0
-            for (int qi = 0; qi < s.Nq; ++qi) a += ws_vm[((size_t)bl * s.H + h) * s.Nq + qi];
+        if (s.Nv > 0) {  // with no vision keys the vision sweep does not run and every mass is 0
+            const float* vm = ws_vm + ((size_t)bl * s.H + h) * s.Nq;
+            for (int qi = 0; qi < s.Nq; ++qi) {
+                float r = vm[qi];
+                for (int sp = 1; sp < vsplit; ++sp) r += vm[sp * share + qi];
+                a += r;
+            }
+        }
         ws_vmh[(size_t)bl * s.H + h] = a;
     }
     __syncthreads();
@@ -302,7 +311,8 @@ __global__ __launch_bounds__(kThreads) void score_vision_kernel(Shape s, int row
                 for (int j = 0; j < 4; ++j) {
                     const int qj = (rb % QB) * 16 + (lane >> 4) * 4 + j;
                     if (rb < NB && qj < s.Nq)
-                        ws_vm[((size_t)bl * s.H + kvh * s.G + rb / QB) * s.Nq + qj] = rsum[sl][j];
+                        ws_vm[((size_t)sp * s.B * s.L * s.H + (size_t)bl * s.H + kvh * s.G + rb / QB) * s.Nq + qj] =
+                            rsum[sl][j];
                 }
             }
         }
@@ -456,16 +466,21 @@ hipError_t launch_score_fin(const Shape& s, const float* ws_colsum, const float*
     return hipGetLastError();
 }
 
+int vision_splits(const Shape& s, const RowPlan& rp) {
+    // With few (unit, row group) workgroups the vision keys are split over several: at the
+    // Qwen2-VL shape (896 units, 2 workgroups per CU) two splits balance the last round
+    // (805 -> 740 us); at 4096 units a split only adds prologues.  The mass-collecting variant
+    // writes one row-mass partial per share, which score_mass adds.
+    const long long units = (long long)s.B * s.L * s.Hkv * rp.rowgroups;
+    return units <= 0 ? 1 : (int)std::min<long long>(std::max<long long>(2048 / units, 1), 4);
+}
+
 hipError_t launch_score_vision(const Shape& s, const RowPlan& rp, const uint16_t* q_text, const uint16_t* k,
                                const float* lse, const float* w_txt, const int32_t* budgets,
                                int32_t vis_threshold, float* ws_part, float* ws_vm, hipStream_t st) {
     const bool mass = ws_vm != nullptr;
-    // With few (unit, row group) workgroups the vision keys are split over several: at the
-    // Qwen2-VL shape (896 units, 2 workgroups per CU) two splits balance the last round
-    // (805 -> 740 us); at 4096 units a split only adds prologues.  The mass-collecting variant
-    // keeps one range (its row sums would need a merge).
     const long long units = (long long)s.B * s.L * s.Hkv * rp.rowgroups;
-    const int vsplit = mass || units <= 0 ? 1 : (int)std::min<long long>(std::max<long long>(2048 / units, 1), 4);
+    const int vsplit = vision_splits(s, rp);
     const long long nblk = units * vsplit;
     if (nblk == 0 || s.Nv == 0) return hipSuccess;
     dim3 grid((unsigned)nblk), block(kThreads);
@@ -501,10 +516,12 @@ hipError_t launch_score_vision(const Shape& s, const RowPlan& rp, const uint16_t
     return hipGetLastError();
 }
 
-hipError_t launch_score_mass(const Shape& s, const float* ws_vm, float* ws_vmh, float* tv_mass, hipStream_t st) {
+hipError_t launch_score_mass(const Shape& s, const RowPlan& rp, const float* ws_vm, float* ws_vmh, float* tv_mass,
+                             hipStream_t st) {
     const long long nblk = (long long)s.B * s.L;
     if (nblk == 0) return hipSuccess;
-    hipLaunchKernelGGL(score_mass_kernel, dim3((unsigned)nblk), dim3(kThreads), 0, st, s, ws_vm, ws_vmh, tv_mass);
+    hipLaunchKernelGGL(score_mass_kernel, dim3((unsigned)nblk), dim3(kThreads), 0, st, s, ws_vm, ws_vmh, tv_mass,
+                       vision_splits(s, rp));
     return hipGetLastError();
 }
 

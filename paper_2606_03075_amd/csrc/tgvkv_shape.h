@@ -41,7 +41,11 @@ hipError_t launch_score_vision(const Shape& s, const RowPlan& rp, const uint16_t
                                const uint16_t* k, const float* lse, const float* w_txt,
                                const int32_t* budgets, int32_t vis_threshold, float* ws_part, float* ws_vm,
                                hipStream_t st);
-hipError_t launch_score_mass(const Shape& s, const float* ws_vm, float* ws_vmh, float* tv_mass, hipStream_t st);
+// Shares of the vision keys a unit's vision sweep is split over (the mass-collecting sweep
+// writes one row-mass partial per share).
+int vision_splits(const Shape& s, const RowPlan& rp);
+hipError_t launch_score_mass(const Shape& s, const RowPlan& rp, const float* ws_vm, float* ws_vmh, float* tv_mass,
+                             hipStream_t st);
 hipError_t launch_score_vis_reduce(const Shape& s, const RowPlan& rp, const float* ws_part,
                                    const int32_t* budgets, int32_t vis_threshold, float* s_vis,
                                    hipStream_t st);
