@@ -40,8 +40,8 @@ def log(*a):
 def parse():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llavanext")
     ap.add_argument("--rho", type=float, default=None, help="retention ratio (default: the workload's first)")
     ap.add_argument("--lse-from-prefill", action="store_true",
