@@ -95,8 +95,13 @@ def run_and_check(cfg, rho, head_mode=0, forced=(0, 0), steps=2, seed=0, skip_te
 
     if schedule == "lse_in":
         # the rows' normalisers a prefill kernel would return: here the fp64 oracle's, rounded to fp32
-        assert gen_seqs is None
-        lse = np.stack([np.stack([sc["lse"] for sc in oracle_seq(b)[0]]) for b in range(B)]).astype(np.float32)
+        # (computed once per generated sequence when the batch repeats generated sequences)
+        src = t["q_text"].src if gen_seqs is not None else list(range(B))
+        first = {}
+        for b in range(B):
+            first.setdefault(src[b], b)
+        lse = np.stack([np.stack([sc["lse"] for sc in oracle_seq(first[src[b]])[0]]) for b in range(B)])
+        lse = lse.astype(np.float32)
         buf.lse.copy_(torch.from_numpy(lse))
     sched = buf.evict(q_d, k_d, v_d, schedule=schedule if skip_text_only else "phases")
     log(f"  schedule {sched}")

@@ -55,6 +55,17 @@ def test_qwen2vl_video_full(lib, rho):
     _properties(buf, cfg)
 
 
+def test_qwen2vl_video_full_lse_in(lib):
+    """The one-sweep schedule (every text row's normaliser given, as a prefill kernel returns it)
+    at the full Qwen2-VL batch: the mass-collecting vision sweep runs split over two shares of the
+    vision keys there (896 units), and the TV masses, scores, budgets, sets and cache must still
+    match.  Sequences 0 and 7 are generated and checked; the batch repeats them."""
+    cfg = CONFIGS["qwen2vl_video"]
+    buf = run_and_check(cfg, cfg.rhos[0], steps=8, seed=0, check_seqs=[0, 7], decode_seqs=[0], gen_seqs=[0, 7],
+                        schedule="lse_in")
+    _properties(buf, cfg)
+
+
 @pytest.mark.parametrize("recipe", ["iid", "depth"])
 def test_stress13b_full(lib, recipe):
     """batch 16 x 40 layers x 40 heads, 35 + 2880 + 256 tokens, 5 % retention, 256 decode steps.
