@@ -94,7 +94,7 @@ def test_validation_before_any_launch(lib):
     # phases, null and misaligned pointers, workspace
     assert lib.tgvkv_score(ok, None, 0, fake, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
     assert lib.tgvkv_score(ok, None, 8, fake, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
-    # the persistent variant takes only ALL or STATS|TEXT, and no budgets
+    # bit 8 is not a phase (it was the removed persistent schedule's flag): with any phases, refused
     assert lib.tgvkv_score(ok, None, 8 | 4, fake, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
     assert lib.tgvkv_score(ok, None, 8 | 1, fake, fake, fake, fake, fake, fake, fake, None, fake, big, s) == -1
     assert lib.tgvkv_score(ok, None, 8 | 7, fake, fake, fake, fake, fake, fake, fake, fake, fake, big, s) == -1
