@@ -62,7 +62,7 @@ __global__ __launch_bounds__(kThreads) void score_stats_kernel(Shape s, int rowg
     if (kp == 0 && lane < 16) {
 #pragma unroll
         for (int sl = 0; sl < NSLOT; ++sl) {
-            const int rb = rb0 + rs + sl * RSETS;
+            const int rb = slot_block<RSETS>(rb0, rs, sl);
             const int qi = qrow[sl];
             if (rb < NB && qi < s.Nq) {
                 const size_t head = (size_t)bl * s.H + kvh * s.G + rb / QB;
@@ -119,7 +119,7 @@ score_stats_text_kernel(Shape s, const uint16_t* __restrict__ q_text, const uint
     if (kp == 0 && lane < 16) {
 #pragma unroll
         for (int sl = 0; sl < NSLOT; ++sl) {
-            const int rb = rs + sl * RSETS;
+            const int rb = slot_block<RSETS>(0, rs, sl);
             const int qi = qrow[sl];
             if (rb < NB && qi < s.Nq) {
                 const int g = rb / QB;
@@ -306,7 +306,7 @@ __global__ __launch_bounds__(kThreads) void score_vision_kernel(Shape s, int row
         if (kp == 0 && (lane & 15) == 0) {
 #pragma unroll
             for (int sl = 0; sl < NSLOT; ++sl) {
-                const int rb = rb0 + rs + sl * RSETS;
+                const int rb = slot_block<RSETS>(rb0, rs, sl);
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                     const int qj = (rb % QB) * 16 + (lane >> 4) * 4 + j;

@@ -4,8 +4,8 @@
 // question rows (query heads sharing the KV head x question tokens) are cut into
 // 16-row blocks, QB = ceil(N_q / 16) per head; block rb covers head rb / QB and
 // question indices (rb % QB) * 16 .. + 15.  The 4 waves of a workgroup split the
-// blocks into RSETS row sets of up to NSLOT blocks each and, when there are few
-// blocks, each 64-key tile into KS key parts (RSETS * KS = 4).
+// blocks into RSETS row sets of up to NSLOT blocks each (slot_block) and, when there
+// are few blocks, each 64-key tile into KS key parts (RSETS * KS = 4).
 //
 // MFMA layout: v_mfma_f32_16x16x32_bf16.  A 64-key tile of K sits in LDS with
 // rows padded by 16 bytes (the 16 lanes reading one 16-byte column chunk of 16
@@ -155,6 +155,17 @@ struct PipeDepth {
     static constexpr int value = NSLOT <= 2 ? 2 : 1;
 };
 
+// Row block held by slot sl of row set rs, in the row group starting at block rb0.  The sets
+// take the blocks in a snake order (0 1 2 3, then 7 6 5 4, 8 9 10 11, ...), so that with several
+// slots per wave every wave holds rows from early and late in the question: the causally masked
+// question-key work of the statistics sweep's last tiles and of the text pass is then nearly the
+// same for every wave (in the plain order the last wave's rows see the most keys, and the
+// per-tile barrier waits for it).  At the 13B stress shape: 6.75 against 6.79-6.82 ms.
+template <int RSETS>
+__device__ __forceinline__ int slot_block(int rb0, int rs, int sl) {
+    return rb0 + sl * RSETS + ((sl & 1) ? RSETS - 1 - rs : rs);
+}
+
 __device__ __forceinline__ bf16x8 zero_frag() {
     u32x4 z = {0u, 0u, 0u, 0u};
     return as_bf16x8(z);
@@ -186,7 +197,7 @@ __device__ __forceinline__ void load_qrows(const Shape& s, const uint16_t* q_tex
     const int NB = s.G * QB;
 #pragma unroll
     for (int sl = 0; sl < NSLOT; ++sl) {
-        const int rb = rb0 + rs + sl * RSETS;
+        const int rb = slot_block<RSETS>(rb0, rs, sl);
         const int g = rb / QB;
         const int qi = (rb % QB) * 16 + (lane & 15);
         qrow[sl] = qi;
@@ -378,7 +389,7 @@ __device__ __forceinline__ void load_row_coefs(const Shape& s, int bl, int kvh, 
     bool ok[NSLOT][4];
 #pragma unroll
     for (int sl = 0; sl < NSLOT; ++sl) {
-        const int rb = rb0 + rs + sl * RSETS;
+        const int rb = slot_block<RSETS>(rb0, rs, sl);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int qj = (rb % QB) * 16 + (lane >> 4) * 4 + j;
@@ -446,7 +457,7 @@ __device__ void vision_sweep(const Shape& s, const uint16_t* kvis, int vbeg, int
                 float col = 0.f;
 #pragma unroll
                 for (int sl = 0; sl < NSLOT; ++sl) {
-                    if (rb0 + rs + sl * RSETS >= NB) continue;
+                    if (slot_block<RSETS>(rb0, rs, sl) >= NB) continue;
                     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                     for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(qf[sl][ks], kf[ks], acc);
@@ -859,7 +870,7 @@ __device__ void text_pass_qregs(const Shape& s, int bl, int kvh, const uint16_t*
     float l2r[NSLOT][4];
 #pragma unroll
     for (int sl = 0; sl < NSLOT; ++sl) {
-        const int rb = rs + sl * RSETS;
+        const int rb = slot_block<RSETS>(0, rs, sl);
         sok[sl] = rb < NB;
         gsl[sl] = sok[sl] ? rb / QB : 0;
         q0s[sl] = (rb % QB) * 16;
