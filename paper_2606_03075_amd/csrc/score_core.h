@@ -454,6 +454,9 @@ __device__ void vision_sweep(const Shape& s, const uint16_t* kvis, int vbeg, int
                 bf16x8 kf[GG::KSTEPS];
                 load_kfrag<D>(kf, buf, kb, lane);
                 const int kcol = key0 + kb * 16 + (lane & 15);  // this lane's key (accumulator column)
+                // the last tile repeats the last key past vend (clamped loads): not a key, weight 0
+                // in the row sums (one multiply-add per probability, no per-element branch)
+                const float inr = kcol < vend ? 1.f : 0.f;
                 float col = 0.f;
 #pragma unroll
                 for (int sl = 0; sl < NSLOT; ++sl) {
@@ -465,8 +468,7 @@ __device__ void vision_sweep(const Shape& s, const uint16_t* kvis, int vbeg, int
                     for (int j = 0; j < 4; ++j) {
                         const float p = fast_exp2(acc[j] * s.scale2 - lse2[sl][j]);
                         col += coef[sl][j] * p;
-                        // the last tile repeats the last key past vend (clamped loads): not a key
-                        if (MASS && kcol < vend) rsum[sl][j] += p;
+                        if (MASS) rsum[sl][j] = __builtin_fmaf(p, inr, rsum[sl][j]);
                     }
                 }
                 col = sum_xor32(sum_xor16(col));
