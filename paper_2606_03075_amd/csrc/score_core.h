@@ -874,7 +874,7 @@ __device__ void text_pass_qregs(const Shape& s, int bl, int kvh, const uint16_t*
     for (int sl = 0; sl < NSLOT; ++sl) {
         const int rb = slot_block<RSETS>(0, rs, sl);
         sok[sl] = rb < NB;
-        gsl[sl] = sok[sl] ? rb / QB : 0;
+        gsl[sl] = sok[sl] ? rb / QB : sl > 0 ? gsl[sl - 1] : 0;
         q0s[sl] = (rb % QB) * 16;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -890,34 +890,38 @@ __device__ void text_pass_qregs(const Shape& s, int bl, int kvh, const uint16_t*
     };
     // question rows x one 16-key block kf of text keys, of which the first kn are keys; c0:
     // the block's first question-key index (causal: keys of later question tokens are masked),
-    // kSysBlock for system keys (visible to every question row); t0: the block's text index
+    // kSysBlock for system keys (visible to every question row); t0: the block's text index.
+    // Every slot is computed, with no per-slot branch (a slot past the last row block has
+    // normalisers +inf, so p = 0; keys past a row are masked by a select): per tile the loop
+    // then runs like the sweep's, where skipping the causally hidden blocks of a wave's slots
+    // (branches between a slot's MFMAs and its exponentials, and spills at the 168-register
+    // cap) had taken 29 of the pass's 39 us at the 13B stress shape.  The column sums of the
+    // slots of one query head go to one flush; a wave whose slots span two heads flushes at
+    // the change (wave-uniform).
     constexpr int kSysBlock = -(1 << 30);
     auto qrow_block = [&](const bf16x8 (&kf)[GG::KSTEPS], int c0, int t0, int kn) {
         float colacc = 0.f;
-        int gcur = -1;
+        int gcur = gsl[0];
 #pragma unroll
         for (int sl = 0; sl < NSLOT; ++sl) {
-            // wave-uniform: a slot past the last block, or whose rows all precede the block
-            if (!sok[sl] || c0 > q0s[sl] + 15) continue;
             f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(qf[sl][ks], kf[ks], acc);
-            const bool full = c0 + 15 <= q0s[sl];  // every key of the block precedes every row
+            const int lim = q0s[sl] + (lane >> 4) * 4 - c0 - (lane & 15);  // key visible to row j iff lim + j >= 0
             float col = 0.f;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const float p = fast_exp2(acc[j] * s.scale2 - l2r[sl][j]);
-                const bool vis = full || c0 + (lane & 15) <= q0s[sl] + (lane >> 4) * 4 + j;
-                col += vis ? p : 0.f;
+                col += lim + j >= 0 ? p : 0.f;
             }
-            if (gsl[sl] != gcur) {
-                if (gcur >= 0) flush(colacc, gcur, t0, kn);
+            if (sl > 0 && gsl[sl] != gcur) {
+                flush(colacc, gcur, t0, kn);
                 colacc = 0.f;
                 gcur = gsl[sl];
             }
             colacc += col;
         }
-        if (gcur >= 0) flush(colacc, gcur, t0, kn);
+        flush(colacc, gcur, t0, kn);
     };
 
     // 1. the system keys into the tiles (every load of a round issued before its stores);
@@ -1022,9 +1026,10 @@ __device__ void text_pass_qregs(const Shape& s, int bl, int kvh, const uint16_t*
     }
     __syncthreads();  // the tiles are free for the question keys
 
-    // 4. question rows x question keys, through the tile pipeline
+    // 4. question rows x question keys, through the tile pipeline (one tile in flight: the
+    //    pass is compute-paced here, and a second register tile would spill)
     const int qbeg = s.Ns + s.Nv;
-    tile_pipeline<D, 2>(
+    tile_pipeline<D, 1>(
         kbase, qbeg, s.N, tiles,
         [&](const char* buf, int key0, int) {
 #pragma unroll
