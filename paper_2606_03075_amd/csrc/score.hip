@@ -26,6 +26,10 @@
 // These kernels serve phase-by-phase calls (and the vision pass restricted to
 // layers whose budget reaches past the text).
 #include <algorithm>
+#include <map>
+#include <mutex>
+#include <tuple>
+#include <type_traits>
 
 #include "score_core.h"
 
@@ -247,6 +251,18 @@ __global__ __launch_bounds__(kThreads) void score_mass_kernel(Shape s, const flo
     }
 }
 
+// How the vision sweep's workgroups are dealt out: each (unit, row group) has vsplit shares
+// of its vision keys; workgroup b < nfull takes share b whole, and the shares after those are
+// each cut into `pieces` workgroups.  The cut shares are the last ones dispatched: they would
+// otherwise run as a partial last round whose few workgroups, one or two key tiles in flight
+// each, cannot keep HBM busy (at llavanext 4096 units over 768 resident workgroups leave 256
+// for a sixth round).
+struct VisionDeal {
+    int vsplit;
+    long long nfull;
+    int pieces;
+};
+
 template <int D, int NSLOT, int KS, bool MASS>
 __global__ __launch_bounds__(kThreads) void score_vision_kernel(Shape s, int rowgroups,
                                                                 const uint16_t* __restrict__ q_text,
@@ -257,14 +273,22 @@ __global__ __launch_bounds__(kThreads) void score_vision_kernel(Shape s, int row
                                                                 int vis_threshold,
                                                                 float* __restrict__ ws_part,
                                                                 float* __restrict__ ws_vm, int out_tiles,
-                                                                int vsplit) {
+                                                                VisionDeal deal) {
     constexpr int RSETS = 4 / KS;
     __shared__ __attribute__((aligned(16))) char tiles[2][Geo<D>::TILE_BYTES];
     __shared__ float red[2][RSETS][kTile];
     extern __shared__ float obuf[];  // out_tiles * kTile scores
-    int bid = blockIdx.x;
-    const int sp = bid % vsplit;  // this workgroup's share of the vision keys
-    bid /= vsplit;
+    const int vsplit = deal.vsplit;
+    long long sh = blockIdx.x;  // this workgroup's share of the vision keys, and its piece of it
+    int piece = 0, npieces = 1;
+    if (sh >= deal.nfull) {
+        const long long j = sh - deal.nfull;
+        sh = deal.nfull + j / deal.pieces;
+        piece = (int)(j % deal.pieces);
+        npieces = deal.pieces;
+    }
+    const int sp = (int)(sh % vsplit);
+    int bid = (int)(sh / vsplit);
     const int rg = bid % rowgroups;
     bid /= rowgroups;
     const int kvh = bid % s.Hkv;
@@ -295,8 +319,12 @@ __global__ __launch_bounds__(kThreads) void score_vision_kernel(Shape s, int row
     float* out = ws_part + (((size_t)bl * s.Hkv + kvh) * rowgroups + rg) * (size_t)s.Nv;
     float rsum[NSLOT][4];
     // every key's score is a sum over this workgroup's rows only, so the keys split freely
-    const int per_t = ((s.Nv + kTile - 1) / kTile + vsplit - 1) / vsplit;
-    const int vbeg = min(sp * per_t * kTile, s.Nv), vend = min(vbeg + per_t * kTile, s.Nv);
+    const int ntv = (s.Nv + kTile - 1) / kTile;
+    const int per_t = (ntv + vsplit - 1) / vsplit;
+    const int t0 = min(sp * per_t, ntv), t1 = min(t0 + per_t, ntv);
+    const int per_p = (t1 - t0 + npieces - 1) / npieces;
+    const int p0 = min(t0 + piece * per_p, t1), p1 = min(p0 + per_p, t1);
+    const int vbeg = min(p0 * kTile, s.Nv), vend = min(p1 * kTile, s.Nv);
     vision_sweep<D, NSLOT, KS, MASS>(s, kvis, vbeg, vend, qf, lse2, coef, rb0, NB, tiles, red, obuf, out_tiles, out,
                                      rsum);
     if (MASS) {
@@ -365,6 +393,54 @@ __global__ __launch_bounds__(kThreads) void score_vis_reduce_kernel(Shape s, int
         else if (rp.nslot == 4) hipLaunchKernelGGL((KERNEL<D, 4, 1, M>), __VA_ARGS__);                    \
         else hipLaunchKernelGGL((KERNEL<D, 6, 1, M>), __VA_ARGS__);                                       \
     } while (0)
+
+template <int N>
+using IC = std::integral_constant<int, N>;
+
+// Calls f(IC<D>, IC<NSLOT>, IC<KS>, IC<MASS>) for the score_vision_kernel variant that
+// launch_score_vision runs for row plan rp (NB row blocks per unit).
+template <typename F>
+void with_vision_variant(int d, bool mass, const RowPlan& rp, int NB, F&& f) {
+    auto plan = [&](auto dd, auto m) {
+        if (!decltype(m)::value && rp.nslot == 1 && rp.ks == 1) {
+            if (NB == 3) f(dd, IC<2>{}, IC<2>{}, m);
+            else if constexpr (!decltype(m)::value) f(dd, IC<4>{}, IC<4>{}, m);
+        } else if (rp.ks == 4) f(dd, IC<1>{}, IC<4>{}, m);
+        else if (rp.ks == 2 && rp.nslot == 1) f(dd, IC<1>{}, IC<2>{}, m);
+        else if (rp.ks == 2) f(dd, IC<2>{}, IC<2>{}, m);
+        else if (rp.nslot == 1) f(dd, IC<1>{}, IC<1>{}, m);
+        else if (rp.nslot == 2) f(dd, IC<2>{}, IC<1>{}, m);
+        else if (rp.nslot == 4) f(dd, IC<4>{}, IC<1>{}, m);
+        else f(dd, IC<6>{}, IC<1>{}, m);
+    };
+    auto with_d = [&](auto m) {
+        if (d == 128) plan(IC<128>{}, m);
+        else plan(IC<64>{}, m);
+    };
+    if (mass) with_d(IC<1>{});
+    else with_d(IC<0>{});
+}
+
+// Workgroups of `kernel` that the current device holds at once (its occupancy per CU times
+// the CU count), asked of the runtime once per device and kernel; 0 if it cannot tell.
+int resident_workgroups(const void* kernel, size_t dyn_lds) {
+    static std::mutex mu;
+    static std::map<std::tuple<int, const void*, size_t>, int> known;
+    int dev = 0;
+    if (kernel == nullptr || hipGetDevice(&dev) != hipSuccess) return 0;
+    const auto key = std::make_tuple(dev, kernel, dyn_lds);
+    std::lock_guard<std::mutex> lock(mu);
+    const auto it = known.find(key);
+    if (it != known.end()) return it->second;
+    int cus = 0, per_cu = 0, n = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, dyn_lds) == hipSuccess)
+        n = cus * per_cu;
+    else
+        (void)hipGetLastError();
+    known[key] = n;
+    return n;
+}
 
 }  // namespace
 
@@ -481,37 +557,55 @@ hipError_t launch_score_vision(const Shape& s, const RowPlan& rp, const uint16_t
     const bool mass = ws_vm != nullptr;
     const long long units = (long long)s.B * s.L * s.Hkv * rp.rowgroups;
     const int vsplit = vision_splits(s, rp);
-    const long long nblk = units * vsplit;
-    if (nblk == 0 || s.Nv == 0) return hipSuccess;
-    dim3 grid((unsigned)nblk), block(kThreads);
+    const long long nsh = units * vsplit;
+    if (nsh == 0 || s.Nv == 0) return hipSuccess;
     // a unit's scores are kept in LDS and written once at the end when they fit (no global
     // store among the key loads); otherwise in bursts of kOutTiles tiles
     const int ntiles = ((s.Nv + kTile - 1) / kTile + vsplit - 1) / vsplit;
     const int out_tiles = (!mass && ntiles * kTile * (int)sizeof(float) <= kWholeOutBytes) ? ntiles : kOutTiles;
     const size_t obytes = (size_t)out_tiles * kTile * sizeof(float);
+    // the kernel variant this plan runs, and how many of its workgroups the GPU holds at once
+    const int NB = s.G * ((s.Nq + 15) / 16);
+    const void* fn = nullptr;
+    with_vision_variant(s.D, mass, rp, NB, [&](auto d, auto ns, auto kss, auto m) {
+        fn = (const void*)&score_vision_kernel<decltype(d)::value, decltype(ns)::value, decltype(kss)::value,
+                                               decltype(m)::value != 0>;
+    });
+    // the shares that would make a partial last round are cut into pieces that fill it (each
+    // piece at least 4 key tiles); the mass-collecting sweep keeps one row-mass partial per share
+    VisionDeal deal{vsplit, nsh, 1};
+    const int slots = mass ? 0 : resident_workgroups(fn, obytes);
+    if (slots > 0 && nsh % slots != 0) {
+        const long long r = nsh % slots;
+        const int most = std::max(ntiles / 4, 1);
+        const int pieces = (int)std::min<long long>((slots + r - 1) / r, most);
+        if (pieces > 1) deal = VisionDeal{vsplit, nsh - r, pieces};
+    }
+    const long long nblk = deal.nfull + (nsh - deal.nfull) * deal.pieces;
+    dim3 grid((unsigned)nblk), block(kThreads);
     if (mass) {
-        if (s.D == 128) TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 128, true, rp, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles, vsplit);
-        else TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 64, true, rp, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles, vsplit);
+        if (s.D == 128) TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 128, true, rp, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles, deal);
+        else TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 64, true, rp, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles, deal);
     } else if (rp.nslot == 1 && rp.ks == 1 && (s.G * ((s.Nq + 15) / 16)) == 3) {
         // three 16-row blocks per unit: two slots over half of each key tile (same row groups);
         // at the LLaVA-1.5 shape 43 us against 46-48 us for the four-slot shape below
         const RowPlan r2{2, 2, rp.rowgroups};
         if (s.D == 128)
-            TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 128, false, r2, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles, vsplit);
+            TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 128, false, r2, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles, deal);
         else
-            TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 64, false, r2, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles, vsplit);
+            TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 64, false, r2, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles, deal);
     } else if (rp.nslot == 1 && rp.ks == 1) {
         // four 16-row blocks per unit: the vision sweep runs faster with every wave holding all
         // four blocks over a quarter of each key tile (same row groups, so the same partials)
         if (s.D == 128)
             hipLaunchKernelGGL((score_vision_kernel<128, 4, 4, false>), grid, block, obytes, st, s, rp.rowgroups,
-                               q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles, vsplit);
+                               q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles, deal);
         else
             hipLaunchKernelGGL((score_vision_kernel<64, 4, 4, false>), grid, block, obytes, st, s, rp.rowgroups,
-                               q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles, vsplit);
+                               q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles, deal);
     } else {
-        if (s.D == 128) TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 128, false, rp, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles, vsplit);
-        else TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 64, false, rp, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles, vsplit);
+        if (s.D == 128) TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 128, false, rp, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles, deal);
+        else TGVKV_ROWPLAN_DISPATCH_M(score_vision_kernel, 64, false, rp, grid, block, obytes, st, s, rp.rowgroups, q_text, k, lse, w_txt, budgets, vis_threshold, ws_part, ws_vm, out_tiles, deal);
     }
     return hipGetLastError();
 }
