@@ -445,6 +445,15 @@ __device__ void vision_sweep(const Shape& s, const uint16_t* kvis, int vbeg, int
 #pragma unroll
             for (int j = 0; j < 4; ++j) rsum[sl][j] = 0.f;
     }
+    // Without row masses a row's coefficient goes into its exponent: coef * 2^(x - lse2) =
+    // 2^(x - c2), c2 = lse2 - log2(coef) (+inf for a zero coefficient, so rows past N_q add 0).
+    // One per-row constant instead of two: at the Qwen2-VL shape's six slots the sweep's
+    // compute runs about 4 % faster (probe of the key-block code).
+    float c2[NSLOT][4];
+#pragma unroll
+    for (int sl = 0; sl < NSLOT; ++sl)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) c2[sl][j] = MASS ? 0.f : lse2[sl][j] - fast_log2(coef[sl][j]);
     tile_pipeline<D, PipeDepth<NSLOT>::value>(
         kvis, vbeg, vend, tiles,
         [&](const char* buf, int key0, int t) {
@@ -466,9 +475,13 @@ __device__ void vision_sweep(const Shape& s, const uint16_t* kvis, int vbeg, int
                     for (int ks = 0; ks < GG::KSTEPS; ++ks) acc = mfma16x16x32(qf[sl][ks], kf[ks], acc);
 #pragma unroll
                     for (int j = 0; j < 4; ++j) {
-                        const float p = fast_exp2(acc[j] * s.scale2 - lse2[sl][j]);
-                        col += coef[sl][j] * p;
-                        if (MASS) rsum[sl][j] = __builtin_fmaf(p, inr, rsum[sl][j]);
+                        if (MASS) {
+                            const float p = fast_exp2(acc[j] * s.scale2 - lse2[sl][j]);
+                            col += coef[sl][j] * p;
+                            rsum[sl][j] = __builtin_fmaf(p, inr, rsum[sl][j]);
+                        } else {
+                            col += fast_exp2(acc[j] * s.scale2 - c2[sl][j]);
+                        }
                     }
                 }
                 col = sum_xor32(sum_xor16(col));
