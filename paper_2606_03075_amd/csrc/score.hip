@@ -169,8 +169,11 @@ __global__ __launch_bounds__(kThreads) void score_text_kernel(Shape s, const uin
                                                               float* __restrict__ lse,
                                                               const float* __restrict__ ws_vm,
                                                               float* __restrict__ ws_colsum,
-                                                              float* __restrict__ ws_vmh, int lse_given) {
-    extern __shared__ float lse2s[];  // [G][N_t] row normalisers, base-2 units
+                                                              float* __restrict__ ws_vmh, int lse_given,
+                                                              long long kl_bytes) {
+    // [G][N_t] row normalisers, base-2 units; with kl_bytes > 0, then the staged text pass's
+    // LDS (text_pass_lds), 16-byte aligned
+    extern __shared__ float lse2s[];
     const int tid = threadIdx.x;
     const int kvh = blockIdx.x % s.Hkv;
     const int bl = blockIdx.x / s.Hkv;
@@ -178,6 +181,12 @@ __global__ __launch_bounds__(kThreads) void score_text_kernel(Shape s, const uin
     if (lse_given) {
         // every text row's normaliser comes from the caller (a prefill kernel's row log-sum-exp)
         for (int x = tid; x < s.G * s.Nt; x += kThreads) lse2s[x] = lse[head0 * s.Nt + x] * kLog2e;
+        if (kl_bytes > 0) {
+            __syncthreads();
+            char* kl = reinterpret_cast<char*>(lse2s) + ((size_t)s.G * s.Nt * sizeof(float) + 15) / 16 * 16;
+            text_pass_lds<D>(s, bl, kvh, q_text, k, lse, lse2s, kl, kl_bytes, ws_colsum, true);
+            return;
+        }
     } else {
         for (int x = tid; x < s.G * s.Nq; x += kThreads) {
             const int g = x / s.Nq, qi = x % s.Nq;
@@ -513,6 +522,24 @@ hipError_t launch_score_text(const Shape& s, const uint16_t* q_text, const uint1
     const long long nblk = (long long)s.B * s.L * s.Hkv;
     if (nblk == 0 || s.Nt == 0) return hipSuccess;
     if (lse_given) {
+        // the unit's text keys staged in LDS by one workgroup per unit (text_pass_lds), when
+        // they fit in one chunk beside the normalisers within 64 KB: against one wave per
+        // (unit, head, 16-key block) walking the row blocks from global memory, at llavanext
+        // 80 -> 20 us
+        const int TB = (s.Nt + 15) / 16;
+        const long long head = ((long long)s.G * s.Nt * 4 + 15) / 16 * 16;
+        const long long kl = (s.D == 128 ? text_part_bytes<128>(s.G, s.Nt) : text_part_bytes<64>(s.G, s.Nt)) +
+                             16LL * TB * (2 * s.D + 16);
+        if (s.Nt > 0 && head + kl <= 65536) {
+            const size_t lds = (size_t)(head + kl);
+            if (s.D == 128)
+                hipLaunchKernelGGL(score_text_kernel<128>, dim3((unsigned)nblk), dim3(kThreads), lds, st, s, q_text,
+                                   k, lse, ws_vm, ws_colsum, ws_vmh, 1, kl);
+            else
+                hipLaunchKernelGGL(score_text_kernel<64>, dim3((unsigned)nblk), dim3(kThreads), lds, st, s, q_text,
+                                   k, lse, ws_vm, ws_colsum, ws_vmh, 1, kl);
+            return hipGetLastError();
+        }
         const long long items = nblk * s.G * ((s.Nt + 15) / 16);
         if (s.D == 128)
             hipLaunchKernelGGL(score_text_cols_kernel<128>, dim3((unsigned)items), dim3(64), 0, st, s, q_text, k, lse,
@@ -526,10 +553,10 @@ hipError_t launch_score_text(const Shape& s, const uint16_t* q_text, const uint1
     const size_t lds = sizeof(float) * (size_t)s.G * s.Nt;
     if (s.D == 128)
         hipLaunchKernelGGL(score_text_kernel<128>, grid, block, lds, st, s, q_text, k, lse, ws_vm, ws_colsum, ws_vmh,
-                           (int)lse_given);
+                           (int)lse_given, 0LL);
     else
         hipLaunchKernelGGL(score_text_kernel<64>, grid, block, lds, st, s, q_text, k, lse, ws_vm, ws_colsum, ws_vmh,
-                           (int)lse_given);
+                           (int)lse_given, 0LL);
     return hipGetLastError();
 }
 

@@ -677,12 +677,13 @@ __host__ __device__ constexpr bool text_lds_fits(int G, int Ns, int Nt, long lon
 // Column sums: per (row block, key block) the 16 rows' probabilities are summed across
 // the lane groups and added to the wave's own LDS partial for those keys; the four
 // waves' partials are then added in wave order.  lse2s holds [G][N_t] base-2
-// normalisers (the question rows' on entry); kl points at kl_bytes of 16-byte aligned
-// LDS with text_lds_fits<D>(G, N_s, N_t, kl_bytes).
+// normalisers (the question rows' on entry; every row's with lse_given, and then the
+// system rows' are not computed and lse is not written); kl points at kl_bytes of 16-byte
+// aligned LDS with text_lds_fits<D>(G, N_s, N_t, kl_bytes).
 template <int D>
 __device__ void text_pass_lds(const Shape& s, int bl, int kvh, const uint16_t* __restrict__ q_text,
                               const uint16_t* __restrict__ k, float* __restrict__ lse, float* lse2s, char* kl,
-                              long long kl_bytes, float* __restrict__ ws_colsum) {
+                              long long kl_bytes, float* __restrict__ ws_colsum, bool lse_given = false) {
     using GG = Geo<D>;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const size_t head0 = (size_t)bl * s.H + kvh * s.G;
@@ -692,7 +693,7 @@ __device__ void text_pass_lds(const Shape& s, int bl, int kvh, const uint16_t* _
     float* part = reinterpret_cast<float*>(kl);                   // [4 waves][G][TK]
     char* kst = kl + text_part_bytes<D>(s.G, s.Nt);               // staged key blocks
     const int KC = min(text_chunk_blocks<D>(s.G, s.Nt, kl_bytes), TB);
-    const int SB = (s.Ns + 15) >> 4;
+    const int SB = lse_given ? 0 : (s.Ns + 15) >> 4;              // system-row blocks to normalise
 
     const int koff = (lane >> 4) * 8;
     auto load_q = [&](bf16x8 (&f)[GG::KSTEPS], int g, int row) {
