@@ -522,15 +522,18 @@ hipError_t launch_score_text(const Shape& s, const uint16_t* q_text, const uint1
     const long long nblk = (long long)s.B * s.L * s.Hkv;
     if (nblk == 0 || s.Nt == 0) return hipSuccess;
     if (lse_given) {
-        // the unit's text keys staged in LDS by one workgroup per unit (text_pass_lds), when
-        // they fit in one chunk beside the normalisers within 64 KB: against one wave per
-        // (unit, head, 16-key block) walking the row blocks from global memory, at llavanext
-        // 80 -> 20 us
+        // the unit's text keys staged in LDS by one workgroup per unit (text_pass_lds; in
+        // chunks of key blocks when they do not all fit beside the normalisers within 64 KB):
+        // against one wave per (unit, head, 16-key block) walking the row blocks from global
+        // memory, at llavanext 80 -> 20 us
         const int TB = (s.Nt + 15) / 16;
         const long long head = ((long long)s.G * s.Nt * 4 + 15) / 16 * 16;
-        const long long kl = (s.D == 128 ? text_part_bytes<128>(s.G, s.Nt) : text_part_bytes<64>(s.G, s.Nt)) +
-                             16LL * TB * (2 * s.D + 16);
-        if (s.Nt > 0 && head + kl <= 65536) {
+        const long long kl = std::min<long long>(
+            (s.D == 128 ? text_part_bytes<128>(s.G, s.Nt) : text_part_bytes<64>(s.G, s.Nt)) +
+                16LL * TB * (2 * s.D + 16),
+            65536 - head);
+        const bool fits = s.D == 128 ? text_lds_fits<128>(s.G, 0, s.Nt, kl) : text_lds_fits<64>(s.G, 0, s.Nt, kl);
+        if (s.Nt > 0 && kl > 0 && fits) {
             const size_t lds = (size_t)(head + kl);
             if (s.D == 128)
                 hipLaunchKernelGGL(score_text_kernel<128>, dim3((unsigned)nblk), dim3(kThreads), lds, st, s, q_text,

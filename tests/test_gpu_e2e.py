@@ -268,6 +268,15 @@ def test_lse_in_shapes(lib):
                                 n_vis=90, n_qst=17), 0.25, steps=2, schedule="lse_in")
 
 
+def test_lse_in_long_text(lib):
+    # text keys staged in two chunks (they do not fit beside the normalisers in 64 KB of LDS):
+    # GQA with 320 text tokens, and one head per KV head with the 13B shape's 291
+    run_and_check(custom_config(name="lt2", batch=1, layers=2, heads_q=4, heads_kv=2, head_dim=128, n_sys=40,
+                                n_vis=300, n_qst=280), 0.3, steps=2, seed=9, schedule="lse_in")
+    run_and_check(custom_config(name="lt1", batch=1, layers=2, heads_q=2, heads_kv=2, head_dim=128, n_sys=35,
+                                n_vis=200, n_qst=256), 0.2, steps=2, seed=10, schedule="lse_in")
+
+
 def test_lse_in_llava15(lib):
     run_and_check(CONFIGS["llava15"], 0.1, steps=4, seed=0, schedule="lse_in")
 
