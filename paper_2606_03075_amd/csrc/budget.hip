@@ -27,6 +27,33 @@ namespace {
 constexpr int kMaxLayers = 512;
 constexpr int kThreads = 256;
 
+// For every layer l, the number of layers j that precede it in a strict order (prec(j, l)).
+// The L x L comparisons are spread over the workgroup: each layer's j range in nch chunks,
+// whose counts part[] holds until they are added in chunk order (integers, so exact).
+// emit(l, count) runs on thread l % kThreads.  Every thread must call it (a barrier inside).
+template <class Prec, class Emit>
+__device__ void rank_layers(int L, int* part, Prec prec, Emit emit) {
+    const int tid = threadIdx.x;
+    const int nch = L <= kThreads / 2 ? kThreads / max(L, 1) : 1;
+    const int per = (L + nch - 1) / nch;
+    for (int t = tid; t < nch * L; t += kThreads) {
+        const int l = t % L, c = t / L;
+        const int j1 = min(L, (c + 1) * per);
+        int n = 0;
+        for (int j = c * per; j < j1; ++j) n += prec(j, l);
+        if (nch == 1) emit(l, n);
+        else part[t] = n;  // t < nch * L <= kThreads
+    }
+    if (nch > 1) {
+        __syncthreads();
+        for (int l = tid; l < L; l += kThreads) {
+            int n = 0;
+            for (int c = 0; c < nch; ++c) n += part[c * L + l];
+            emit(l, n);
+        }
+    }
+}
+
 __global__ __launch_bounds__(kThreads) void budget_kernel(Shape s, const float* __restrict__ tv_mass, long long total,
                                                           int cap_tokens, int add, int reserve, int n_forced,
                                                           int32_t* __restrict__ budgets,
@@ -77,10 +104,12 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(Shape s, const float* 
     __shared__ int sh_over;
     while (n_active > 0) {
         if (tid == 0) {
+            // a capped layer's share is 0 (set when it is capped): adding +0.0 leaves the bits
+            // of the sum as they are (it starts at +0.0 and every share is >= 0), and with no
+            // test per layer the loads of a group of layers issue together
             double Fa = 0.0;
 #pragma unroll 8
-            for (int l = 0; l < L; ++l)
-                if (active[l]) Fa += f[l];
+            for (int l = 0; l < L; ++l) Fa += f[l];
             sh_sum = Fa;
             sh_over = 0;
         }
@@ -102,6 +131,7 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(Shape s, const float* 
             if (active[l] && x[l] > capd) {
                 x[l] = capd;
                 active[l] = 0;
+                f[l] = 0.0;
             }
         }
         // remaining and cap are integers below 2^53: the subtraction is exact in any order
@@ -112,42 +142,39 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(Shape s, const float* 
 
     // x becomes the fractional part of each layer still below the cap, -1 for the others
     // (fractions lie in [0, 1), so -1 ranks below every eligible layer and ties none)
-    int part = 0;
+    long long part = 0;
     for (int l = tid; l < L; l += kThreads) {
         const double fl = floor(x[l]);
         long long base = (long long)fl;
         if (base > cap) base = cap;
         bcount[l] = F + base;
         x[l] = F + base < N ? x[l] - fl : -1.0;
-        part += (int)base;
+        part += base;
     }
-    __shared__ long long sh_base;
-    if (tid == 0) sh_base = 0;
+    // the floors' sum (integers, exact in any order): per wave by shuffles, then the wave sums
+    __shared__ long long wpart[kThreads / 64];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) part += shfl_xor(part, o);
+    if ((tid & 63) == 0) wpart[tid >> 6] = part;
     __syncthreads();
-    atomicAdd(reinterpret_cast<unsigned long long*>(&sh_base), (unsigned long long)part);
-    __syncthreads();
-    const long long r = total - ((long long)L * F + sh_base);
+    long long base_sum = 0;
+#pragma unroll
+    for (int w = 0; w < kThreads / 64; ++w) base_sum += wpart[w];
+    const long long r = total - ((long long)L * F + base_sum);
 
     // +1 to the r eligible layers ranked first by (fraction desc, layer asc); every rank is
     // taken before any count changes
     __shared__ int cnt[kMaxLayers];
-    for (int l = tid; l < L; l += kThreads) {
-        const double fr = x[l];
-        int rank = 0;
-#pragma unroll 8
-        for (int j = 0; j < L; ++j) rank += (x[j] > fr) || (x[j] == fr && j < l);
-        cnt[l] = (int)bcount[l] + (fr >= 0.0 && rank < r ? 1 : 0);
-    }
+    __shared__ int rank_part[kThreads];
+    rank_layers(
+        L, rank_part, [&](int j, int l) { return (x[j] > x[l]) || (x[j] == x[l] && j < l) ? 1 : 0; },
+        [&](int l, int rank) { cnt[l] = (int)bcount[l] + (x[l] >= 0.0 && rank < r ? 1 : 0); });
     __syncthreads();
 
     if (unit_order != nullptr) {
-        for (int l = tid; l < L; l += kThreads) {
-            const int c = cnt[l];
-            int rank = 0;
-#pragma unroll 8
-            for (int j = 0; j < L; ++j) rank += (cnt[j] > c) || (cnt[j] == c && j < l);
-            unit_order[(size_t)rank * s.B + b] = b * L + l;
-        }
+        rank_layers(
+            L, rank_part, [&](int j, int l) { return (cnt[j] > cnt[l]) || (cnt[j] == cnt[l] && j < l) ? 1 : 0; },
+            [&](int l, int rank) { unit_order[(size_t)rank * s.B + b] = b * L + l; });
     }
 
     // budgets and the two offset tables: prefix sums of the per-layer counts (integers, so
