@@ -7,9 +7,10 @@
 // 32-bit keys (4 passes of 8 bits with an LDS histogram; the digit holding the
 // k-th key is found by a wave-wide scan of the histogram), which yields the k-th
 // largest key and how many of its ties to take; ties go to the lower position.
-// One ordered pass over the positions, 1024 at a time, then emits the retained
-// positions already in ascending order, with no sort: within a pass the ranks of
-// ties and of kept positions come from wave ballots and per-wave totals in LDS.
+// The retained positions are then emitted already in ascending order, with no sort:
+// each thread takes a contiguous chunk of positions, one workgroup scan of the chunks'
+// (tie, other kept) counts gives every thread the rank of its first tie and the output
+// slot of its first kept position, and a second walk over the chunk writes them.
 // The workgroup has 1024 threads: the work is a few latency-bound rounds per
 // (sequence, layer, group), and there are few such units.  Without TPR (an ablation of Table 5)
 // all non-forced positions compete on one scale: text by s^T, vision by s^V times
@@ -92,26 +93,6 @@ __device__ void find_digit(const int* hist, int kr, uint32_t* sel) {
     }
 }
 
-// Prefix counts of a per-thread flag in thread order for one round: returns the
-// number of set flags in lower threads of the workgroup; *total gets the round's
-// count.  part holds kWaves ints (one buffer per call in flight).
-__device__ __forceinline__ int round_prefix(bool flag, int* part, int* total) {
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const unsigned long long m = __ballot(flag);
-    const int below = __popcll(m & ((1ull << lane) - 1ull));
-    if (lane == 0) part[wave] = __popcll(m);
-    __syncthreads();
-    int before = 0, all = 0;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-        const int t = part[w];
-        before += w < wave ? t : 0;
-        all += t;
-    }
-    *total = all;
-    return before + below;
-}
-
 template <bool LDS_KEYS>
 __global__ __launch_bounds__(kThreads) void select_kernel(Shape s, const float* __restrict__ s_vis,
                                                           const float* __restrict__ s_txt,
@@ -119,7 +100,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(Shape s, const float* 
                                                           const int64_t* __restrict__ idx_off,
                                                           int32_t* __restrict__ idx) {
     __shared__ int hist[256];
-    __shared__ int part[2][2][kWaves];
+    __shared__ int wtot[kWaves][2];
     __shared__ uint32_t sel[2];
     __shared__ uint32_t keys[LDS_KEYS ? kLdsKeys : 1];
     const int tid = threadIdx.x;
@@ -186,24 +167,54 @@ __global__ __launch_bounds__(kThreads) void select_kernel(Shape s, const float* 
         take_ties = kr;
     }
 
-    // ordered emission, kThreads positions per round: a tie is kept while its rank among the
-    // ties (in position order) is below take_ties; kept positions are written in order
-    int ties_before = 0, kept_before = 0;
-    const int rounds = (s.N + kThreads - 1) / kThreads;
-    for (int r = 0; r < rounds; ++r) {
-        const int p = r * kThreads + tid;
-        const bool valid = p < s.N;
-        const uint32_t key = valid ? key_at(p) : kNotCand;
-        const bool outright = valid && c.kept_outright(p);
-        const bool cand = !outright && key != kNotCand && valid && c.cand(p);
-        const bool tie = cand && key == thr;
-        int round_ties, round_kept;
-        const int tie_rank = ties_before + round_prefix(tie, part[r & 1][0], &round_ties);
-        const bool keep = outright || (cand && key > thr) || (tie && tie_rank < take_ties);
-        const int pos = kept_before + round_prefix(keep, part[r & 1][1], &round_kept);
+    // ordered emission.  A tie is kept while its rank among the ties (in position order) is
+    // below take_ties, so the kept ties before a position are min(take_ties, ties before it).
+    // Each wave owns a contiguous run of 64-position groups.  It counts its ties and its other
+    // kept positions (ballots only); one barrier, and every wave adds the counts of the waves
+    // before it; then it walks its groups again, ranking each group's ties and kept positions
+    // by ballots, and writes the kept positions in order.
+    const int lane = tid & 63, wave = tid >> 6;
+    const unsigned long long below = (1ull << lane) - 1ull;
+    const int ngrp = (s.N + 63) >> 6;
+    const int gpw = (ngrp + kWaves - 1) / kWaves;
+    const int g0 = min(wave * gpw, ngrp), g1 = min(g0 + gpw, ngrp);
+    auto classify = [&](int p, bool& tie) {  // kept outright or above the threshold; tie
+        tie = false;
+        if (p >= s.N) return false;
+        const uint32_t key = key_at(p);
+        const bool outright = c.kept_outright(p);
+        const bool cand = !outright && key != kNotCand && c.cand(p);
+        tie = cand && key == thr;
+        return outright || (cand && key > thr);
+    };
+    int nt = 0, nk = 0;  // uniform over the wave
+    for (int gq = g0; gq < g1; ++gq) {
+        bool tie;
+        const bool other = classify(gq * 64 + lane, tie);
+        nt += __popcll(__ballot(tie));
+        nk += __popcll(__ballot(other));
+    }
+    if (lane == 0) {
+        wtot[wave][0] = nt;
+        wtot[wave][1] = nk;
+    }
+    __syncthreads();
+    int tb = 0, ob = 0;  // ties and other kept positions before this wave's run
+    for (int w = 0; w < wave; ++w) {
+        tb += wtot[w][0];
+        ob += wtot[w][1];
+    }
+    for (int gq = g0; gq < g1; ++gq) {
+        const int p = gq * 64 + lane;
+        bool tie;
+        const bool other = classify(p, tie);
+        const unsigned long long tm = __ballot(tie);
+        const bool keep = other || (tie && tb + __popcll(tm & below) < take_ties);
+        const unsigned long long km = __ballot(keep);
+        const int pos = ob + min(take_ties, tb) + __popcll(km & below);
         if (keep && pos < bgt) out[pos] = p;
-        ties_before += round_ties;
-        kept_before += round_kept;
+        tb += __popcll(tm);
+        ob += __popcll(__ballot(other));
     }
 }
 
