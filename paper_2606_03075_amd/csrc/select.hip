@@ -8,9 +8,9 @@
 // k-th key is found by a wave-wide scan of the histogram), which yields the k-th
 // largest key and how many of its ties to take; ties go to the lower position.
 // The retained positions are then emitted already in ascending order, with no sort:
-// each thread takes a contiguous chunk of positions, one workgroup scan of the chunks'
-// (tie, other kept) counts gives every thread the rank of its first tie and the output
-// slot of its first kept position, and a second walk over the chunk writes them.
+// each wave takes a contiguous run of 64-position groups, wave ballots count and rank
+// the ties and the kept positions, and the waves' counts, added across one barrier, give
+// each run the rank of its first tie and the output slot of its first kept position.
 // The workgroup has 1024 threads: the work is a few latency-bound rounds per
 // (sequence, layer, group), and there are few such units.  Without TPR (an ablation of Table 5)
 // all non-forced positions compete on one scale: text by s^T, vision by s^V times
