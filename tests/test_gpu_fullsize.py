@@ -66,6 +66,17 @@ def test_qwen2vl_video_full_lse_in(lib):
     _properties(buf, cfg)
 
 
+def test_llavanext_full_lse_in(lib):
+    """The one-sweep schedule at the benchmark's LLaVA-NeXT batch (4096 units, one row slot per
+    wave in the mass-collecting vision sweep, the unit's text keys staged in LDS for the text
+    pass): TV masses, scores, budgets, sets and cache against the oracle.  Sequences 0 and 3 are
+    generated and checked; the batch repeats them."""
+    cfg = CONFIGS["llavanext"]
+    buf = run_and_check(cfg, cfg.rhos[0], steps=8, seed=0, check_seqs=[0, 3], decode_seqs=[0], gen_seqs=[0, 3],
+                        schedule="lse_in")
+    _properties(buf, cfg)
+
+
 @pytest.mark.parametrize("recipe", ["iid", "depth"])
 def test_stress13b_full(lib, recipe):
     """batch 16 x 40 layers x 40 heads, 35 + 2880 + 256 tokens, 5 % retention, 256 decode steps.
