@@ -77,6 +77,17 @@ def test_llavanext_full_lse_in(lib):
     _properties(buf, cfg)
 
 
+def test_llavanext_full_vision_only(lib):
+    """Vision-only eviction (App. B.3) at the benchmark's LLaVA-NeXT batch: every layer keeps all
+    its text and a TVB share of 5 % of the vision tokens, so compaction and decode carry more rows.
+    Sequences 0 and 3 are generated and checked; the batch repeats them."""
+    cfg = CONFIGS["llavanext"]
+    buf = run_and_check(cfg, cfg.rhos[0], steps=8, seed=0, check_seqs=[0, 3], decode_seqs=[0], gen_seqs=[0, 3],
+                        vision_only=True)
+    budgets = buf.budgets.cpu().numpy()
+    assert np.all(budgets >= cfg.n_text)  # all text kept in every layer
+
+
 @pytest.mark.parametrize("recipe", ["iid", "depth"])
 def test_stress13b_full(lib, recipe):
     """batch 16 x 40 layers x 40 heads, 35 + 2880 + 256 tokens, 5 % retention, 256 decode steps.
