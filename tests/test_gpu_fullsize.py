@@ -88,6 +88,15 @@ def test_llavanext_full_vision_only(lib):
     assert np.all(budgets >= cfg.n_text)  # all text kept in every layer
 
 
+def test_llavanext_full_no_tpr(lib):
+    """Text and vision ranked together (TPR off, an ablation of Table 5) at the benchmark's
+    LLaVA-NeXT batch: every layer needs its vision scores, and the joint top-k runs over all
+    2979 positions.  Sequences 0 and 3 are generated and checked; the batch repeats them."""
+    cfg = CONFIGS["llavanext"]
+    run_and_check(cfg, cfg.rhos[0], steps=4, seed=0, check_seqs=[0, 3], decode_seqs=[0], gen_seqs=[0, 3],
+                  joint_rank=True)
+
+
 @pytest.mark.parametrize("recipe", ["iid", "depth"])
 def test_stress13b_full(lib, recipe):
     """batch 16 x 40 layers x 40 heads, 35 + 2880 + 256 tokens, 5 % retention, 256 decode steps.
